@@ -1,0 +1,190 @@
+/*
+ * boost_cap.h -- C-ABI of the tiered-memory (HBM + pinned host) decode path.
+ *
+ * Method: BOOST, "Concurrent Access to Host Memory and HBM to Accelerate LLM
+ * Inference".  Weights are placed page by page on two tiers by modulo page
+ * placement (MPP); the KV pool is split linearly between the tiers with KV
+ * heads outermost and handed out by a wave-aware allocator (DSR); hand-written
+ * CDNA4 kernels read every operand through a device page table so that each
+ * workgroup streams from exactly one tier.
+ *
+ * Conventions
+ *   - Every call returns 0 (BOOST_OK) or a negative BOOST_E* code; nothing
+ *     throws across the ABI.  boost_last_error() gives a message for the last
+ *     failing call of the calling thread.
+ *   - A "page" is 2 MiB (BOOST_PAGE_BYTES), the GPU page size the paper places
+ *     (§1, §4.4).  Tier codes: BOOST_TIER_HBM = 0, BOOST_TIER_HOST = 1.
+ *   - Device pointers are plain addresses in the current HIP device's address
+ *     space; `stream` is a hipStream_t passed as void* (NULL = default stream).
+ *   - The library owns placed tensors, KV pools and their page tables and
+ *     frees them in *_free / *_destroy.  The caller owns activations, queries,
+ *     outputs, block tables, context lengths and streams.
+ *   - Decode calls (boost_decode_gemv, boost_kv_write, boost_paged_attn_decode)
+ *     are asynchronous on `stream`, never synchronise and never allocate; the
+ *     first call on a tensor or pool may be made inside HIP graph capture.
+ *     Two decode calls that use the same tensor or pool must be ordered on one
+ *     stream (they share the tensor's split-row scratch).
+ *   - Allocator calls (boost_kv_alloc / boost_kv_free) are CPU-only
+ *     bookkeeping and are not thread-safe: one scheduler thread per pool.
+ */
+#ifndef BOOST_CAP_H
+#define BOOST_CAP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define BOOST_OK 0
+#define BOOST_EINVAL (-22) /* bad argument (null, zero size, shape, range)    */
+#define BOOST_ENOMEM (-12) /* allocation or HBM budget failure                */
+#define BOOST_EAGAIN (-11) /* KV pool cannot serve the request now (§4.3)     */
+#define BOOST_ENODEV (-19) /* call needs a device but the context is plan-only */
+#define BOOST_EHIP (-5)    /* a HIP runtime call failed                       */
+
+#define BOOST_TIER_HBM 0
+#define BOOST_TIER_HOST 1
+
+#define BOOST_DTYPE_F32 0
+#define BOOST_DTYPE_BF16 1
+
+#define BOOST_PAGE_BYTES (2ull * 1024ull * 1024ull)
+
+typedef struct boost_ctx boost_ctx;
+typedef struct boost_tensor boost_tensor;
+typedef struct boost_kv_pool boost_kv_pool;
+
+/* Message of the calling thread's last failing call ("" if none). */
+const char *boost_last_error(void);
+
+/* ABI version (major * 100 + minor). */
+int boost_version(void);
+
+/* ------------------------------------------------------------------ context */
+
+/* Open a context on HIP device `device` (>= 0), or a plan-only context with
+ * device = -1: plan-only contexts serve the placement planner and the KV
+ * allocator bookkeeping and return BOOST_ENODEV from every call that touches
+ * a GPU.  *out is owned by the caller and released with boost_shutdown.
+ * Errors: EINVAL (null out, bad device), EHIP. */
+int boost_init(int device, boost_ctx **out);
+int boost_shutdown(boost_ctx *ctx);
+
+/* Device facts: compute units and HIP device id (-1 when plan-only). */
+int boost_ctx_info(const boost_ctx *ctx, int *device, int *n_cu);
+
+/* Host backing of host-tier pages: 1 = coherent (fine-grained, uncached on
+ * the GPU; default), 0 = non-coherent.  Affects pages placed afterwards. */
+int boost_set_host_coherent(boost_ctx *ctx, int coherent);
+
+/* ------------------------------------------------------- a0: calibration */
+
+/* Measure alpha (§2.3: host read bandwidth over HBM read bandwidth; the paper
+ * measures each tier's peak separately, §5.1).  One streaming-read kernel
+ * reads a device buffer of `hbm_bytes` and a pinned, device-mapped host buffer
+ * of `host_bytes` (both allocated and freed inside the call, so this call
+ * synchronises and must not be captured), `iters` timed passes each after one
+ * warm-up pass; the best grid of a small sweep is kept for each tier.
+ * Outputs (any may be NULL): GB/s (1e9 B/s) of each tier and alpha.
+ * Errors: EINVAL (sizes < 64 MiB, iters < 1), ENODEV, ENOMEM, EHIP. */
+int boost_calibrate(boost_ctx *ctx, uint64_t hbm_bytes, uint64_t host_bytes,
+                    int iters, double *hbm_gbps, double *host_gbps,
+                    double *alpha);
+
+/* Read bandwidth (GB/s) of one streaming pass over `bytes` at device address
+ * `src` with `grid` workgroups of 256 lanes, timed over `iters` passes on the
+ * default stream (synchronises).  Used by calibration and tier probes.
+ * Errors: EINVAL (null, bytes not a multiple of 4 KiB, grid < 1), ENODEV, EHIP. */
+int boost_stream_read_gbps(boost_ctx *ctx, const void *src, uint64_t bytes,
+                           int grid, int iters, double *gbps);
+
+/* C1: modulus M = K + 1 with K = ceil(1/alpha) (§3.1 modulo placement, §4.4
+ * ceil rule keeping the host share at or below alpha).  alpha in (0, 1].
+ * Errors: EINVAL. */
+int boost_modulus_from_alpha(double alpha, uint32_t *M);
+
+/* ----------------------------------------------------- a1: weight placement */
+
+/* Superpage size in pages, lcm(footprint, page) / page (§3.2, §4.4); 1 when
+ * footprint is 0. Errors: EINVAL (null). */
+int boost_superpage_pages(uint64_t footprint_bytes, uint32_t *S);
+
+/* C2: modulo page placement of one tensor of `bytes` bytes (§3.1, §4.4):
+ * n = ceil(bytes / 2 MiB) pages; superpage j = pages [jS, (j+1)S); superpage j
+ * is on host iff j mod M == M - 1.  The phase restarts for every tensor
+ * (§3.1), so a tensor with fewer than M superpages has no host page.
+ * Writes min(n, tier_cap) tier codes to tier_out (may be NULL) and n to
+ * *n_pages.  Pure CPU.  Errors: EINVAL (bytes 0, M < 2, null n_pages). */
+int boost_plan_mpp(uint64_t bytes, uint32_t M, uint64_t footprint_bytes,
+                   uint8_t *tier_out, uint64_t tier_cap, uint64_t *n_pages);
+
+/* C3: modulus under an HBM budget.  The paper always places about an alpha
+ * share on host; when the weights exceed a budget we keep the modulo rule and
+ * take the largest M in [2, M_alpha] whose HBM-resident pages (whole pages,
+ * every tensor placed on its own) fit in hbm_budget_bytes.  footprints may be
+ * NULL (all 0).  Errors: EINVAL, ENOMEM (even M = 2 does not fit). */
+int boost_modulus_from_budget(const uint64_t *tensor_bytes,
+                              const uint64_t *footprints, size_t n_tensors,
+                              uint64_t hbm_budget_bytes, uint32_t M_alpha,
+                              uint32_t *M);
+
+/* Place one weight tensor by MPP (§3.1, §4.4): plan the tier map, back HBM
+ * pages with one device slab and host pages with pinned, device-mapped host
+ * memory, copy `bytes` bytes from `src` (host or device address; the bytes are
+ * copied, src stays the caller's) and upload a device page table.  The last
+ * partial page is zero-filled.  Synchronises (load time only, §4.4).
+ * *out is released with boost_tensor_free.
+ * Errors: EINVAL, ENODEV, ENOMEM, EHIP. */
+int boost_place_weights(boost_ctx *ctx, const void *src, uint64_t bytes,
+                        uint32_t M, uint64_t footprint_bytes,
+                        boost_tensor **out);
+
+/* Same with an explicit tier map of n_pages codes (n_pages must equal
+ * ceil(bytes / 2 MiB)): all-HBM, all-host and contrast placements. */
+int boost_place_weights_map(boost_ctx *ctx, const void *src, uint64_t bytes,
+                            const uint8_t *tiers, uint64_t n_pages,
+                            boost_tensor **out);
+
+/* Tier map and page count of a placed tensor (tier_out may be NULL). */
+int boost_tensor_tiers(const boost_tensor *t, uint8_t *tier_out,
+                       uint64_t tier_cap, uint64_t *n_pages);
+
+/* Copy `bytes` bytes starting at logical offset `offset` of a placed tensor
+ * back to host memory `dst` through its page table (checks, synchronises). */
+int boost_tensor_read(const boost_tensor *t, uint64_t offset, void *dst,
+                      uint64_t bytes);
+
+int boost_tensor_free(boost_tensor *t);
+
+/* ------------------------------------------------------ a4: decode GEMV */
+
+/* Work-unit schedule of the GEMV (library-wide):
+ *   BOOST_SCHED_ADDRESS: workgroups take units in address order, blind to
+ *     tiers (the transparent kernel of §3.1: a wave's host share comes only
+ *     from placement);
+ *   BOOST_SCHED_CAP: CTA specialisation (§3.2): `host_workers` persistent
+ *     workgroups, dispatched first, stream every host-page unit while all
+ *     other workgroups stream HBM-page units, so host and HBM reads overlap in
+ *     every wave (§3 "CAP").  host_workers = 0 picks the default. */
+#define BOOST_SCHED_ADDRESS 0
+#define BOOST_SCHED_CAP 1
+int boost_gemv_set_schedule(boost_ctx *ctx, int schedule, int host_workers);
+
+/* y[b, n] = sum_k W[n, k] * x[b, k] (§3.1 handwritten matmul; §4.4 up/down
+ * projections).  W: placed tensor holding an [N, K] row-major bf16 matrix
+ * (nn.Linear layout; bytes must equal N*K*2).  x: device bf16 [B, K]
+ * contiguous.  y: device [B, N] contiguous, fp32 (y_dtype BOOST_DTYPE_F32) or
+ * bf16 rounded to nearest even (BOOST_DTYPE_BF16).  Accumulation is fp32 and
+ * the reduction order is fixed, so results are bitwise reproducible and do
+ * not depend on the placement.  1 <= B <= 8, K % 8 == 0, N >= 1.
+ * Errors: EINVAL, ENODEV, EHIP (launch failure). */
+int boost_decode_gemv(boost_ctx *ctx, const boost_tensor *W, int N, int K,
+                      const void *x, int B, void *y, int y_dtype, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BOOST_CAP_H */

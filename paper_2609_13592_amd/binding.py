@@ -1,0 +1,267 @@
+"""ctypes binding of the C-ABI declared in include/boost_cap.h.
+
+Argument marshalling only: every function below converts Python values to C
+arguments, calls the entry point of the same name and turns a negative status
+into ``BoostError``.  No computation happens here and there is no fallback:
+if the library is missing, ``load()`` raises.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(HERE, "_lib", "libboostcap.so")
+
+OK, EINVAL, ENOMEM, EAGAIN, ENODEV, EHIP = 0, -22, -12, -11, -19, -5
+TIER_HBM, TIER_HOST = 0, 1
+DTYPE_F32, DTYPE_BF16 = 0, 1
+SCHED_ADDRESS, SCHED_CAP = 0, 1
+PAGE_BYTES = 2 * 1024 * 1024
+
+_vp = C.c_void_p
+_u64 = C.c_uint64
+_u32 = C.c_uint32
+_i32 = C.c_int
+_dbl = C.c_double
+
+
+class BoostError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"boost error {code}: {msg}")
+        self.code = code
+
+
+class KVCfg(C.Structure):
+    _fields_ = [("layers", _u32), ("kv_heads", _u32), ("head_dim", _u32),
+                ("block_tokens", _u32), ("n_blocks", _u32), ("M", _u32),
+                ("tier_mode", _i32), ("max_batch", _u32),
+                ("max_blocks_per_seq", _u32)]
+
+
+class KVInfo(C.Structure):
+    _fields_ = [("nb_pool", _u32), ("blocks_per_page", _u32),
+                ("pages_per_tensor", _u64), ("host_pages_per_tensor", _u64),
+                ("n_shh", _u32), ("shh_host_heads", _u32),
+                ("local_host_heads", _u32), ("tau", _dbl)]
+
+
+class KVStats(C.Structure):
+    _fields_ = [("free_shh", _u32), ("free_local", _u32),
+                ("used_blocks", _u64), ("used_host_head_blocks", _u64),
+                ("requests", _u32), ("shh_requests", _u32)]
+
+
+_SIGS = {
+    "boost_last_error": (C.c_char_p, []),
+    "boost_version": (_i32, []),
+    "boost_init": (_i32, [_i32, C.POINTER(_vp)]),
+    "boost_shutdown": (_i32, [_vp]),
+    "boost_ctx_info": (_i32, [_vp, C.POINTER(_i32), C.POINTER(_i32)]),
+    "boost_set_host_coherent": (_i32, [_vp, _i32]),
+    "boost_calibrate": (_i32, [_vp, _u64, _u64, _i32, C.POINTER(_dbl),
+                               C.POINTER(_dbl), C.POINTER(_dbl)]),
+    "boost_stream_read_gbps": (_i32, [_vp, _vp, _u64, _i32, _i32, C.POINTER(_dbl)]),
+    "boost_modulus_from_alpha": (_i32, [_dbl, C.POINTER(_u32)]),
+    "boost_superpage_pages": (_i32, [_u64, C.POINTER(_u32)]),
+    "boost_plan_mpp": (_i32, [_u64, _u32, _u64, _vp, _u64, C.POINTER(_u64)]),
+    "boost_modulus_from_budget": (_i32, [_vp, _vp, C.c_size_t, _u64, _u32,
+                                         C.POINTER(_u32)]),
+    "boost_place_weights": (_i32, [_vp, _vp, _u64, _u32, _u64, C.POINTER(_vp)]),
+    "boost_place_weights_map": (_i32, [_vp, _vp, _u64, _vp, _u64, C.POINTER(_vp)]),
+    "boost_tensor_tiers": (_i32, [_vp, _vp, _u64, C.POINTER(_u64)]),
+    "boost_tensor_read": (_i32, [_vp, _u64, _vp, _u64]),
+    "boost_tensor_free": (_i32, [_vp]),
+    "boost_gemv_set_schedule": (_i32, [_vp, _i32, _i32]),
+    "boost_decode_gemv": (_i32, [_vp, _vp, _i32, _i32, _vp, _i32, _vp, _i32, _vp]),
+}
+
+_lib = None
+
+
+def lib_path() -> str:
+    return _LIB_PATH
+
+
+def load():
+    """Load the HIP library (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        raise ImportError(f"{_LIB_PATH} is missing: build it with "
+                          "`python -m paper_2609_13592_amd.build`")
+    # One HIP runtime per process: torch ships its own libamdhip64 (same
+    # soname).  Loading torch first makes the library bind to that copy
+    # instead of pulling in a second runtime that would see no device.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
+    lib = C.CDLL(_LIB_PATH)
+    for name, (res, args) in _SIGS.items():
+        fn = getattr(lib, name, None)
+        if fn is None:
+            continue
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _check(rc: int):
+    if rc < 0:
+        msg = load().boost_last_error().decode(errors="replace")
+        raise BoostError(rc, msg)
+    return rc
+
+
+def _ptr(a) -> int:
+    """Address of a numpy array, torch tensor or integer."""
+    if a is None:
+        return 0
+    if isinstance(a, int):
+        return a
+    if isinstance(a, np.ndarray):
+        assert a.flags["C_CONTIGUOUS"]
+        return a.ctypes.data
+    if hasattr(a, "data_ptr"):
+        return a.data_ptr()
+    raise TypeError(type(a))
+
+
+def _stream(s) -> int:
+    if s is None:
+        return 0
+    if isinstance(s, int):
+        return s
+    return s.cuda_stream
+
+
+# ------------------------------------------------------------------ context
+def boost_version() -> int:
+    return load().boost_version()
+
+
+def _runtime_first(device: int):
+    """PyTorch and the library share one HIP runtime in this process; let
+    torch create its device context before the library touches the device."""
+    import sys
+    torch = sys.modules.get("torch")
+    if torch is None or device < 0:
+        return
+    torch.cuda.init()
+    torch.empty(1, device=f"cuda:{device}")
+
+
+def boost_init(device: int) -> int:
+    _runtime_first(device)
+    h = _vp()
+    _check(load().boost_init(device, C.byref(h)))
+    return h.value
+
+
+def boost_shutdown(ctx: int):
+    _check(load().boost_shutdown(ctx))
+
+
+def boost_ctx_info(ctx: int):
+    d, n = _i32(), _i32()
+    _check(load().boost_ctx_info(ctx, C.byref(d), C.byref(n)))
+    return d.value, n.value
+
+
+def boost_set_host_coherent(ctx: int, coherent: bool):
+    _check(load().boost_set_host_coherent(ctx, int(bool(coherent))))
+
+
+# -------------------------------------------------------------- calibration
+def boost_calibrate(ctx: int, hbm_bytes: int, host_bytes: int, iters: int):
+    d, h, a = _dbl(), _dbl(), _dbl()
+    _check(load().boost_calibrate(ctx, hbm_bytes, host_bytes, iters, C.byref(d),
+                                  C.byref(h), C.byref(a)))
+    return d.value, h.value, a.value
+
+
+def boost_stream_read_gbps(ctx: int, src, nbytes: int, grid: int, iters: int) -> float:
+    g = _dbl()
+    _check(load().boost_stream_read_gbps(ctx, _ptr(src), nbytes, grid, iters,
+                                         C.byref(g)))
+    return g.value
+
+
+def boost_modulus_from_alpha(alpha: float) -> int:
+    m = _u32()
+    _check(load().boost_modulus_from_alpha(alpha, C.byref(m)))
+    return m.value
+
+
+# ---------------------------------------------------------------- placement
+def boost_superpage_pages(footprint: int) -> int:
+    s = _u32()
+    _check(load().boost_superpage_pages(footprint, C.byref(s)))
+    return s.value
+
+
+def boost_plan_mpp(nbytes: int, M: int, footprint: int = 0) -> np.ndarray:
+    n = _u64()
+    _check(load().boost_plan_mpp(nbytes, M, footprint, None, 0, C.byref(n)))
+    out = np.zeros(n.value, dtype=np.uint8)
+    _check(load().boost_plan_mpp(nbytes, M, footprint, _ptr(out), out.size,
+                                 C.byref(n)))
+    return out
+
+
+def boost_modulus_from_budget(sizes, budget: int, M_alpha: int, footprints=None) -> int:
+    s = np.ascontiguousarray(sizes, dtype=np.uint64)
+    f = None if footprints is None else np.ascontiguousarray(footprints, dtype=np.uint64)
+    m = _u32()
+    _check(load().boost_modulus_from_budget(_ptr(s), _ptr(f), s.size, budget,
+                                            M_alpha, C.byref(m)))
+    return m.value
+
+
+def boost_place_weights(ctx: int, src, nbytes: int, M: int, footprint: int = 0) -> int:
+    h = _vp()
+    _check(load().boost_place_weights(ctx, _ptr(src), nbytes, M, footprint,
+                                      C.byref(h)))
+    return h.value
+
+
+def boost_place_weights_map(ctx: int, src, nbytes: int, tiers) -> int:
+    t = np.ascontiguousarray(tiers, dtype=np.uint8)
+    h = _vp()
+    _check(load().boost_place_weights_map(ctx, _ptr(src), nbytes, _ptr(t), t.size,
+                                          C.byref(h)))
+    return h.value
+
+
+def boost_tensor_tiers(t: int) -> np.ndarray:
+    n = _u64()
+    _check(load().boost_tensor_tiers(t, None, 0, C.byref(n)))
+    out = np.zeros(n.value, dtype=np.uint8)
+    _check(load().boost_tensor_tiers(t, _ptr(out), out.size, C.byref(n)))
+    return out
+
+
+def boost_tensor_read(t: int, offset: int, nbytes: int) -> np.ndarray:
+    out = np.zeros(nbytes, dtype=np.uint8)
+    _check(load().boost_tensor_read(t, offset, _ptr(out), nbytes))
+    return out
+
+
+def boost_tensor_free(t: int):
+    _check(load().boost_tensor_free(t))
+
+
+# -------------------------------------------------------------------- GEMV
+def boost_gemv_set_schedule(ctx: int, schedule: int, host_workers: int = 0):
+    _check(load().boost_gemv_set_schedule(ctx, schedule, host_workers))
+
+
+def boost_decode_gemv(ctx: int, W: int, N: int, K: int, x, B: int, y,
+                      y_dtype: int = DTYPE_F32, stream=None):
+    _check(load().boost_decode_gemv(ctx, W, N, K, _ptr(x), B, _ptr(y), y_dtype,
+                                    _stream(stream)))

@@ -1,0 +1,58 @@
+// Library-internal state shared by the HIP translation units.
+#pragma once
+#include <hip/hip_runtime.h>
+
+#include "common.h"
+
+#define BOOST_HIP(call)                                                     \
+  do {                                                                      \
+    hipError_t e_ = (call);                                                 \
+    if (e_ != hipSuccess)                                                   \
+      return bst::fail(BOOST_EHIP, "%s failed: %s (%s:%d)", #call,          \
+                       hipGetErrorString(e_), __FILE__, __LINE__);          \
+  } while (0)
+
+struct boost_ctx {
+  int device = -1;          // -1: plan-only
+  int n_cu = 0;
+  int host_coherent = 1;
+  int gemv_schedule = BOOST_SCHED_CAP;
+  int gemv_host_workers = 0;  // 0: default
+};
+
+namespace bst {
+
+// One allocation that backs whole pages of one tier.
+struct Slab {
+  void* raw = nullptr;      // what hipMalloc / hipHostMalloc returned
+  char* base = nullptr;     // device-visible, 2 MiB aligned
+  char* host_base = nullptr;  // host-visible (host tier only)
+  uint64_t pages = 0;
+  bool host = false;
+};
+
+int slab_alloc(boost_ctx* ctx, uint64_t pages, bool host, Slab& s);
+void slab_free(Slab& s);
+
+}  // namespace bst
+
+struct boost_tensor {
+  boost_ctx* ctx = nullptr;
+  uint64_t bytes = 0;
+  uint64_t n_pages = 0;
+  std::vector<uint8_t> tiers;
+  std::vector<char*> page_ptr;          // device-visible address per page
+  std::vector<char*> copy_ptr;          // address for host-side copies
+  std::vector<int32_t> hbm_pages, host_pages;
+  bst::Slab hbm, host;
+  // device-side copies
+  char** d_page_table = nullptr;        // [n_pages]
+  int32_t* d_hbm_pages = nullptr;       // HBM page ids, ascending
+  int32_t* d_host_pages = nullptr;      // host page ids, ascending
+  float* d_partial = nullptr;           // split-row partial sums
+  int* d_flags = nullptr;               // split-row arrival counters
+};
+
+namespace bst {
+constexpr int kMaxGemvBatch = 8;
+}

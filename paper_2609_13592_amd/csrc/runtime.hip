@@ -1,0 +1,263 @@
+// Context, memory backend and weight placement (§4.2 PAM design, §4.4 PAM
+// implementation).  HBM pages of a tensor share one device slab; host pages
+// live in pinned, device-mapped host memory from hipHostMalloc (the MI355X
+// counterpart of the paper's mmap + mbind + host registration per 2 MB page);
+// a device page table gives every page's device-visible address.
+#include <algorithm>
+#include <cstring>
+
+#include "runtime.h"
+
+namespace bst {
+
+int slab_alloc(boost_ctx* ctx, uint64_t pages, bool host, Slab& s) {
+  s = Slab{};
+  s.pages = pages;
+  s.host = host;
+  if (pages == 0) return BOOST_OK;
+  const size_t bytes = pages * kPage + kPage;  // room to align to 2 MiB
+  if (host) {
+    unsigned flags = hipHostMallocMapped |
+                     (ctx->host_coherent ? hipHostMallocCoherent
+                                         : hipHostMallocNonCoherent);
+    hipError_t e = hipHostMalloc(&s.raw, bytes, flags);
+    if (e != hipSuccess || !s.raw)
+      return fail(BOOST_ENOMEM, "hipHostMalloc(%zu) failed: %s", bytes,
+                  hipGetErrorString(e));
+    void* dev = nullptr;
+    e = hipHostGetDevicePointer(&dev, s.raw, 0);
+    if (e != hipSuccess) {
+      (void)hipHostFree(s.raw);
+      s.raw = nullptr;
+      return fail(BOOST_EHIP, "hipHostGetDevicePointer failed: %s",
+                  hipGetErrorString(e));
+    }
+    uint64_t pad = (kPage - (reinterpret_cast<uintptr_t>(dev) & (kPage - 1))) &
+                   (kPage - 1);
+    s.base = static_cast<char*>(dev) + pad;
+    s.host_base = static_cast<char*>(s.raw) + pad;
+  } else {
+    hipError_t e = hipMalloc(&s.raw, bytes);
+    if (e != hipSuccess || !s.raw)
+      return fail(BOOST_ENOMEM, "hipMalloc(%zu) failed: %s", bytes,
+                  hipGetErrorString(e));
+    uint64_t pad = (kPage - (reinterpret_cast<uintptr_t>(s.raw) & (kPage - 1))) &
+                   (kPage - 1);
+    s.base = static_cast<char*>(s.raw) + pad;
+  }
+  return BOOST_OK;
+}
+
+void slab_free(Slab& s) {
+  if (s.raw) {
+    if (s.host)
+      (void)hipHostFree(s.raw);
+    else
+      (void)hipFree(s.raw);
+  }
+  s = Slab{};
+}
+
+static int free_tensor(boost_tensor* t) {
+  if (!t) return BOOST_OK;
+  if (t->ctx && t->ctx->device >= 0) (void)hipSetDevice(t->ctx->device);
+  (void)hipFree(t->d_page_table);
+  (void)hipFree(t->d_hbm_pages);
+  (void)hipFree(t->d_host_pages);
+  (void)hipFree(t->d_partial);
+  (void)hipFree(t->d_flags);
+  slab_free(t->hbm);
+  slab_free(t->host);
+  delete t;
+  return BOOST_OK;
+}
+
+static int upload(void** dst, const void* src, size_t bytes) {
+  if (bytes == 0) bytes = 16;  // keep a valid (unused) pointer
+  BOOST_HIP(hipMalloc(dst, bytes));
+  if (src) BOOST_HIP(hipMemcpy(*dst, src, bytes, hipMemcpyHostToDevice));
+  return BOOST_OK;
+}
+
+static int place(boost_ctx* ctx, const void* src, uint64_t bytes,
+                 const uint8_t* tiers, uint64_t n_pages, boost_tensor** out) {
+  if (!ctx || !src || !out || !tiers) return fail(BOOST_EINVAL, "null argument");
+  if (ctx->device < 0) return fail(BOOST_ENODEV, "plan-only context");
+  if (bytes == 0) return fail(BOOST_EINVAL, "tensor of 0 bytes");
+  if (n_pages != pages_of(bytes))
+    return fail(BOOST_EINVAL, "tier map has %llu pages, tensor needs %llu",
+                (unsigned long long)n_pages, (unsigned long long)pages_of(bytes));
+  if (n_pages >= (1ull << 31)) return fail(BOOST_EINVAL, "tensor too large");
+  BOOST_HIP(hipSetDevice(ctx->device));
+  auto* t = new boost_tensor();
+  t->ctx = ctx;
+  t->bytes = bytes;
+  t->n_pages = n_pages;
+  t->tiers.assign(tiers, tiers + n_pages);
+  for (uint64_t i = 0; i < n_pages; ++i) {
+    if (tiers[i] == BOOST_TIER_HBM)
+      t->hbm_pages.push_back(static_cast<int32_t>(i));
+    else if (tiers[i] == BOOST_TIER_HOST)
+      t->host_pages.push_back(static_cast<int32_t>(i));
+    else {
+      delete t;
+      return fail(BOOST_EINVAL, "tier code %u at page %llu", tiers[i],
+                  (unsigned long long)i);
+    }
+  }
+  int rc = slab_alloc(ctx, t->hbm_pages.size(), false, t->hbm);
+  if (!rc) rc = slab_alloc(ctx, t->host_pages.size(), true, t->host);
+  if (rc) {
+    free_tensor(t);
+    return rc;
+  }
+  t->page_ptr.resize(n_pages);
+  t->copy_ptr.resize(n_pages);
+  for (size_t i = 0; i < t->hbm_pages.size(); ++i)
+    t->page_ptr[t->hbm_pages[i]] = t->copy_ptr[t->hbm_pages[i]] =
+        t->hbm.base + i * kPage;
+  for (size_t i = 0; i < t->host_pages.size(); ++i) {
+    t->page_ptr[t->host_pages[i]] = t->host.base + i * kPage;
+    t->copy_ptr[t->host_pages[i]] = t->host.host_base + i * kPage;
+  }
+
+  auto done = [&](int code) {
+    if (code) free_tensor(t);
+    return code;
+  };
+  // copy the bytes in, page by page; zero the tail of a partial last page
+  for (uint64_t i = 0; i < n_pages; ++i) {
+    const uint64_t off = i * kPage;
+    const uint64_t len = std::min<uint64_t>(kPage, bytes - off);
+    hipError_t e = hipMemcpy(t->copy_ptr[i], static_cast<const char*>(src) + off,
+                             len, hipMemcpyDefault);
+    if (e != hipSuccess)
+      return done(fail(BOOST_EHIP, "copy of page %llu failed: %s",
+                       (unsigned long long)i, hipGetErrorString(e)));
+    if (len < kPage) {
+      if (t->tiers[i] == BOOST_TIER_HOST)
+        std::memset(t->copy_ptr[i] + len, 0, kPage - len);
+      else
+        e = hipMemset(t->page_ptr[i] + len, 0, kPage - len);
+      if (e != hipSuccess)
+        return done(fail(BOOST_EHIP, "hipMemset failed: %s", hipGetErrorString(e)));
+    }
+  }
+  int r = upload(reinterpret_cast<void**>(&t->d_page_table), t->page_ptr.data(),
+                 n_pages * sizeof(char*));
+  if (!r) r = upload(reinterpret_cast<void**>(&t->d_hbm_pages), t->hbm_pages.data(),
+                     t->hbm_pages.size() * sizeof(int32_t));
+  if (!r) r = upload(reinterpret_cast<void**>(&t->d_host_pages), t->host_pages.data(),
+                     t->host_pages.size() * sizeof(int32_t));
+  // split-row scratch: one slot pair per page boundary, zeroed once here
+  const size_t nb = n_pages + 1;
+  if (!r) r = upload(reinterpret_cast<void**>(&t->d_partial), nullptr,
+                     nb * 2 * kMaxGemvBatch * sizeof(float));
+  if (!r) r = upload(reinterpret_cast<void**>(&t->d_flags), nullptr, nb * sizeof(int));
+  if (r) return done(r);
+  hipError_t e = hipMemset(t->d_flags, 0, nb * sizeof(int));
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  if (e != hipSuccess)
+    return done(fail(BOOST_EHIP, "placement sync failed: %s", hipGetErrorString(e)));
+  *out = t;
+  return BOOST_OK;
+}
+
+}  // namespace bst
+
+using namespace bst;
+
+extern "C" {
+
+int boost_init(int device, boost_ctx** out) {
+  if (!out) return fail(BOOST_EINVAL, "null out");
+  *out = nullptr;
+  auto* c = new boost_ctx();
+  if (device >= 0) {
+    int n = 0;
+    hipError_t e = hipGetDeviceCount(&n);
+    if (e != hipSuccess || device >= n) {
+      delete c;
+      return fail(e != hipSuccess ? BOOST_EHIP : BOOST_EINVAL,
+                  "device %d unavailable (%d devices, %s)", device, n,
+                  hipGetErrorString(e));
+    }
+    e = hipSetDevice(device);
+    hipDeviceProp_t p;
+    if (e == hipSuccess) e = hipGetDeviceProperties(&p, device);
+    if (e != hipSuccess) {
+      delete c;
+      return fail(BOOST_EHIP, "device %d: %s", device, hipGetErrorString(e));
+    }
+    c->device = device;
+    c->n_cu = p.multiProcessorCount;
+  } else if (device != -1) {
+    delete c;
+    return fail(BOOST_EINVAL, "device %d", device);
+  }
+  *out = c;
+  return BOOST_OK;
+}
+
+int boost_shutdown(boost_ctx* ctx) {
+  delete ctx;
+  return BOOST_OK;
+}
+
+int boost_ctx_info(const boost_ctx* ctx, int* device, int* n_cu) {
+  if (!ctx) return fail(BOOST_EINVAL, "null ctx");
+  if (device) *device = ctx->device;
+  if (n_cu) *n_cu = ctx->n_cu;
+  return BOOST_OK;
+}
+
+int boost_set_host_coherent(boost_ctx* ctx, int coherent) {
+  if (!ctx) return fail(BOOST_EINVAL, "null ctx");
+  ctx->host_coherent = coherent ? 1 : 0;
+  return BOOST_OK;
+}
+
+int boost_place_weights(boost_ctx* ctx, const void* src, uint64_t bytes,
+                        uint32_t M, uint64_t footprint_bytes, boost_tensor** out) {
+  std::vector<uint8_t> tiers;
+  int rc = mpp_tiers(bytes, M, footprint_bytes, tiers);
+  if (rc) return rc;
+  return place(ctx, src, bytes, tiers.data(), tiers.size(), out);
+}
+
+int boost_place_weights_map(boost_ctx* ctx, const void* src, uint64_t bytes,
+                            const uint8_t* tiers, uint64_t n_pages,
+                            boost_tensor** out) {
+  return place(ctx, src, bytes, tiers, n_pages, out);
+}
+
+int boost_tensor_tiers(const boost_tensor* t, uint8_t* tier_out, uint64_t tier_cap,
+                       uint64_t* n_pages) {
+  if (!t || !n_pages) return fail(BOOST_EINVAL, "null argument");
+  *n_pages = t->n_pages;
+  if (tier_out)
+    std::memcpy(tier_out, t->tiers.data(), std::min<uint64_t>(tier_cap, t->n_pages));
+  return BOOST_OK;
+}
+
+int boost_tensor_read(const boost_tensor* t, uint64_t offset, void* dst,
+                      uint64_t bytes) {
+  if (!t || !dst) return fail(BOOST_EINVAL, "null argument");
+  if (offset > t->bytes || bytes > t->bytes - offset)
+    return fail(BOOST_EINVAL, "range beyond tensor");
+  BOOST_HIP(hipSetDevice(t->ctx->device));
+  uint64_t done = 0;
+  while (done < bytes) {
+    const uint64_t off = offset + done;
+    const uint64_t page = off / kPage, in = off % kPage;
+    const uint64_t len = std::min(bytes - done, kPage - in);
+    BOOST_HIP(hipMemcpy(static_cast<char*>(dst) + done, t->copy_ptr[page] + in, len,
+                        hipMemcpyDefault));
+    done += len;
+  }
+  return BOOST_OK;
+}
+
+int boost_tensor_free(boost_tensor* t) { return free_tensor(t); }
+
+}  // extern "C"

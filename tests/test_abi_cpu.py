@@ -1,0 +1,108 @@
+"""C-ABI checks that need no GPU: the library loads, exports every symbol the
+headers declare, and its CPU-only planners match the oracle bit for bit."""
+import glob
+import os
+import re
+
+import numpy as np
+import pytest
+from hypothesis import given, settings, strategies as st
+
+from oracle import placement as opl
+from paper_2609_13592_amd import binding as bd
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_symbols():
+    names = set()
+    for h in glob.glob(os.path.join(ROOT, "include", "*.h")):
+        src = open(h).read()
+        src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+        for m in re.finditer(r"\b(boost_[a-z0-9_]+)\s*\(", src):
+            names.add(m.group(1))
+    return sorted(names)
+
+
+def test_library_loads_and_exports_every_declared_symbol():
+    lib = bd.load()
+    names = declared_symbols()
+    assert len(names) >= 15
+    missing = [n for n in names if not hasattr(lib, n)]
+    assert not missing, missing
+    assert bd.boost_version() >= 100
+
+
+def test_plan_only_context():
+    ctx = bd.boost_init(-1)
+    assert bd.boost_ctx_info(ctx) == (-1, 0)
+    with pytest.raises(bd.BoostError) as e:
+        bd.boost_place_weights(ctx, np.zeros(16, np.uint8), 16, 4)
+    assert e.value.code == bd.ENODEV
+    bd.boost_shutdown(ctx)
+
+
+def test_bad_arguments():
+    for bad in (0.0, -1.0, 1.5):
+        with pytest.raises(bd.BoostError) as e:
+            bd.boost_modulus_from_alpha(bad)
+        assert e.value.code == bd.EINVAL
+    with pytest.raises(bd.BoostError):
+        bd.boost_plan_mpp(0, 4)
+    with pytest.raises(bd.BoostError):
+        bd.boost_plan_mpp(100, 1)
+    with pytest.raises(bd.BoostError) as e:
+        bd.boost_init(-2)
+    assert e.value.code == bd.EINVAL
+
+
+@given(st.floats(min_value=1e-4, max_value=1.0, allow_nan=False))
+@settings(max_examples=400, deadline=None)
+def test_modulus_matches_oracle(alpha):
+    assert bd.boost_modulus_from_alpha(alpha) == opl.modulus_from_alpha(alpha)
+
+
+def test_modulus_paper_values():
+    assert bd.boost_modulus_from_alpha(0.1) == 11
+    assert bd.boost_modulus_from_alpha(350 / 3330) == 11
+
+
+@given(st.integers(1, 300 * opl.PAGE), st.integers(2, 40),
+       st.sampled_from([0, 1, 4096, 28672 * 128, 3 * 1024 * 1024,
+                        7 * 1024 * 1024, opl.PAGE, 5 * opl.PAGE]))
+@settings(max_examples=300, deadline=None)
+def test_plan_mpp_matches_oracle(nbytes, M, footprint):
+    got = bd.boost_plan_mpp(nbytes, M, footprint)
+    exp = opl.mpp_tier_map(nbytes, M, footprint)
+    assert np.array_equal(got, exp)
+    assert bd.boost_superpage_pages(footprint) == opl.superpage_pages(footprint)
+
+
+def test_plan_mpp_exhaustive_small():
+    for n in range(1, 65):
+        for M in range(2, 17):
+            assert np.array_equal(bd.boost_plan_mpp(n * opl.PAGE, M),
+                                  opl.mpp_tier_map(n * opl.PAGE, M))
+
+
+@given(st.lists(st.integers(1, 200), min_size=1, max_size=10),
+       st.floats(0.3, 1.05), st.integers(2, 300))
+@settings(max_examples=200, deadline=None)
+def test_budget_modulus_matches_oracle(pages, frac, M_alpha):
+    sizes = [p * opl.PAGE - 123 for p in pages]
+    budget = int(sum(pages) * frac) * opl.PAGE
+    try:
+        exp = opl.modulus_from_budget(sizes, budget, M_alpha)
+    except MemoryError:
+        with pytest.raises(bd.BoostError) as e:
+            bd.boost_modulus_from_budget(sizes, budget, M_alpha)
+        assert e.value.code == bd.ENOMEM
+        return
+    assert bd.boost_modulus_from_budget(sizes, budget, M_alpha) == exp
+
+
+def test_budget_modulus_70b_chain():
+    d, f, v = 8192, 28672, 128256
+    per_layer = [(64 + 16) * 128 * d * 2, d * 64 * 128 * 2, 2 * f * d * 2, d * f * 2]
+    sizes = per_layer * 80 + [v * d * 2] * 2
+    assert bd.boost_modulus_from_budget(sizes, 120 * 10 ** 9, 10 ** 6) == 6

@@ -1,0 +1,189 @@
+"""GPU parity of the tiered-page GEMV against the oracle (through the C-ABI)."""
+import numpy as np
+import pytest
+
+import synth
+from oracle import gemv as og
+from oracle import placement as opl
+from paper_2609_13592_amd import binding as bd
+from tests.gpu_util import dev_f32, dev_u16, host_u16, stream, sync, to_dev_u16
+
+pytestmark = pytest.mark.gpu
+TOL = 2e-2          # stated bar for bf16 inputs (max rel err)
+
+
+def assert_f32_bound(y, w, x, rows=None):
+    """Internal gate: every output within the worst-case fp32 summation error
+    K * 2^-24 * sum_k |w x| of the fp64 result (any summation order)."""
+    wf = og.bf16_to_f32(w).astype(np.float64)
+    xf = og.bf16_to_f32(x).astype(np.float64)
+    ref = xf @ wf.T
+    mag = np.abs(xf) @ np.abs(wf).T
+    K = wf.shape[1]
+    yy = y if rows is None else y[:, rows]
+    assert np.all(np.abs(yy - ref) <= K * 2.0 ** -24 * mag + 1e-30)
+
+
+def run_gemv(ctx, t, N, K, x_dev, B, y_dtype=bd.DTYPE_F32):
+    y = dev_f32(B, N) if y_dtype == bd.DTYPE_F32 else dev_u16(B, N)
+    bd.boost_decode_gemv(ctx, t, N, K, x_dev, B, y, y_dtype, stream())
+    sync()
+    return y.cpu().numpy() if y_dtype == bd.DTYPE_F32 else host_u16(y)
+
+
+def place(ctx, w, tiers=None, M=None):
+    nbytes = w.nbytes
+    if tiers is not None:
+        return bd.boost_place_weights_map(ctx, w, nbytes, tiers)
+    return bd.boost_place_weights(ctx, w, nbytes, M)
+
+
+def test_calibration(gpu_ctx):
+    hbm, host, alpha = bd.boost_calibrate(gpu_ctx, 2 << 30, 512 << 20, 3)
+    print(f"calibration: hbm {hbm:.1f} GB/s host {host:.1f} GB/s alpha {alpha:.5f}")
+    assert 1000 < hbm < 8200
+    assert 2 < host < 200
+    assert 0 < alpha < 0.1
+    M = bd.boost_modulus_from_alpha(alpha)
+    assert M == opl.modulus_from_alpha(alpha)
+
+
+def test_single_layer_parity(gpu_ctx):
+    """4096 x 4096 bf16 layer, 16 pages, page 15 on host (M = 16)."""
+    w, x = synth.single_layer_inputs()
+    t = place(gpu_ctx, w, M=16)
+    try:
+        tiers = bd.boost_tensor_tiers(t)
+        assert np.array_equal(tiers, opl.mpp_tier_map(w.nbytes, 16))
+        assert np.flatnonzero(tiers).tolist() == [15]
+        # bytes of the host page and of an HBM page read back unchanged
+        for page in (0, 15):
+            got = bd.boost_tensor_read(t, page * opl.PAGE, opl.PAGE)
+            assert np.array_equal(got, w.view(np.uint8).reshape(-1)[
+                page * opl.PAGE:(page + 1) * opl.PAGE])
+        xd = to_dev_u16(x)
+        r64, r32 = og.gemv_f64(w, x), og.gemv_f32(w, x)
+        for sched in (bd.SCHED_CAP, bd.SCHED_ADDRESS):
+            bd.boost_gemv_set_schedule(gpu_ctx, sched)
+            y = run_gemv(gpu_ctx, t, 4096, 4096, xd, 1)
+            assert og.rel_err(y, r64) <= TOL
+            assert og.rel_err(y, r32) <= TOL
+            assert_f32_bound(y, w, x)
+    finally:
+        bd.boost_gemv_set_schedule(gpu_ctx, bd.SCHED_CAP)
+        bd.boost_tensor_free(t)
+
+
+@pytest.mark.parametrize("N,K,B", [(4096, 4096, 1), (300, 14336, 1), (5000, 520, 3),
+                                   (1000, 8, 8), (257, 4104, 2), (77, 28672, 5)])
+def test_placement_invariance_and_parity(gpu_ctx, N, K, B):
+    """Bitwise-equal y under all-HBM, alternating, MPP and all-host maps and
+    both schedules; every result within the bar of the oracle."""
+    w, x = synth.gemv_inputs(11 + N + K + B, N, K, B)
+    n = opl.n_pages(w.nbytes)
+    maps = {"hbm": np.zeros(n, np.uint8), "host": np.ones(n, np.uint8),
+            "alt": (np.arange(n) % 2).astype(np.uint8),
+            "mpp3": opl.mpp_tier_map(w.nbytes, 3)}
+    xd = to_dev_u16(x)
+    r64 = og.gemv_f64(w, x)
+    r32 = og.gemv_f32(w, x)
+    outs = []
+    for name, tiers in maps.items():
+        t = place(gpu_ctx, w, tiers=tiers)
+        try:
+            for sched in (bd.SCHED_CAP, bd.SCHED_ADDRESS):
+                bd.boost_gemv_set_schedule(gpu_ctx, sched, 3)
+                y = run_gemv(gpu_ctx, t, N, K, xd, B)
+                assert og.rel_err(y, r64) <= TOL, (name, sched)
+                assert og.rel_err(y, r32) <= TOL, (name, sched)
+                assert_f32_bound(y, w, x)
+                outs.append(y)
+        finally:
+            bd.boost_gemv_set_schedule(gpu_ctx, bd.SCHED_CAP)
+            bd.boost_tensor_free(t)
+    for y in outs[1:]:
+        assert np.array_equal(y.view(np.uint32), outs[0].view(np.uint32))
+
+
+def test_exact_pins(gpu_ctx):
+    """W = I gives x back, all-ones gives K: exact in fp32."""
+    n = 1024
+    eye = synth.round_bf16(np.eye(n, dtype=np.float32))
+    rng = np.random.default_rng(5)
+    x = synth.normal_bf16(rng, (2, n), 1.0)
+    t = place(gpu_ctx, eye, tiers=(np.arange(opl.n_pages(eye.nbytes)) % 2).astype(np.uint8))
+    try:
+        y = run_gemv(gpu_ctx, t, n, n, to_dev_u16(x), 2)
+        assert np.array_equal(y, og.bf16_to_f32(x))
+    finally:
+        bd.boost_tensor_free(t)
+    K = 4096
+    ones = synth.round_bf16(np.ones((520, K), np.float32))
+    t = place(gpu_ctx, ones, M=2)
+    try:
+        y = run_gemv(gpu_ctx, t, 520, K, to_dev_u16(ones[:1]), 1)
+        assert np.all(y == K)
+    finally:
+        bd.boost_tensor_free(t)
+
+
+def test_bf16_output(gpu_ctx):
+    N, K = 2000, 4096
+    w, x = synth.gemv_inputs(21, N, K, 2)
+    t = place(gpu_ctx, w, M=3)
+    try:
+        xd = to_dev_u16(x)
+        yb = run_gemv(gpu_ctx, t, N, K, xd, 2, bd.DTYPE_BF16)
+        yf = run_gemv(gpu_ctx, t, N, K, xd, 2, bd.DTYPE_F32)
+        assert og.rel_err(og.bf16_to_f32(yb), og.gemv_f64(w, x)) <= TOL
+        # bf16 output is the round-to-nearest-even of the fp32 result
+        assert np.array_equal(yb, og.f32_to_bf16(yf))
+    finally:
+        bd.boost_tensor_free(t)
+
+
+def test_bad_arguments(gpu_ctx):
+    w, x = synth.gemv_inputs(1, 64, 512, 1)
+    t = place(gpu_ctx, w, M=2)
+    xd = to_dev_u16(x)
+    y = dev_f32(9, 64)
+    try:
+        for args in ((64, 520, 1), (63, 512, 1), (64, 512, 9), (64, 512, 0)):
+            N, K, B = args
+            with pytest.raises(bd.BoostError) as e:
+                bd.boost_decode_gemv(gpu_ctx, t, N, K, xd, B, y, bd.DTYPE_F32, stream())
+            assert e.value.code == bd.EINVAL
+        with pytest.raises(bd.BoostError):
+            bd.boost_decode_gemv(gpu_ctx, t, 64, 512, xd, 1, y, 7, stream())
+    finally:
+        bd.boost_tensor_free(t)
+
+
+@pytest.mark.parametrize("kind", [0, 1, 2, 3, 9])
+def test_full_size_chain_tensor_sampled(gpu_ctx, kind):
+    """Full-size Llama-3-8B-shaped tensors (fused qkv, o, gate_up, down,
+    lm_head) placed by MPP at M = 11: sampled rows against the oracle."""
+    import torch
+    per_layer, head = synth.chain_shapes(synth.LLAMA8B)
+    shapes = {k: (n, kk) for _, k, n, kk in per_layer}
+    shapes[9] = head[2:]
+    N, K = shapes[kind]
+    wt = synth.chain_weight_torch(3, kind, N, K, "cuda")
+    w_dev = wt.view(torch.int16)
+    rng = np.random.default_rng(kind)
+    x = synth.normal_bf16(rng, (1, K), 1.0)
+    t = bd.boost_place_weights(gpu_ctx, w_dev, N * K * 2, 11)
+    try:
+        tiers = bd.boost_tensor_tiers(t)
+        assert np.array_equal(tiers, opl.mpp_tier_map(N * K * 2, 11))
+        y = run_gemv(gpu_ctx, t, N, K, to_dev_u16(x), 1)
+        rows = np.unique(np.concatenate([rng.integers(0, N, 200), [0, N - 1],
+                                         (np.arange(0, N * K, opl.PAGE // 2) // K)]))
+        w_rows = w_dev[torch.from_numpy(rows).cuda()].cpu().numpy().view(np.uint16)
+        ref = og.gemv_rows_f64(w_rows, rows, x)
+        assert og.rel_err(y[:, rows], ref) <= TOL
+        assert_f32_bound(y, w_rows, x, rows)
+    finally:
+        bd.boost_tensor_free(t)
+        del wt, w_dev
+        torch.cuda.empty_cache()
