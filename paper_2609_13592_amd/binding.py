@@ -13,7 +13,8 @@ import os
 import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-_LIB_PATH = os.path.join(HERE, "_lib", "libboostcap.so")
+# BOOST_LIB may name another build of the same library (e.g. a tuning variant)
+_LIB_PATH = os.environ.get("BOOST_LIB") or os.path.join(HERE, "_lib", "libboostcap.so")
 
 OK, EINVAL, ENOMEM, EAGAIN, ENODEV, EHIP = 0, -22, -12, -11, -19, -5
 TIER_HBM, TIER_HOST = 0, 1

@@ -5,7 +5,7 @@
 // restricted to ONE page, so a workgroup reads one tier for its whole life
 // (§3.2 CTA-level confinement: a workgroup never mixes tiers).  A row that
 // straddles a page boundary is split-K across the two workgroups of those
-// pages; each writes its partial sum and the second to arrive adds them in a
+// pages; each stores its partial sum and a small second kernel adds them in a
 // fixed order (part of the earlier page first), so results are bitwise
 // reproducible and independent of the placement.
 //
@@ -47,7 +47,6 @@ struct GemvParams {
   void* y;
   int y_bf16;
   float* partial;  // [(n_pages + 1) boundaries][2 sides][kMaxGemvBatch]
-  int* flags;      // [(n_pages + 1) boundaries]
 };
 
 __device__ __forceinline__ float lo_bf16(uint32_t v) { return __uint_as_float(v << 16); }
@@ -89,62 +88,73 @@ __device__ __forceinline__ void store_y(const GemvParams& P, int b, int64_t row,
     static_cast<float*>(P.y)[i] = v;
 }
 
-// Combine the two halves of a row split at page boundary `bnd` (between pages
-// bnd-1 and bnd).  side 0 = the part in the earlier page.
+// A row cut by page boundary `bnd` (between pages bnd-1 and bnd) is summed by
+// two workgroups, one per page; each stores its partial sum here (side 0 = the
+// part on the earlier page) and split_fixup adds them after the main kernel.
 template <int B>
-__device__ void finish_split(const GemvParams& P, int64_t row, int bnd, int side,
-                             const float* v) {
+__device__ __forceinline__ void store_split(const GemvParams& P, int bnd, int side,
+                                            const float* v) {
   float* slot = P.partial + (static_cast<int64_t>(bnd) * 2 + side) * bst::kMaxGemvBatch;
 #pragma unroll
-  for (int b = 0; b < B; ++b)
-    __hip_atomic_store(slot + b, v[b], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  const int prev = __hip_atomic_fetch_add(P.flags + bnd, 1, __ATOMIC_ACQ_REL,
-                                          __HIP_MEMORY_SCOPE_AGENT);
-  if (prev == 1) {
-    const float* s0 = P.partial + static_cast<int64_t>(bnd) * 2 * bst::kMaxGemvBatch;
-    const float* s1 = s0 + bst::kMaxGemvBatch;
-#pragma unroll
-    for (int b = 0; b < B; ++b) {
-      const float a0 = __hip_atomic_load(s0 + b, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      const float a1 = __hip_atomic_load(s1 + b, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      store_y(P, b, row, a0 + a1);
-    }
-    __hip_atomic_store(P.flags + bnd, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
+  for (int b = 0; b < B; ++b) slot[b] = v[b];
 }
 
-// One unit: rows [r_first + j*RW*kWaves, ...) of page `page`, restricted to
-// the page's bytes.
-template <int B, int RW, int UN>
-__device__ void gemv_unit(const GemvParams& P, int page, int j) {
+// Raw buffer resource over `bytes` bytes at `base` (CDNA: offsets at or past
+// num_records read as zero, with no fault).  Word 3 selects 32-bit data.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base,
+                                                            uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0,
+                                           static_cast<int>(bytes), 0x00020000);
+}
+
+// Cache policy of weight loads: 2 = non-temporal (streamed once per token,
+// no reuse to keep in L2).
+#ifndef BOOST_W_AUX
+#define BOOST_W_AUX 2
+#endif
+template <int AUX = 0>
+__device__ __forceinline__ uint4 load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  auto v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, AUX);
+  return *reinterpret_cast<uint4*>(&v);
+}
+
+// Offsets at or above this are outside every resource used here (a page is
+// 2 MiB, x is at most 8 * 512 K elements), so the load returns zero.
+constexpr uint32_t kOOB = 0x80000000u;
+
+// One unit: a group of rows of page `page`, restricted to the page's bytes.
+// The wavefronts of the workgroup form (kWaves / KS) row slots of RW rows;
+// the KS wavefronts of a slot split K into KS contiguous column ranges
+// (split-K inside the workgroup) and combine their partial sums through LDS
+// in a fixed order.  The page's buffer resource covers exactly its valid
+// bytes, so columns of a cut row that lie on the neighbouring page, and
+// columns past K, read as zero without a branch.
+template <int B, int RW, int UN, int KS>
+__device__ void gemv_unit(const GemvParams& P, int page, int j, float* lds) {
+  constexpr int kSlots = kWaves / KS;
+  constexpr int kRowsWg = kSlots * RW;
   const int64_t K = P.K;
   const int64_t total = static_cast<int64_t>(P.N) * K;
   const int64_t pe0 = static_cast<int64_t>(page) * kPageElems;
   const int64_t pe1 = min(pe0 + kPageElems, total);
   const int64_t r_lo = pe0 / K;
   const int64_t r_hi = (pe1 - 1) / K;  // inclusive
+  const int64_t rbase = r_lo + static_cast<int64_t>(j) * kRowsWg;
+  if (rbase > r_hi) return;  // uniform over the workgroup
   const int wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
-  const int64_t r0 = r_lo + static_cast<int64_t>(j) * (RW * kWaves) + wave * RW;
-  if (r0 > r_hi) return;
+  const int slot = wave / KS, part = wave % KS;
+  const int64_t r0 = rbase + slot * RW;
 
-  const char* page_base = P.page_table[page];  // element pe0
-  int64_t c0[RW], c1[RW];
-  const char* rp[RW];  // address of column 0 of the row (may lie outside the page)
-  bool whole = true;
+  const __amdgpu_buffer_rsrc_t wr =
+      make_rsrc(P.page_table[page], static_cast<uint32_t>((pe1 - pe0) * 2));
+  const __amdgpu_buffer_rsrc_t xr =
+      make_rsrc(P.x, static_cast<uint32_t>(B * K * 2));
+  uint32_t ro[RW];  // byte offset of column 0 of each row from the page start
 #pragma unroll
   for (int i = 0; i < RW; ++i) {
     const int64_t r = r0 + i;
-    const int64_t e0 = r * K;
-    if (r <= r_hi) {
-      c0[i] = max(static_cast<int64_t>(0), pe0 - e0);
-      c1[i] = min(K, pe1 - e0);
-    } else {
-      c0[i] = 0;
-      c1[i] = 0;
-    }
-    whole = whole && c0[i] == 0 && c1[i] == K;
-    rp[i] = page_base + (e0 - pe0) * 2;
+    ro[i] = r <= r_hi ? static_cast<uint32_t>((r * K - pe0) * 2) : kOOB;
   }
 
   float acc[RW][B];
@@ -153,101 +163,130 @@ __device__ void gemv_unit(const GemvParams& P, int page, int j) {
 #pragma unroll
     for (int b = 0; b < B; ++b) acc[i][b] = 0.f;
 
-  const uint4 zero = make_uint4(0, 0, 0, 0);
-  const int64_t step = 64 * 8;
-  if (whole) {
-    // every row of this wavefront lies wholly inside the page
-    for (int64_t kb = 0; kb < K; kb += step * UN) {
-      uint4 wv[UN][RW], xv[UN][B];
+  constexpr int kStep = 64 * 8;  // columns covered by one load of a wavefront
+  // this wavefront's columns: [k_beg, k_end), k_beg a multiple of kStep
+  const int64_t kper = (((K + KS - 1) / KS) + kStep - 1) / kStep * kStep;
+  const int64_t k_beg = part * kper;
+  const int64_t k_end = min(K, k_beg + kper);
+  for (int64_t kb = k_beg; kb < k_end; kb += kStep * UN) {
+    uint4 wv[UN][RW], xv[UN][B];
 #pragma unroll
-      for (int u = 0; u < UN; ++u) {
-        const int64_t kc = kb + u * step + lane * 8;
-        const bool in = kc < K;
+    for (int u = 0; u < UN; ++u) {
+      const int64_t kc = kb + u * kStep + lane * 8;
+      const uint32_t oob = kc < k_end ? 0u : kOOB;
+      const uint32_t kc2 = static_cast<uint32_t>(kc * 2);
 #pragma unroll
-        for (int i = 0; i < RW; ++i)
-          wv[u][i] = in ? *reinterpret_cast<const uint4*>(rp[i] + kc * 2) : zero;
+      for (int b = 0; b < B; ++b)
+        xv[u][b] = load16(xr, (static_cast<uint32_t>(b * K * 2) + kc2) | oob);
 #pragma unroll
-        for (int b = 0; b < B; ++b)
-          xv[u][b] = in ? *reinterpret_cast<const uint4*>(P.x + b * K + kc) : zero;
-      }
-#pragma unroll
-      for (int u = 0; u < UN; ++u)
-#pragma unroll
-        for (int i = 0; i < RW; ++i)
-#pragma unroll
-          for (int b = 0; b < B; ++b) acc[i][b] = dot8(wv[u][i], xv[u][b], acc[i][b]);
+      for (int i = 0; i < RW; ++i) wv[u][i] = load16<BOOST_W_AUX>(wr, (ro[i] + kc2) | oob);
     }
-  } else {
-    // some row is cut by a page boundary: read only this page's columns;
-    // out-of-page lanes load a safe in-page address and contribute zero
-    for (int64_t kb = 0; kb < K; kb += step * UN) {
-      uint4 wv[UN][RW], xv[UN][B];
 #pragma unroll
-      for (int u = 0; u < UN; ++u) {
-        const int64_t kc = kb + u * step + lane * 8;
-        const bool in = kc < K;
+    for (int u = 0; u < UN; ++u)
 #pragma unroll
-        for (int i = 0; i < RW; ++i) {
-          const bool ok = in && kc >= c0[i] && kc < c1[i];
-          wv[u][i] = ok ? *reinterpret_cast<const uint4*>(rp[i] + kc * 2) : zero;
-        }
+      for (int i = 0; i < RW; ++i)
 #pragma unroll
-        for (int b = 0; b < B; ++b)
-          xv[u][b] = in ? *reinterpret_cast<const uint4*>(P.x + b * K + kc) : zero;
-      }
-#pragma unroll
-      for (int u = 0; u < UN; ++u)
-#pragma unroll
-        for (int i = 0; i < RW; ++i)
-#pragma unroll
-          for (int b = 0; b < B; ++b) acc[i][b] = dot8(wv[u][i], xv[u][b], acc[i][b]);
-    }
+        for (int b = 0; b < B; ++b) acc[i][b] = dot8(wv[u][i], xv[u][b], acc[i][b]);
   }
 
+  float v[RW][B];
+#pragma unroll
+  for (int i = 0; i < RW; ++i)
+#pragma unroll
+    for (int b = 0; b < B; ++b) v[i][b] = wave_sum(acc[i][b]);
+
+  if constexpr (KS > 1) {
+    // partial sums of the KS column ranges meet in LDS; the slot's first
+    // wavefront adds them in range order
+    if (lane == 0)
+#pragma unroll
+      for (int i = 0; i < RW; ++i)
+#pragma unroll
+        for (int b = 0; b < B; ++b) lds[(wave * RW + i) * B + b] = v[i][b];
+    __syncthreads();
+    if (part == 0 && lane == 0)
+#pragma unroll
+      for (int i = 0; i < RW; ++i)
+#pragma unroll
+        for (int b = 0; b < B; ++b) {
+          float s = lds[(wave * RW + i) * B + b];
+#pragma unroll
+          for (int q = 1; q < KS; ++q) s += lds[((wave + q) * RW + i) * B + b];
+          v[i][b] = s;
+        }
+    __syncthreads();  // LDS is reused by the next unit of a persistent worker
+  }
+  if (part != 0 || lane != 0) return;
 #pragma unroll
   for (int i = 0; i < RW; ++i) {
-    float v[B];
-#pragma unroll
-    for (int b = 0; b < B; ++b) v[b] = wave_sum(acc[i][b]);
     const int64_t r = r0 + i;
-    if (r > r_hi || lane != 0) continue;
-    if (c0[i] == 0 && c1[i] == K) {
+    if (r > r_hi) continue;
+    const int64_t e0 = r * K;
+    if (e0 >= pe0 && e0 + K <= pe1) {
 #pragma unroll
-      for (int b = 0; b < B; ++b) store_y(P, b, r, v[b]);
-    } else if (c0[i] > 0) {
-      finish_split<B>(P, r, page, 1, v);  // tail of a row begun on page-1
+      for (int b = 0; b < B; ++b) store_y(P, b, r, v[i][b]);
+    } else if (e0 < pe0) {
+      store_split<B>(P, page, 1, v[i]);  // tail of a row begun on page-1
     } else {
-      finish_split<B>(P, r, page + 1, 0, v);  // head of a row ending on page+1
+      store_split<B>(P, page + 1, 0, v[i]);  // head of a row ending on page+1
     }
   }
 }
 
-template <int B, int RW, int UN>
+template <int B, int RW, int UN, int KS>
 __global__ __launch_bounds__(kThreads) void gemv_kernel(GemvParams P) {
+  __shared__ float lds[kWaves * RW * B];
   const int bid = blockIdx.x;
   const int U = P.units_per_page;
   if (P.address_order) {
-    gemv_unit<B, RW, UN>(P, bid / U, bid % U);
+    gemv_unit<B, RW, UN, KS>(P, bid / U, bid % U, lds);
   } else if (bid < P.host_workers) {
     const int n_host_units = P.n_host_pages * U;
     for (int v = bid; v < n_host_units; v += P.host_workers)
-      gemv_unit<B, RW, UN>(P, P.host_pages[v / U], v % U);
+      gemv_unit<B, RW, UN, KS>(P, P.host_pages[v / U], v % U, lds);
   } else {
     const int u = bid - P.host_workers;
-    gemv_unit<B, RW, UN>(P, P.hbm_pages[u / U], u % U);
+    gemv_unit<B, RW, UN, KS>(P, P.hbm_pages[u / U], u % U, lds);
   }
 }
 
+// y of every row cut by a page boundary: part on the earlier page plus part
+// on the later page, in that order.  One lane per (boundary, batch row).
+__global__ __launch_bounds__(256) void split_fixup(GemvParams P, int n_pages, int B) {
+  const int t = blockIdx.x * blockDim.x + threadIdx.x;
+  const int bnd = 1 + t / B, b = t % B;
+  if (bnd >= n_pages) return;
+  const int64_t e = static_cast<int64_t>(bnd) * kPageElems;
+  if (e % P.K == 0) return;  // this boundary falls between rows
+  const float* s0 = P.partial + static_cast<int64_t>(bnd) * 2 * bst::kMaxGemvBatch;
+  store_y(P, b, e / P.K, s0[b] + s0[bst::kMaxGemvBatch + b]);
+}
+
+#ifndef BOOST_GEMV_UN1
+#define BOOST_GEMV_UN1 8
+#endif
+// Rows per wavefront and loads in flight per row, by batch size.
 template <int B>
 struct Shape {
-  static constexpr int RW = B <= 2 ? 2 : (B <= 4 ? 2 : 1);
-  static constexpr int UN = B <= 2 ? 4 : (B <= 4 ? 2 : 2);
+  static constexpr int RW = B == 1 ? 1 : (B <= 4 ? 2 : 1);
+  static constexpr int UN = B == 1 ? BOOST_GEMV_UN1 : (B <= 4 ? 4 : 2);
 };
 
-template <int B>
+// Wavefronts per row (split-K inside the workgroup) for a row of K columns:
+// enough that each wavefront reads a few KiB of a row, so long rows do not
+// serialise many round trips in one wavefront.
+#ifndef BOOST_GEMV_KS_MAX
+#define BOOST_GEMV_KS_MAX 4
+#endif
+inline int k_splits(int K) {
+  const int ks = K <= 6144 ? 1 : (K <= 12288 ? 2 : 4);
+  return ks < BOOST_GEMV_KS_MAX ? ks : BOOST_GEMV_KS_MAX;
+}
+
+template <int B, int KS>
 int launch(GemvParams& P, int n_pages, const boost_ctx* ctx, hipStream_t s) {
   constexpr int RW = Shape<B>::RW, UN = Shape<B>::UN;
-  const int rows_wg = RW * kWaves;
+  const int rows_wg = RW * (kWaves / KS);
   // units per page: enough for the page that meets the most rows
   const int64_t K = P.K, total = static_cast<int64_t>(P.N) * K;
   int64_t most = 0;
@@ -270,10 +309,25 @@ int launch(GemvParams& P, int n_pages, const boost_ctx* ctx, hipStream_t s) {
     grid = P.host_workers + static_cast<int64_t>(P.n_hbm_pages) * P.units_per_page;
   }
   if (grid > 0x7fffffff) return bst::fail(BOOST_EINVAL, "grid too large");
-  hipLaunchKernelGGL((gemv_kernel<B, RW, UN>), dim3(static_cast<unsigned>(grid)),
+  hipLaunchKernelGGL((gemv_kernel<B, RW, UN, KS>), dim3(static_cast<unsigned>(grid)),
                      dim3(kThreads), 0, s, P);
   BOOST_HIP(hipGetLastError());
+  if (n_pages > 1 && kPageElems % P.K != 0) {
+    const int lanes = (n_pages - 1) * B;
+    hipLaunchKernelGGL(split_fixup, dim3((lanes + 255) / 256), dim3(256), 0, s, P,
+                       n_pages, B);
+    BOOST_HIP(hipGetLastError());
+  }
   return BOOST_OK;
+}
+
+template <int B>
+int launch_b(GemvParams& P, int n_pages, const boost_ctx* ctx, hipStream_t s) {
+  switch (k_splits(P.K)) {
+    case 1: return launch<B, 1>(P, n_pages, ctx, s);
+    case 2: return launch<B, 2>(P, n_pages, ctx, s);
+    default: return launch<B, 4>(P, n_pages, ctx, s);
+  }
 }
 
 }  // namespace
@@ -321,18 +375,17 @@ int boost_decode_gemv(boost_ctx* ctx, const boost_tensor* W, int N, int K, const
   P.y = y;
   P.y_bf16 = y_dtype == BOOST_DTYPE_BF16;
   P.partial = W->d_partial;
-  P.flags = W->d_flags;
   auto s = static_cast<hipStream_t>(stream);
   const int n = static_cast<int>(W->n_pages);
   switch (B) {
-    case 1: return launch<1>(P, n, ctx, s);
-    case 2: return launch<2>(P, n, ctx, s);
-    case 3: return launch<3>(P, n, ctx, s);
-    case 4: return launch<4>(P, n, ctx, s);
-    case 5: return launch<5>(P, n, ctx, s);
-    case 6: return launch<6>(P, n, ctx, s);
-    case 7: return launch<7>(P, n, ctx, s);
-    default: return launch<8>(P, n, ctx, s);
+    case 1: return launch_b<1>(P, n, ctx, s);
+    case 2: return launch_b<2>(P, n, ctx, s);
+    case 3: return launch_b<3>(P, n, ctx, s);
+    case 4: return launch_b<4>(P, n, ctx, s);
+    case 5: return launch_b<5>(P, n, ctx, s);
+    case 6: return launch_b<6>(P, n, ctx, s);
+    case 7: return launch_b<7>(P, n, ctx, s);
+    default: return launch_b<8>(P, n, ctx, s);
   }
 }
 

@@ -50,7 +50,6 @@ struct boost_tensor {
   int32_t* d_hbm_pages = nullptr;       // HBM page ids, ascending
   int32_t* d_host_pages = nullptr;      // host page ids, ascending
   float* d_partial = nullptr;           // split-row partial sums
-  int* d_flags = nullptr;               // split-row arrival counters
 };
 
 namespace bst {

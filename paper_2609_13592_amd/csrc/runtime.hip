@@ -65,7 +65,6 @@ static int free_tensor(boost_tensor* t) {
   (void)hipFree(t->d_hbm_pages);
   (void)hipFree(t->d_host_pages);
   (void)hipFree(t->d_partial);
-  (void)hipFree(t->d_flags);
   slab_free(t->hbm);
   slab_free(t->host);
   delete t;
@@ -153,9 +152,8 @@ static int place(boost_ctx* ctx, const void* src, uint64_t bytes,
   const size_t nb = n_pages + 1;
   if (!r) r = upload(reinterpret_cast<void**>(&t->d_partial), nullptr,
                      nb * 2 * kMaxGemvBatch * sizeof(float));
-  if (!r) r = upload(reinterpret_cast<void**>(&t->d_flags), nullptr, nb * sizeof(int));
   if (r) return done(r);
-  hipError_t e = hipMemset(t->d_flags, 0, nb * sizeof(int));
+  hipError_t e = hipMemset(t->d_partial, 0, nb * 2 * kMaxGemvBatch * sizeof(float));
   if (e == hipSuccess) e = hipDeviceSynchronize();
   if (e != hipSuccess)
     return done(fail(BOOST_EHIP, "placement sync failed: %s", hipGetErrorString(e)));

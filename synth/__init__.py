@@ -23,9 +23,10 @@ PAGE_BYTES = 2 * 1024 * 1024
 def round_bf16(a: np.ndarray) -> np.ndarray:
     """float32 array -> bfloat16 bit patterns (uint16), round-to-nearest-even."""
     a = np.ascontiguousarray(a, dtype=np.float32)
-    u = a.view(np.uint32).astype(np.uint64)
-    lsb = (u >> 16) & 1
-    r = ((u + 0x7FFF + lsb) >> 16).astype(np.uint16)
+    u = a.view(np.uint32)
+    # finite values stay below 2^32 after adding the rounding bias
+    lsb = (u >> np.uint32(16)) & np.uint32(1)
+    r = ((u + np.uint32(0x7FFF) + lsb) >> np.uint32(16)).astype(np.uint16)
     nan = np.isnan(a)
     if nan.any():
         r[nan] = 0x7FC0
