@@ -183,6 +183,120 @@ int boost_gemv_set_schedule(boost_ctx *ctx, int schedule, int host_workers);
 int boost_decode_gemv(boost_ctx *ctx, const boost_tensor *W, int N, int K,
                       const void *x, int B, void *y, int y_dtype, void *stream);
 
+/* ------------------------------------------- a2/a3: KV pool and allocator */
+
+/* KV pool placement modes. */
+#define BOOST_KV_LPP 0      /* linear page placement, last 1/M of pages on host */
+#define BOOST_KV_ALL_HBM 1  /* every page in HBM (HBM-only baseline) */
+#define BOOST_KV_ALL_HOST 2 /* every page on host (stress / capacity bound) */
+
+/* Request / block types of the allocator (§4.3). */
+#define BOOST_KV_LOCAL 0 /* all-local: no head on host (fewer host heads) */
+#define BOOST_KV_SHH 1   /* single-head-host (more host heads when H > M) */
+
+typedef struct boost_kv_cfg {
+  uint32_t layers;             /* layers sharing one block id space */
+  uint32_t kv_heads;           /* H */
+  uint32_t head_dim;           /* D: 64 or 128 */
+  uint32_t block_tokens;       /* tokens per block: 16 (§4.3) */
+  uint32_t n_blocks;           /* blocks wanted; rounded up so every head's
+                                  region is whole pages */
+  uint32_t M;                  /* host share of pages 1/M (BOOST_KV_LPP) */
+  int32_t tier_mode;           /* BOOST_KV_* */
+  uint32_t q_heads;            /* Hq, a multiple of H (attention scratch) */
+  uint32_t max_batch;          /* largest B of a decode call (scratch) */
+  uint32_t max_blocks_per_seq; /* widest block-table row (scratch) */
+} boost_kv_cfg;
+
+typedef struct boost_kv_info {
+  uint32_t nb_pool;               /* blocks in the pool */
+  uint32_t blocks_per_page;       /* head-blocks per 2 MiB page */
+  uint64_t pages_per_tensor;      /* pages of one layer's K (or V) */
+  uint64_t host_pages_per_tensor; /* of which on host (the LPP tail) */
+  uint32_t n_shh;                 /* blocks on the SHH list */
+  uint32_t shh_host_heads;        /* host heads of an SHH block */
+  uint32_t local_host_heads;      /* host heads of an all-local block */
+  double tau;                     /* n_shh / nb_pool: the greedy threshold */
+} boost_kv_info;
+
+typedef struct boost_kv_usage {
+  uint32_t free_shh, free_local;  /* free blocks on each list */
+  uint64_t used_blocks;           /* blocks held by requests */
+  uint64_t used_host_head_blocks; /* sum of host heads over held blocks */
+  uint32_t requests, shh_requests;
+} boost_kv_usage;
+
+/* Create a KV pool (§4.2 LPP; §4.5 heads-outermost layout).  Every layer has
+ * a K and a V tensor laid out [H][NB][T][D] bf16 with NB rounded up so each
+ * head's region is whole 2 MiB pages; the last floor(pages / M) pages of each
+ * tensor are host-resident (BOOST_KV_LPP), so a block's host heads are the
+ * heads whose region reaches into that tail.  Blocks with the larger host-head
+ * count form the SHH list, the rest the all-local list (§4.3, §4.5).  On a
+ * device context the pages are backed (HBM slab + pinned host pages) and a
+ * device page table is uploaded; on a plan-only context only the allocator
+ * exists.  Errors: EINVAL (shape, M < 2 for LPP, head-block not dividing a
+ * page), ENOMEM, EHIP. */
+int boost_kv_pool_create(boost_ctx *ctx, const boost_kv_cfg *cfg,
+                         boost_kv_pool **out);
+int boost_kv_pool_info(const boost_kv_pool *pool, boost_kv_info *info);
+int boost_kv_pool_destroy(boost_kv_pool *pool);
+
+/* Host heads (0..H) of one block.  Errors: EINVAL (block out of range). */
+int boost_kv_block_host_heads(const boost_kv_pool *pool, int32_t block,
+                              uint32_t *n_host_heads);
+
+/* Append n_blocks blocks to request `request_id` (§4.3 wave-aware block
+ * fulfillment).  A new request takes the SHH type when the free-SHH fraction
+ * exceeds tau (strictly) and SHH blocks are free, else all-local if any are
+ * free, else SHH; an existing request keeps its type.  Blocks come from the
+ * list of the request's type, lowest id first; when that list empties the
+ * request switches to the other list and stays there (sticky fallback).  The
+ * call is all-or-nothing: with fewer than n_blocks free blocks nothing changes
+ * and BOOST_EAGAIN is returned (the scheduler decides, §4.3).  block_ids_out
+ * receives n_blocks ids in allocation order.  CPU only.
+ * Errors: EINVAL (n_blocks 0, null), EAGAIN. */
+int boost_kv_alloc(boost_kv_pool *pool, uint64_t request_id, uint32_t n_blocks,
+                   int32_t *block_ids_out);
+
+/* Return every block of the request to its list and forget the request.
+ * Errors: EINVAL (unknown request). */
+int boost_kv_free(boost_kv_pool *pool, uint64_t request_id);
+
+/* Current type (BOOST_KV_LOCAL / BOOST_KV_SHH) of a live request. */
+int boost_kv_request_type(const boost_kv_pool *pool, uint64_t request_id,
+                          int *type);
+int boost_kv_stats(const boost_kv_pool *pool, boost_kv_usage *out);
+
+/* ------------------------------------------------ a5: paged attention */
+
+/* Write n tokens of one layer into the pool: token i goes to slot
+ * slots[i] = block * T + offset (negative slots are skipped, slots past the
+ * pool are ignored).  k, v: device bf16 [n, H, D] contiguous; slots: device
+ * int32 [n].  Asynchronous on `stream`.  Errors: EINVAL, ENODEV, EHIP. */
+int boost_kv_write(boost_ctx *ctx, const boost_kv_pool *pool, int layer,
+                   const int32_t *slots, const void *k, const void *v, int n,
+                   void *stream);
+
+/* GQA decode attention over the pool (§3.3 KV head chunks per workgroup;
+ * §4.5 paged layout):  for request b and query head h (KV head g = h / (Hq/H))
+ *   o[b,h,:] = sum_t softmax_t(scale * q[b,h,:] . k[b,t,g,:]) v[b,t,g,:]
+ * over t < ctx_lens[b], where token t of request b lives in block
+ * block_tables[b * max_blocks + t / T] at offset t % T.  Work item = (KV head,
+ * request, context partition): the Hq/H query heads of a KV head share every
+ * K/V load, partitions are merged by log-sum-exp in a fixed order, and items
+ * of the heads that can hold host pages are dispatched first.
+ * q: device bf16 [B, Hq, D]; block_tables: device int32 [B, max_blocks];
+ * ctx_lens: device int32 [B]; out: device [B, Hq, D] fp32 or bf16.
+ * scale <= 0 selects 1/sqrt(D).  A block id outside the pool contributes
+ * nothing; ctx_lens[b] = 0 gives a zero row.  1 <= B <= max_batch,
+ * Hq == q_heads of the pool, max_blocks <= max_blocks_per_seq.
+ * Errors: EINVAL, ENODEV, EHIP. */
+int boost_paged_attn_decode(boost_ctx *ctx, const boost_kv_pool *pool, int layer,
+                            const void *q, int B, int Hq,
+                            const int32_t *block_tables, int max_blocks,
+                            const int32_t *ctx_lens, float scale, void *out,
+                            int out_dtype, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -13,6 +13,9 @@ h // G with G = Hq / H):
     o[b, h, :] = sum_t p_t * v[b, t, g, :]
 
 K and V are given per request in logical order as [L_b, H, D] bf16.
+
+Reading for the degenerate case the paper never meets: a request with an
+empty context (L_b = 0) has no softmax; its output row is zero.
 """
 from __future__ import annotations
 
@@ -23,6 +26,8 @@ from .gemv import bf16_to_f32
 
 def _attend(q, k, v, scale):
     # q [G, D], k [L, D], v [L, D] -> [G, D] in the dtype of the inputs
+    if k.shape[0] == 0:
+        return np.zeros_like(q)
     s = (q @ k.T) * scale
     s = s - s.max(axis=1, keepdims=True)
     e = np.exp(s)

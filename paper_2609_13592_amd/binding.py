@@ -17,6 +17,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.environ.get("BOOST_LIB") or os.path.join(HERE, "_lib", "libboostcap.so")
 
 OK, EINVAL, ENOMEM, EAGAIN, ENODEV, EHIP = 0, -22, -12, -11, -19, -5
+KV_LPP, KV_ALL_HBM, KV_ALL_HOST = 0, 1, 2
+KV_LOCAL, KV_SHH = 0, 1
 TIER_HBM, TIER_HOST = 0, 1
 DTYPE_F32, DTYPE_BF16 = 0, 1
 SCHED_ADDRESS, SCHED_CAP = 0, 1
@@ -38,7 +40,7 @@ class BoostError(RuntimeError):
 class KVCfg(C.Structure):
     _fields_ = [("layers", _u32), ("kv_heads", _u32), ("head_dim", _u32),
                 ("block_tokens", _u32), ("n_blocks", _u32), ("M", _u32),
-                ("tier_mode", _i32), ("max_batch", _u32),
+                ("tier_mode", _i32), ("q_heads", _u32), ("max_batch", _u32),
                 ("max_blocks_per_seq", _u32)]
 
 
@@ -76,6 +78,17 @@ _SIGS = {
     "boost_tensor_read": (_i32, [_vp, _u64, _vp, _u64]),
     "boost_tensor_free": (_i32, [_vp]),
     "boost_gemv_set_schedule": (_i32, [_vp, _i32, _i32]),
+    "boost_kv_pool_create": (_i32, [_vp, C.POINTER(KVCfg), C.POINTER(_vp)]),
+    "boost_kv_pool_info": (_i32, [_vp, C.POINTER(KVInfo)]),
+    "boost_kv_pool_destroy": (_i32, [_vp]),
+    "boost_kv_block_host_heads": (_i32, [_vp, C.c_int32, C.POINTER(_u32)]),
+    "boost_kv_alloc": (_i32, [_vp, _u64, _u32, _vp]),
+    "boost_kv_free": (_i32, [_vp, _u64]),
+    "boost_kv_request_type": (_i32, [_vp, _u64, C.POINTER(_i32)]),
+    "boost_kv_stats": (_i32, [_vp, C.POINTER(KVStats)]),
+    "boost_kv_write": (_i32, [_vp, _vp, _i32, _vp, _vp, _vp, _i32, _vp]),
+    "boost_paged_attn_decode": (_i32, [_vp, _vp, _i32, _vp, _i32, _i32, _vp, _i32,
+                                       _vp, C.c_float, _vp, _i32, _vp]),
     "boost_decode_gemv": (_i32, [_vp, _vp, _i32, _i32, _vp, _i32, _vp, _i32, _vp]),
 }
 
@@ -266,3 +279,71 @@ def boost_decode_gemv(ctx: int, W: int, N: int, K: int, x, B: int, y,
                       y_dtype: int = DTYPE_F32, stream=None):
     _check(load().boost_decode_gemv(ctx, W, N, K, _ptr(x), B, _ptr(y), y_dtype,
                                     _stream(stream)))
+
+
+# ------------------------------------------------------------- KV pool / DSR
+def boost_kv_pool_create(ctx: int, layers: int, kv_heads: int, head_dim: int,
+                         n_blocks: int, M: int, tier_mode: int = KV_LPP,
+                         q_heads: int = 0, max_batch: int = 0,
+                         max_blocks_per_seq: int = 0, block_tokens: int = 16) -> int:
+    cfg = KVCfg(layers, kv_heads, head_dim, block_tokens, n_blocks, M, tier_mode,
+                q_heads or kv_heads, max_batch, max_blocks_per_seq)
+    h = _vp()
+    _check(load().boost_kv_pool_create(ctx, C.byref(cfg), C.byref(h)))
+    return h.value
+
+
+def boost_kv_pool_info(pool: int) -> dict:
+    i = KVInfo()
+    _check(load().boost_kv_pool_info(pool, C.byref(i)))
+    return {f: getattr(i, f) for f, _ in KVInfo._fields_}
+
+
+def boost_kv_pool_destroy(pool: int):
+    _check(load().boost_kv_pool_destroy(pool))
+
+
+def boost_kv_block_host_heads(pool: int, block: int) -> int:
+    n = _u32()
+    _check(load().boost_kv_block_host_heads(pool, block, C.byref(n)))
+    return n.value
+
+
+def boost_kv_alloc(pool: int, request_id: int, n_blocks: int):
+    """Block ids as a list, or EAGAIN (the int) when the pool cannot serve."""
+    out = np.zeros(max(n_blocks, 1), dtype=np.int32)
+    rc = load().boost_kv_alloc(pool, request_id, n_blocks, _ptr(out))
+    if rc == EAGAIN:
+        return EAGAIN
+    _check(rc)
+    return out[:n_blocks].tolist()
+
+
+def boost_kv_free(pool: int, request_id: int):
+    _check(load().boost_kv_free(pool, request_id))
+
+
+def boost_kv_request_type(pool: int, request_id: int) -> int:
+    t = _i32()
+    _check(load().boost_kv_request_type(pool, request_id, C.byref(t)))
+    return t.value
+
+
+def boost_kv_stats(pool: int) -> dict:
+    st = KVStats()
+    _check(load().boost_kv_stats(pool, C.byref(st)))
+    return {f: getattr(st, f) for f, _ in KVStats._fields_}
+
+
+def boost_kv_write(ctx: int, pool: int, layer: int, slots, k, v, n: int, stream=None):
+    _check(load().boost_kv_write(ctx, pool, layer, _ptr(slots), _ptr(k), _ptr(v), n,
+                                 _stream(stream)))
+
+
+def boost_paged_attn_decode(ctx: int, pool: int, layer: int, q, B: int, Hq: int,
+                            block_tables, max_blocks: int, ctx_lens, scale: float,
+                            out, out_dtype: int = DTYPE_F32, stream=None):
+    _check(load().boost_paged_attn_decode(ctx, pool, layer, _ptr(q), B, Hq,
+                                          _ptr(block_tables), max_blocks,
+                                          _ptr(ctx_lens), scale, _ptr(out), out_dtype,
+                                          _stream(stream)))

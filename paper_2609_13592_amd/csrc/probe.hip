@@ -14,27 +14,40 @@ constexpr int kThreads = 256;
 constexpr int kUnroll = 8;
 
 // Each workgroup reads one contiguous slice; lanes stride by 256 vectors so a
-// wavefront's 64 lanes cover 1 KiB contiguous per load.  The XOR of all words
-// is stored only when it equals a magic value, which keeps the loads alive
-// without a data-dependent store in practice.
-__global__ __launch_bounds__(kThreads) void stream_read(const uint4* __restrict__ src,
+// wavefront's 64 lanes cover 1 KiB contiguous per load.  Loads are raw buffer
+// loads with the non-temporal policy, exactly as the decode kernels stream
+// their operands, so alpha is the ratio the kernels can actually reach.  The
+// slice is addressed as windows of at most 2 GiB (the 32-bit buffer offset).
+// The XOR of all words is stored only when it equals a magic value, which
+// keeps the loads alive without a data-dependent store in practice.
+__global__ __launch_bounds__(kThreads) void stream_read(const char* __restrict__ src,
                                                         uint64_t n_vec,
                                                         uint32_t* __restrict__ sink) {
   const uint64_t per = (n_vec + gridDim.x - 1) / gridDim.x;
   const uint64_t beg = static_cast<uint64_t>(blockIdx.x) * per;
   const uint64_t end = beg + per < n_vec ? beg + per : n_vec;
   uint32_t acc = 0;
-  uint64_t i = beg + threadIdx.x;
-  for (; i + (kUnroll - 1) * kThreads < end; i += kUnroll * kThreads) {
-    uint4 v[kUnroll];
+  if (beg < end) {
+    const uint64_t span = (end - beg) * 16;  // bytes of this slice (< 2^31 checked on host)
+    const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<char*>(src) + beg * 16, 0, static_cast<int>(span), 0x00020000);
+    const uint32_t n = static_cast<uint32_t>(end - beg);
+    uint32_t i = threadIdx.x;
+    for (; i + (kUnroll - 1) * kThreads < n; i += kUnroll * kThreads) {
+      uint4 v[kUnroll];
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) v[u] = src[i + u * kThreads];
+      for (int u = 0; u < kUnroll; ++u) {
+        auto t = __builtin_amdgcn_raw_buffer_load_b128(r, (i + u * kThreads) * 16, 0, 2);
+        v[u] = *reinterpret_cast<uint4*>(&t);
+      }
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
-  }
-  for (; i < end; i += kThreads) {
-    uint4 v = src[i];
-    acc ^= v.x ^ v.y ^ v.z ^ v.w;
+      for (int u = 0; u < kUnroll; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
+    }
+    for (; i < n; i += kThreads) {
+      auto t = __builtin_amdgcn_raw_buffer_load_b128(r, i * 16, 0, 2);
+      uint4 v = *reinterpret_cast<uint4*>(&t);
+      acc ^= v.x ^ v.y ^ v.z ^ v.w;
+    }
   }
   if (acc == 0x9e3779b9u) sink[blockIdx.x] = acc;
 }
@@ -45,13 +58,15 @@ int measure(const void* src, uint64_t bytes, int grid, int iters, uint32_t* sink
   BOOST_HIP(hipEventCreate(&a));
   BOOST_HIP(hipEventCreate(&b));
   const uint64_t n_vec = bytes / 16;
+  if ((n_vec + grid - 1) / grid * 16 >= (1ull << 31))
+    return bst::fail(BOOST_EINVAL, "slice per workgroup exceeds 2 GiB; raise the grid");
   hipLaunchKernelGGL(stream_read, dim3(grid), dim3(kThreads), 0, 0,
-                     static_cast<const uint4*>(src), n_vec, sink);
+                     static_cast<const char*>(src), n_vec, sink);
   BOOST_HIP(hipGetLastError());
   BOOST_HIP(hipEventRecord(a, 0));
   for (int it = 0; it < iters; ++it)
     hipLaunchKernelGGL(stream_read, dim3(grid), dim3(kThreads), 0, 0,
-                       static_cast<const uint4*>(src), n_vec, sink);
+                       static_cast<const char*>(src), n_vec, sink);
   BOOST_HIP(hipGetLastError());
   BOOST_HIP(hipEventRecord(b, 0));
   BOOST_HIP(hipEventSynchronize(b));

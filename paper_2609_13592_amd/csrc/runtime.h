@@ -55,3 +55,18 @@ struct boost_tensor {
 namespace bst {
 constexpr int kMaxGemvBatch = 8;
 }
+
+#include "dsr.h"
+
+struct boost_kv_pool {
+  boost_ctx* ctx = nullptr;
+  boost_kv_cfg cfg{};
+  bst::KvGeom geom;
+  bst::Dsr dsr;
+  // device backing (absent on a plan-only context)
+  bst::Slab hbm, host;
+  char** d_page_table = nullptr;  // [layers][2 (K, V)][pages]
+  float* d_part_acc = nullptr;    // [max_batch][q_heads][max_parts][D]
+  float* d_part_ml = nullptr;     // [max_batch][q_heads][max_parts][2] (max, sum)
+  int max_parts = 0;
+};

@@ -1,0 +1,161 @@
+"""GPU parity of the paged-attention decode over a tiered KV pool."""
+import numpy as np
+import pytest
+
+import synth
+from oracle import attention as oa
+from oracle import gemv as og
+from oracle import kvpool as okv
+from paper_2609_13592_amd import binding as bd
+from tests.gpu_util import dev_f32, dev_u16, fill_pool, host_u16, stream, sync, to_dev_u16
+
+pytestmark = pytest.mark.gpu
+TOL = 2e-2
+
+
+def run_attn(ctx, pool, layer, q, tables, lens, out_dtype=bd.DTYPE_F32, scale=0.0):
+    import torch
+    B, Hq, D = q.shape
+    qd = to_dev_u16(q)
+    td = torch.from_numpy(np.ascontiguousarray(tables, dtype=np.int32)).cuda()
+    ld = torch.from_numpy(np.asarray(lens, dtype=np.int32)).cuda()
+    out = dev_f32(B, Hq, D) if out_dtype == bd.DTYPE_F32 else dev_u16(B, Hq, D)
+    bd.boost_paged_attn_decode(ctx, pool, layer, qd, B, Hq, td, tables.shape[1], ld,
+                               scale, out, out_dtype, stream())
+    sync()
+    return out.cpu().numpy() if out_dtype == bd.DTYPE_F32 else host_u16(out)
+
+
+def new_pool(ctx, H, Hq, nb, M, mode, layers=1, max_batch=64, max_blocks=256):
+    return bd.boost_kv_pool_create(ctx, layers, H, 128, nb, M, mode, q_heads=Hq,
+                                   max_batch=max_batch, max_blocks_per_seq=max_blocks)
+
+
+@pytest.mark.parametrize("Hq,H", [(32, 8), (64, 8), (8, 8), (16, 8)])
+def test_small_parity_and_placement_invariance(gpu_ctx, Hq, H):
+    lengths = np.array([1, 15, 16, 17, 300, 1000, 0, 2049])
+    _, q, ks, vs = synth.attention_inputs(len(lengths), Hq, H, 128, 0, 0, seed=4,
+                                          kv_seed=5, lengths=lengths)
+    ref = oa.decode_attention(q, ks, vs)
+    outs = []
+    for mode, M in ((bd.KV_ALL_HBM, 0), (bd.KV_LPP, 3), (bd.KV_ALL_HOST, 0)):
+        pool = new_pool(gpu_ctx, H, Hq, 2000, M, mode, max_blocks=160)
+        try:
+            tables = fill_pool(bd, gpu_ctx, pool, 0, lengths, ks, vs)
+            o = run_attn(gpu_ctx, pool, 0, q, tables, lengths)
+            assert og.rel_err(o, ref) <= TOL
+            assert np.max(np.abs(o - ref)) < 1e-4
+            assert np.all(o[6] == 0)             # empty context: zero row
+            outs.append(o)
+        finally:
+            bd.boost_kv_pool_destroy(pool)
+    for o in outs[1:]:
+        assert np.array_equal(o.view(np.uint32), outs[0].view(np.uint32))
+
+
+def test_host_heads_follow_block_types(gpu_ctx):
+    """LPP with H = 8 and a modulus above H: the tail lies in head 7, so an SHH
+    request has exactly its head-7 data on host; output still exact."""
+    H, Hq, M = 8, 32, 12
+    pool = new_pool(gpu_ctx, H, Hq, 4096, M, bd.KV_LPP)
+    try:
+        info = bd.boost_kv_pool_info(pool)
+        g = okv.kv_geometry(4096, H, 128, M)
+        assert info["host_pages_per_tensor"] == g.host_pages
+        assert info["shh_host_heads"] == 1 and info["local_host_heads"] == 0
+        lengths = synth.context_lengths(9, 16, 200, 900)
+        _, q, ks, vs = synth.attention_inputs(16, Hq, H, 128, 0, 0, seed=9, kv_seed=10,
+                                              lengths=lengths)
+        tables = fill_pool(bd, gpu_ctx, pool, 0, lengths, ks, vs)
+        types = [bd.boost_kv_request_type(pool, b) for b in range(16)]
+        assert bd.KV_SHH in types and bd.KV_LOCAL in types
+        o = run_attn(gpu_ctx, pool, 0, q, tables, lengths)
+        assert og.rel_err(o, oa.decode_attention(q, ks, vs)) <= TOL
+    finally:
+        bd.boost_kv_pool_destroy(pool)
+
+
+def test_two_layers_and_bf16_output(gpu_ctx):
+    H, Hq = 8, 32
+    pool = new_pool(gpu_ctx, H, Hq, 1024, 5, bd.KV_LPP, layers=2)
+    try:
+        lengths = np.array([33, 400, 129])
+        _, q, k0, v0 = synth.attention_inputs(3, Hq, H, 128, 0, 0, seed=1, kv_seed=2,
+                                              lengths=lengths)
+        _, _, k1, v1 = synth.attention_inputs(3, Hq, H, 128, 0, 0, seed=1, kv_seed=3,
+                                              lengths=lengths)
+        tables = fill_pool(bd, gpu_ctx, pool, 0, lengths, k0, v0)
+        fill_pool(bd, gpu_ctx, pool, 1, lengths, k1, v1, tables=tables)
+        o0 = run_attn(gpu_ctx, pool, 0, q, tables, lengths)
+        o1 = run_attn(gpu_ctx, pool, 1, q, tables, lengths)
+        assert og.rel_err(o0, oa.decode_attention(q, k0, v0)) <= TOL
+        assert og.rel_err(o1, oa.decode_attention(q, k1, v1)) <= TOL
+        ob = run_attn(gpu_ctx, pool, 1, q, tables, lengths, bd.DTYPE_BF16)
+        assert np.array_equal(ob, og.f32_to_bf16(o1))
+        # an explicit scale replaces 1/sqrt(D)
+        o2 = run_attn(gpu_ctx, pool, 0, q, tables, lengths, scale=0.05)
+        assert og.rel_err(o2, oa.decode_attention(q, k0, v0, scale=0.05)) <= TOL
+    finally:
+        bd.boost_kv_pool_destroy(pool)
+
+
+def test_bad_arguments(gpu_ctx):
+    import torch
+    pool = new_pool(gpu_ctx, 8, 32, 512, 4, bd.KV_LPP, max_batch=4, max_blocks=8)
+    q = dev_u16(4, 32, 128)
+    t = torch.zeros((4, 8), dtype=torch.int32, device="cuda")
+    lens = torch.zeros(4, dtype=torch.int32, device="cuda")
+    out = dev_f32(4, 32, 128)
+    try:
+        for args in ((0, 5, 32, 8), (0, 4, 16, 8), (0, 4, 32, 9), (1, 4, 32, 8)):
+            layer, B, Hq, mb = args
+            with pytest.raises(bd.BoostError) as e:
+                bd.boost_paged_attn_decode(gpu_ctx, pool, layer, q, B, Hq, t, mb, lens,
+                                           0.0, out, bd.DTYPE_F32, stream())
+            assert e.value.code == bd.EINVAL
+    finally:
+        bd.boost_kv_pool_destroy(pool)
+
+
+def test_config3_full_size_sampled(gpu_ctx):
+    """Batch 64, 32/8 heads, lengths U[512, 4096] (seed 0), admitted through
+    the allocator after a seeded churn warm-up, pool modulus 111: sampled
+    (request, head) pairs against the oracle; the all-HBM pool agrees bitwise."""
+    B, Hq, H = 64, 32, 8
+    lengths, q, ks, vs = synth.attention_inputs(B, Hq, H, 128, 512, 4096, seed=0,
+                                                kv_seed=1)
+    need = sum((int(L) + 15) // 16 for L in lengths)
+    nb = need + 16384
+    outs = []
+    for mode, M in ((bd.KV_LPP, 111), (bd.KV_ALL_HBM, 0)):
+        pool = new_pool(gpu_ctx, H, Hq, nb, M, mode, max_batch=64, max_blocks=256)
+        try:
+            # churn warm-up (replace events: retire the victim, admit a new
+            # request) so block ids are scattered as in a live pool; a quarter
+            # of the churn requests stay alive
+            live = set()
+            for victim, L in synth.churn_trace(2, 256, 48, 512, 4096):
+                r = 1000 + victim
+                if r in live:
+                    bd.boost_kv_free(pool, r)
+                    live.discard(r)
+                if bd.boost_kv_alloc(pool, r, (L + 15) // 16) != bd.EAGAIN:
+                    live.add(r)
+            for r in sorted(live):
+                if r % 4:
+                    bd.boost_kv_free(pool, r)
+            tables = fill_pool(bd, gpu_ctx, pool, 0, lengths, ks, vs, max_blocks=256)
+            st = bd.boost_kv_stats(pool)
+            assert st["used_blocks"] >= need
+            outs.append(run_attn(gpu_ctx, pool, 0, q, tables, lengths))
+        finally:
+            bd.boost_kv_pool_destroy(pool)
+    assert np.array_equal(outs[0].view(np.uint32), outs[1].view(np.uint32))
+    rng = np.random.default_rng(0)
+    pairs = [(int(b), int(h)) for b, h in zip(rng.integers(0, B, 48), rng.integers(0, Hq, 48))]
+    pairs += [(0, 0), (B - 1, Hq - 1)]
+    ref = oa.decode_attention(q, ks, vs, heads=pairs)
+    got = np.array([outs[0][b, h] for b, h in pairs])
+    exp = np.array([ref[p] for p in pairs])
+    assert og.rel_err(got, exp) <= TOL
+    assert np.max(np.abs(got - exp)) < 1e-4

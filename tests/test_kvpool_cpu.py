@@ -1,0 +1,167 @@
+"""KV pool geometry and allocator through the C-ABI (plan-only context),
+bit-exact against the oracle: host heads per block, lists, threshold and
+every allocation decision of random traces."""
+import json
+import os
+
+import numpy as np
+import pytest
+from hypothesis import given, settings, strategies as st
+
+from oracle import kvpool as okv
+from paper_2609_13592_amd import binding as bd
+
+WORKED = json.load(open(os.path.join(os.path.dirname(__file__), "golden",
+                                     "dsr_worked_example.json")))
+
+
+@pytest.fixture(scope="module")
+def plan_ctx():
+    ctx = bd.boost_init(-1)
+    yield ctx
+    bd.boost_shutdown(ctx)
+
+
+def make(ctx, nb, H, D, M, mode=bd.KV_LPP):
+    return bd.boost_kv_pool_create(ctx, 2, H, D, nb, M, mode, q_heads=H * 4)
+
+
+def host_heads(pool, nb):
+    return np.array([bd.boost_kv_block_host_heads(pool, b) for b in range(nb)])
+
+
+@given(st.integers(1, 5000), st.sampled_from([1, 2, 4, 8, 16]),
+       st.sampled_from([64, 128]), st.integers(2, 200))
+@settings(max_examples=120, deadline=None)
+def test_geometry_matches_oracle(plan_ctx, nb_req, H, D, M):
+    pool = make(plan_ctx, nb_req, H, D, M)
+    try:
+        info = bd.boost_kv_pool_info(pool)
+        g = okv.kv_geometry(nb_req, H, D, M)
+        assert info["nb_pool"] == g.nb_pool
+        assert info["blocks_per_page"] == g.blocks_per_page
+        assert info["pages_per_tensor"] == g.pages
+        assert info["host_pages_per_tensor"] == g.host_pages
+        assert np.array_equal(host_heads(pool, g.nb_pool), g.host_heads)
+        shh, loc = okv.block_lists(g)
+        assert info["n_shh"] == len(shh)
+        assert info["tau"] == len(shh) / g.nb_pool
+    finally:
+        bd.boost_kv_pool_destroy(pool)
+
+
+def test_all_hbm_and_all_host_modes(plan_ctx):
+    for mode, expect in ((bd.KV_ALL_HBM, 0), (bd.KV_ALL_HOST, 8)):
+        pool = make(plan_ctx, 1000, 8, 128, 0, mode)
+        try:
+            info = bd.boost_kv_pool_info(pool)
+            assert info["n_shh"] == 0
+            assert set(host_heads(pool, info["nb_pool"]).tolist()) == {expect}
+        finally:
+            bd.boost_kv_pool_destroy(pool)
+
+
+def test_bad_configs(plan_ctx):
+    with pytest.raises(bd.BoostError):
+        make(plan_ctx, 100, 8, 128, 1)                 # M < 2
+    with pytest.raises(bd.BoostError):
+        make(plan_ctx, 100, 8, 96, 4)                  # head_dim
+    with pytest.raises(bd.BoostError):
+        bd.boost_kv_pool_create(plan_ctx, 1, 8, 128, 100, 4, q_heads=12)  # Hq % H
+    pool = make(plan_ctx, 100, 8, 128, 4)
+    with pytest.raises(bd.BoostError):
+        bd.boost_kv_block_host_heads(pool, 10 ** 6)
+    with pytest.raises(bd.BoostError):
+        bd.boost_kv_free(pool, 12345)
+    with pytest.raises(bd.BoostError):
+        bd.boost_kv_alloc(pool, 1, 0)
+    bd.boost_kv_pool_destroy(pool)
+
+
+POOL_TRACE = json.load(open(os.path.join(os.path.dirname(__file__), "golden",
+                                         "dsr_pool_scale_example.json")))
+
+
+def test_pool_scale_worked_example(plan_ctx):
+    g = POOL_TRACE["pool"]
+    pool = make(plan_ctx, g["n_blocks"], g["H"], g["D"], g["M"])
+    try:
+        assert bd.boost_kv_pool_info(pool)["tau"] == POOL_TRACE["tau"]
+        for stp in POOL_TRACE["steps"]:
+            op = stp["op"]
+            if op == "alloc":
+                got = bd.boost_kv_alloc(pool, stp["rid"], stp["n"])
+                if stp.get("expect") == "EAGAIN":
+                    assert got == bd.EAGAIN, stp
+                elif "expect_range" in stp:
+                    assert got == list(range(*stp["expect_range"])), stp
+                else:
+                    exp = [b for r in stp["expect_ranges"] for b in range(*r)]
+                    assert got == exp, stp
+            elif op == "free":
+                bd.boost_kv_free(pool, stp["rid"])
+            elif op == "type":
+                assert bd.boost_kv_request_type(pool, stp["rid"]) == stp["expect"]
+            else:
+                s = bd.boost_kv_stats(pool)
+                assert s["used_blocks"] == stp["used_blocks"]
+                assert s["used_host_head_blocks"] == stp["used_host_head_blocks"]
+    finally:
+        bd.boost_kv_pool_destroy(pool)
+
+
+def replay(plan_ctx, nb_req, H, M, events):
+    pool = make(plan_ctx, nb_req, H, 128, M)
+    g = okv.kv_geometry(nb_req, H, 128, M)
+    shh, loc = okv.block_lists(g)
+    a = okv.DSRAllocator(shh, loc)
+    live = []
+    try:
+        for kind, rid, n in events:
+            if kind == "free":
+                if not live:
+                    continue
+                r = live[rid % len(live)]
+                a.free_request(r)
+                bd.boost_kv_free(pool, r)
+                live.remove(r)
+            else:
+                exp = a.alloc(rid, n)
+                got = bd.boost_kv_alloc(pool, rid, n)
+                assert got == exp
+                if exp != okv.EAGAIN and rid not in live:
+                    live.append(rid)
+                if rid in a.req_type:
+                    assert bd.boost_kv_request_type(pool, rid) == a.req_type[rid]
+            s = bd.boost_kv_stats(pool)
+            assert s["free_shh"] == a.n_free(okv.SHH)
+            assert s["free_local"] == a.n_free(okv.LOCAL)
+            assert s["used_blocks"] == a.in_use_blocks()
+            assert s["used_host_head_blocks"] == a.in_use_host_head_blocks(g.host_heads)
+    finally:
+        bd.boost_kv_pool_destroy(pool)
+
+
+@given(st.integers(1, 1600), st.sampled_from([1, 2, 4, 8]), st.integers(2, 40),
+       st.lists(st.tuples(st.sampled_from(["alloc", "alloc", "alloc", "free"]),
+                          st.integers(0, 30), st.integers(1, 300)),
+                min_size=1, max_size=80))
+@settings(max_examples=150, deadline=None)
+def test_decisions_match_oracle(plan_ctx, nb_req, H, M, events):
+    replay(plan_ctx, nb_req, H, M, events)
+
+
+def test_long_churn_matches_oracle(plan_ctx):
+    """Seeded admit / grow / retire churn on a config-3-shaped pool
+    (H = 8, ~9.7K blocks, M = 111): every decision bit-exact."""
+    rng = np.random.default_rng(2)
+    events = []
+    for i in range(3000):
+        r = rng.random()
+        if r < 0.45:
+            events.append(("alloc", int(rng.integers(0, 120)), int(rng.integers(32, 257))))
+        elif r < 0.75:
+            events.append(("alloc", int(rng.integers(0, 120)), 1))
+        else:
+            events.append(("free", int(rng.integers(0, 1000)), 0))
+    replay(plan_ctx, 9250, 8, 111, events)

@@ -81,3 +81,12 @@ def test_f32_close_to_f64_and_subset():
     assert np.max(np.abs(o32 - o64)) < 1e-5
     sub = oa.decode_attention(q, ks, vs, heads=[(2, 5), (0, 0)])
     assert np.array_equal(sub[(2, 5)], o64[2, 5]) and np.array_equal(sub[(0, 0)], o64[0, 0])
+
+
+def test_empty_context_gives_zero_row():
+    rng = np.random.default_rng(2)
+    q = synth.normal_bf16(rng, (2, 2, 8), 1.0)
+    ks = [np.zeros((0, 1, 8), np.uint16), synth.normal_bf16(rng, (3, 1, 8), 1.0)]
+    vs = [np.zeros((0, 1, 8), np.uint16), synth.normal_bf16(rng, (3, 1, 8), 1.0)]
+    o = oa.decode_attention(q, ks, vs)
+    assert np.all(o[0] == 0) and np.all(np.isfinite(o[1])) and np.any(o[1] != 0)

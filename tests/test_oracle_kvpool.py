@@ -178,3 +178,31 @@ def test_churn_keeps_host_share_near_target():
     # a rolling median over 50 steps never leaves a +-1.5% band
     roll = [np.median(shares[i:i + 50]) for i in range(0, len(shares) - 50, 10)]
     assert max(abs(r - 1.0 / M) for r in roll) < 0.015
+
+
+POOL_TRACE = json.load(open(os.path.join(HERE, "golden", "dsr_pool_scale_example.json")))
+
+
+def test_pool_scale_worked_example():
+    g = POOL_TRACE["pool"]
+    geom = kv.kv_geometry(g["n_blocks"], g["H"], g["D"], g["M"])
+    shh, loc = kv.block_lists(geom)
+    a = kv.DSRAllocator(shh, loc)
+    assert a.tau == POOL_TRACE["tau"]
+    for stp in POOL_TRACE["steps"]:
+        op = stp["op"]
+        if op == "alloc":
+            got = a.alloc(stp["rid"], stp["n"])
+            if stp.get("expect") == "EAGAIN":
+                assert got == kv.EAGAIN
+            elif "expect_range" in stp:
+                assert got == list(range(*stp["expect_range"]))
+            else:
+                assert got == [b for r in stp["expect_ranges"] for b in range(*r)]
+        elif op == "free":
+            a.free_request(stp["rid"])
+        elif op == "type":
+            assert a.req_type[stp["rid"]] == stp["expect"]
+        else:
+            assert a.in_use_blocks() == stp["used_blocks"]
+            assert a.in_use_host_head_blocks(geom.host_heads) == stp["used_host_head_blocks"]
