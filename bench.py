@@ -60,6 +60,7 @@ class Chain:
         self.bd, self.ctx, self.torch = bd, ctx, torch
         per_layer, head = synth.chain_shapes(synth.LLAMA8B)
         self.ops = []            # (boost handle, hbm-only handle, N, K, x, y)
+        self.views = {}          # op index -> staged view (prefetch baseline)
         self.alg_bytes = 0
         self.host_pages = 0
         self.pages = 0
@@ -84,6 +85,50 @@ class Chain:
             self.alg_bytes += nbytes + K * 2 + N * 4
         torch.cuda.synchronize()
         torch.cuda.empty_cache()
+        # prefetch baseline: a ring of two staging areas, one staged tensor
+        # copied ahead of its use on a second stream
+        self.staged = [i for i, op in enumerate(self.ops)
+                       if bd.boost_tensor_tiers(op[0]).sum()]
+        most = max([int(bd.boost_tensor_tiers(self.ops[i][0]).sum()) for i in self.staged],
+                   default=0)
+        self.ring = [torch.empty(max(1, most) * bd.PAGE_BYTES, dtype=torch.uint8,
+                                 device="cuda") for _ in range(2)]
+        for k, i in enumerate(self.staged):
+            buf = self.ring[k % 2]
+            self.views[i] = bd.boost_staged_view(ctx, self.ops[i][0], buf, buf.numel())
+        self.copy_stream = torch.cuda.Stream()
+        self.ev_ready = {i: torch.cuda.Event() for i in self.staged}
+        self.ev_free = [torch.cuda.Event(), torch.cuda.Event()]
+        self.staged_bytes = most * len(self.staged) and sum(
+            int(bd.boost_tensor_tiers(self.ops[i][0]).sum()) for i in self.staged) * bd.PAGE_BYTES
+
+    def _issue_prefetch(self, k):
+        i = self.staged[k]
+        cs = self.copy_stream
+        cs.wait_event(self.ev_free[k % 2])
+        self.bd.boost_prefetch(self.ctx, self.views[i], cs.cuda_stream)
+        self.ev_ready[i].record(cs)
+
+    def run_prefetch(self, stream_obj):
+        """One step of the prefetch baseline: staged tensors are read from
+        HBM staging after their host pages were copied in (one ahead)."""
+        bd, torch = self.bd, self.torch
+        sp = stream_obj.cuda_stream
+        for k in range(min(2, len(self.staged))):
+            self._issue_prefetch(k)
+        pos = {i: k for k, i in enumerate(self.staged)}
+        for i, (t, h, N, K, x, y) in enumerate(self.ops):
+            if i in pos:
+                k = pos[i]
+                stream_obj.wait_event(self.ev_ready[i])
+                bd.boost_decode_gemv(self.ctx, self.views[i], N, K, x, 1, y,
+                                     bd.DTYPE_F32, sp)
+                self.ev_free[k % 2].record(stream_obj)
+                if k + 2 < len(self.staged):
+                    self._issue_prefetch(k + 2)
+            else:
+                bd.boost_decode_gemv(self.ctx, t, N, K, x, 1, y, bd.DTYPE_F32, sp)
+        stream_obj.wait_stream(self.copy_stream)
 
     def run(self, which, stream, events=None):
         bd = self.bd
@@ -96,6 +141,8 @@ class Chain:
                 events[i][1].record()
 
     def free(self):
+        for v in self.views.values():
+            self.bd.boost_tensor_free(v)
         for t, h, *_ in self.ops:
             self.bd.boost_tensor_free(t)
             self.bd.boost_tensor_free(h)
@@ -111,6 +158,73 @@ def time_steps(torch, fn, steps):
         b.record()
     torch.cuda.synchronize()
     return np.array([a.elapsed_time(b) for a, b in ev])
+
+
+# --------------------------------------------------------------- attention
+def attention_bench(bd, ctx, torch, M, steps, warmup):
+    """Paged-attention decode, batch 64, 32/8 heads, head_dim 128, context
+    lengths U[512, 4096] (seed 0), K/V ~N(0, 1) bf16, blocks from the
+    wave-aware pool (linear placement at modulus M) vs an all-HBM pool."""
+    import synth
+    B, Hq, H, D = 64, 32, 8, 128
+    lengths = synth.context_lengths(0, B, 512, 4096)
+    need = [(int(L) + 15) // 16 for L in lengths]
+    mb = max(need)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(1)
+    total = int(lengths.sum())
+    k = torch.randn((total, H, D), generator=g, device="cuda").to(torch.bfloat16)
+    v = torch.randn((total, H, D), generator=g, device="cuda").to(torch.bfloat16)
+    q = torch.randn((B, Hq, D), generator=g, device="cuda").to(torch.bfloat16)
+    lens = torch.from_numpy(lengths.astype(np.int32)).cuda()
+    sp = torch.cuda.current_stream().cuda_stream
+    res = {}
+    pools = {}
+    for name, mode, m in (("boost", bd.KV_LPP, M), ("hbm", bd.KV_ALL_HBM, 0)):
+        pool = bd.boost_kv_pool_create(ctx, 1, H, D, sum(need), m, mode, q_heads=Hq,
+                                       max_batch=B, max_blocks_per_seq=mb)
+        tables = np.full((B, mb), -1, np.int32)
+        slots = []
+        for b in range(B):
+            tables[b, :need[b]] = bd.boost_kv_alloc(pool, b, need[b])
+            t = np.arange(int(lengths[b]))
+            slots.append(tables[b, t // 16] * 16 + t % 16)
+        sl = torch.from_numpy(np.concatenate(slots).astype(np.int32)).cuda()
+        bd.boost_kv_write(ctx, pool, 0, sl, k, v, total, sp)
+        st = bd.boost_kv_stats(pool)
+        pools[name] = (pool, torch.from_numpy(tables).cuda(), st)
+    del k, v
+    out = torch.empty((B, Hq, D), dtype=torch.float32, device="cuda")
+
+    def call(name):
+        pool, td, _ = pools[name]
+        bd.boost_paged_attn_decode(ctx, pool, 0, q, B, Hq, td, mb, lens, 0.0, out,
+                                   bd.DTYPE_F32, sp)
+    for _ in range(warmup):
+        call("boost")
+        call("hbm")
+    ms = {"boost": [], "hbm": []}
+    for _ in range(steps):
+        for name in ("boost", "hbm"):
+            a = torch.cuda.Event(enable_timing=True)
+            b_ = torch.cuda.Event(enable_timing=True)
+            a.record()
+            call(name)
+            b_.record()
+            torch.cuda.synchronize()
+            ms[name].append(a.elapsed_time(b_))
+    alg = total * H * D * 2 * 2 + B * Hq * D * 2 + B * Hq * D * 4
+    st = pools["boost"][2]
+    for name in ("boost", "hbm"):
+        t = float(np.median(ms[name]))
+        res[name] = {"ms": round(t, 4), "gbps": round(alg / (t * 1e-3) / 1e9, 1)}
+    res["host_share"] = round(st["used_host_head_blocks"] / (H * st["used_blocks"]), 5)
+    res["shh_requests"] = int(st["shh_requests"])
+    res["alg_bytes"] = int(alg)
+    res["speedup_vs_hbm_only"] = round(res["hbm"]["ms"] / res["boost"]["ms"], 4)
+    for pool, _, _ in pools.values():
+        bd.boost_kv_pool_destroy(pool)
+    return res
 
 
 # ----------------------------------------------------------- CPU baseline
@@ -191,16 +305,18 @@ def main():
     log("step: timed")
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    boost_ms, hbm_ms = [], []
+    boost_ms, hbm_ms, pre_ms = [], [], []
     for i in range(args.steps):
-        # interleaved A/B so both see the same clocks and thermal state
+        # interleaved A/B/C so all see the same clocks and thermal state
         boost_ms.append(time_steps(torch, lambda: step("boost"), 1)[0])
         hbm_ms.append(time_steps(torch, lambda: step("hbm"), 1)[0])
+        pre_ms.append(time_steps(torch, lambda: chain.run_prefetch(stream), 1)[0])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    boost_ms, hbm_ms = np.array(boost_ms), np.array(hbm_ms)
+    boost_ms, hbm_ms, pre_ms = np.array(boost_ms), np.array(hbm_ms), np.array(pre_ms)
     ms = float(np.median(boost_ms))
     ms_hbm = float(np.median(hbm_ms))
+    ms_pre = float(np.median(pre_ms))
 
     # per-launch durations of the GEMV kernel (roofline of the dominant kernel)
     log("step: per-launch timing")
@@ -223,6 +339,8 @@ def main():
         torch.cuda.synchronize()
         del a, b
 
+    log("step: attention")
+    attn = attention_bench(bd, ctx, torch, M, max(10, args.steps), 3)
     eff = chain.alg_bytes / (ms * 1e-3) / 1e9
     eff_hbm = chain.alg_bytes / (ms_hbm * 1e-3) / 1e9
     host_share = chain.host_pages / chain.pages
@@ -263,6 +381,11 @@ def main():
         "hbm_only": {"ms_per_step": round(ms_hbm, 4), "value": round(eff_hbm, 2),
                      "pct_of_hbm_roofline": round(100 * eff_hbm / bw_hbm, 2)},
         "speedup_vs_hbm_only": round(ms_hbm / ms, 4),
+        "prefetch": {"ms_per_step": round(ms_pre, 4),
+                     "value": round(chain.alg_bytes / (ms_pre * 1e-3) / 1e9, 2),
+                     "staged_tensors": len(chain.staged),
+                     "staged_bytes_per_step": int(chain.staged_bytes)},
+        "attention": attn,
         "step_ms_iqr": [round(float(np.percentile(boost_ms, 25)), 4),
                         round(float(np.percentile(boost_ms, 75)), 4)],
         "roofline": {"bound": "hbm", "kernel": "gemv_kernel<1,2,4>",

@@ -158,6 +158,25 @@ int boost_tensor_read(const boost_tensor *t, uint64_t offset, void *dst,
 
 int boost_tensor_free(boost_tensor *t);
 
+/* ------------------------------------------- a6: prefetch-to-HBM baseline */
+
+/* Prefetch baseline (§2.5 "Prefetching", §5.1 evaluated policies): data that
+ * lives on host is copied into HBM before use and read from there, so every
+ * staged byte also costs an HBM write.  boost_staged_view makes a view of a
+ * placed tensor whose HBM pages are the tensor's own and whose host pages are
+ * replaced by staging pages in caller-owned device memory `staging` (at least
+ * n_host_pages * 2 MiB bytes, 16-byte aligned).  The view holds no copy of the
+ * HBM pages, must be freed (boost_tensor_free) before the tensor, and reads
+ * only HBM in decode calls.  Errors: EINVAL (staging too small), ENODEV, EHIP. */
+int boost_staged_view(boost_ctx *ctx, const boost_tensor *t, void *staging,
+                      uint64_t staging_bytes, boost_tensor **view);
+
+/* Copy the source tensor's host pages into the view's staging pages
+ * (host-to-device DMA) on `stream`; a decode call on the view ordered after
+ * it reads the staged bytes.  No-op for a view of a tensor with no host page.
+ * Errors: EINVAL (not a view), EHIP. */
+int boost_prefetch(boost_ctx *ctx, const boost_tensor *view, void *stream);
+
 /* ------------------------------------------------------ a4: decode GEMV */
 
 /* Work-unit schedule of the GEMV (library-wide):

@@ -78,6 +78,8 @@ _SIGS = {
     "boost_tensor_read": (_i32, [_vp, _u64, _vp, _u64]),
     "boost_tensor_free": (_i32, [_vp]),
     "boost_gemv_set_schedule": (_i32, [_vp, _i32, _i32]),
+    "boost_staged_view": (_i32, [_vp, _vp, _vp, _u64, C.POINTER(_vp)]),
+    "boost_prefetch": (_i32, [_vp, _vp, _vp]),
     "boost_kv_pool_create": (_i32, [_vp, C.POINTER(KVCfg), C.POINTER(_vp)]),
     "boost_kv_pool_info": (_i32, [_vp, C.POINTER(KVInfo)]),
     "boost_kv_pool_destroy": (_i32, [_vp]),
@@ -268,6 +270,17 @@ def boost_tensor_read(t: int, offset: int, nbytes: int) -> np.ndarray:
 
 def boost_tensor_free(t: int):
     _check(load().boost_tensor_free(t))
+
+
+# ------------------------------------------------------- prefetch baseline
+def boost_staged_view(ctx: int, t: int, staging, staging_bytes: int) -> int:
+    h = _vp()
+    _check(load().boost_staged_view(ctx, t, _ptr(staging), staging_bytes, C.byref(h)))
+    return h.value
+
+
+def boost_prefetch(ctx: int, view: int, stream=None):
+    _check(load().boost_prefetch(ctx, view, _stream(stream)))
 
 
 # -------------------------------------------------------------------- GEMV

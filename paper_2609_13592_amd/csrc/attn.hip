@@ -32,11 +32,24 @@ constexpr int kThreads = 256;
 constexpr int kD = 128;          // head dimension of this kernel
 constexpr int kT = 16;           // tokens per block
 constexpr int kLanesTok = kD / 8;  // lanes per token row (16)
-constexpr int kUnroll = 4;       // blocks in flight per workgroup
+#ifndef BOOST_ATTN_UNROLL
+#define BOOST_ATTN_UNROLL 4
+#endif
+#ifndef BOOST_ATTN_ITEMS
+#define BOOST_ATTN_ITEMS 2048
+#endif
+constexpr int kUnroll = BOOST_ATTN_UNROLL;  // blocks in flight per workgroup
+constexpr int kMaxPartBlocks = 256;         // blocks per partition, at most
 
 struct AttnParams {
-  const char* const* pk;  // page table of this layer's K tensor
-  const char* const* pv;  // ... and V tensor
+  // Linear placement makes the tier of a pool page a fixed function of its
+  // offset: pages [0, first_host) of a tensor are consecutive in the HBM slab
+  // and pages [first_host, pages) consecutive in the host slab.
+  const char* k_hbm;   // this layer's K tensor: first HBM page
+  const char* k_host;  // ... first host page
+  const char* v_hbm;
+  const char* v_host;
+  uint64_t host_from;  // byte offset where the tensor's host tail begins
   const uint16_t* q;      // [B, Hq, D]
   const int32_t* tables;  // [B, max_blocks]
   const int32_t* lens;    // [B]
@@ -76,6 +89,31 @@ __device__ __forceinline__ uint4 load_block(const char* base, bool ok, uint32_t 
   return *reinterpret_cast<uint4*>(&v);
 }
 
+// Sum over the 16 lanes of a DPP row.  Every lane ends with the same bits:
+// each step adds a lane's value to its partner's, and the partners' values are
+// equal-by-construction from the previous step (xor 1, xor 2 within a quad,
+// then the mirrored quad, then the mirrored half-row).
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+  // bound_ctrl set: these patterns never leave the 16-lane row, and it lets
+  // the move fold into the add (v_add_f32_dpp)
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xf, 0xf, true));
+}
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
+// a.lo * b.lo + a.hi * b.hi + c with two bf16 pairs packed in 32 bits
+__device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a),
+                                         __builtin_bit_cast(bf16x2_t, b), c, false);
+}
+
+__device__ __forceinline__ float row16_sum(float v) {
+  v += dpp<0xb1>(v);   // quad_perm [1,0,3,2]
+  v += dpp<0x4e>(v);   // quad_perm [2,3,0,1]
+  v += dpp<0x141>(v);  // row_half_mirror
+  v += dpp<0x140>(v);  // row_mirror
+  return v;
+}
+
 // merge running state (m, l, acc) with another one; symmetric in its operands
 template <int G>
 __device__ __forceinline__ void merge_state(float* m, float* l, float (*acc)[8],
@@ -85,12 +123,62 @@ __device__ __forceinline__ void merge_state(float* m, float* l, float (*acc)[8],
   for (int j = 0; j < G; ++j) {
     const float M = fmaxf(m[j], m2[j]);
     if (M == -INFINITY) continue;  // both empty
-    const float c1 = m[j] == -INFINITY ? 0.f : __expf(m[j] - M);
-    const float c2 = m2[j] == -INFINITY ? 0.f : __expf(m2[j] - M);
+    const float c1 = __builtin_amdgcn_exp2f(m[j] - M);  // m = -inf gives 0
+    const float c2 = __builtin_amdgcn_exp2f(m2[j] - M);
     l[j] = l[j] * c1 + l2[j] * c2;
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[j][e] = acc[j][e] * c1 + acc2[j][e] * c2;
     m[j] = M;
+  }
+}
+
+// Online-softmax update of one token slot with U blocks.  Scores are in the
+// log2 domain (q . k * scale * log2 e), so exp2 is one instruction.  With
+// MASKED false every token is valid; otherwise invalid tokens have score -inf
+// and contribute nothing.
+template <int G, int U, bool MASKED>
+__device__ __forceinline__ void consume(const uint32_t (*qp)[4], const uint4* kb,
+                                        const uint4* vb, const bool* valid, float sc2,
+                                        float* m, float* l, float (*acc)[8]) {
+  float sc[U][G];
+#pragma unroll
+  for (int u = 0; u < U; ++u)
+#pragma unroll
+    for (int j = 0; j < G; ++j) {
+      float d = dot2(qp[j][0], kb[u].x, 0.f);
+      d = dot2(qp[j][1], kb[u].y, d);
+      d = dot2(qp[j][2], kb[u].z, d);
+      d = dot2(qp[j][3], kb[u].w, d);
+      d = row16_sum(d) * sc2;  // q . k over the 16 lanes of the token row
+      sc[u][j] = (!MASKED || valid[u]) ? d : -INFINITY;
+    }
+#pragma unroll
+  for (int j = 0; j < G; ++j) {
+    float mc = m[j];
+#pragma unroll
+    for (int u = 0; u < U; ++u) mc = fmaxf(mc, sc[u][j]);
+    if (MASKED && mc == -INFINITY) continue;  // nothing valid yet
+    const float c = __builtin_amdgcn_exp2f(m[j] - mc);  // exp2(-inf) = 0 at start
+    l[j] *= c;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[j][e] *= c;
+    m[j] = mc;
+  }
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    float vf[8];
+    unpack8(vb[u], vf);
+#pragma unroll
+    for (int j = 0; j < G; ++j) {
+      // masked: an invalid token (score -inf) weighs 0, also while the
+      // running max is still -inf
+      const float p = (MASKED && sc[u][j] == -INFINITY)
+                          ? 0.f
+                          : __builtin_amdgcn_exp2f(sc[u][j] - m[j]);
+      l[j] += p;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[j][e] = fmaf(p, vf[e], acc[j][e]);
+    }
   }
 }
 
@@ -109,17 +197,24 @@ __global__ __launch_bounds__(kThreads) void attn_partition(AttnParams P) {
   const int n_blk = min((L + kT - 1) / kT, P.max_blocks);
   const int blk_beg = part * P.part_blocks;
   if (L <= 0 || blk_beg >= n_blk) return;  // uniform: empty partition
-  const int blk_end = min(n_blk, blk_beg + P.part_blocks);
+  const int nbp = min(n_blk, blk_beg + P.part_blocks) - blk_beg;
+  // leading blocks whose 16 tokens are all inside the context
+  const int nfull = max(0, min(nbp, L / kT - blk_beg));
+  const int32_t* row = P.tables + static_cast<int64_t>(b) * P.max_blocks + blk_beg;
+  const uint64_t head_off = static_cast<uint64_t>(g) * P.nb * (kT * kD * 2);
 
-  float qf[G][8];
+  // q stays in bf16 pairs for the dot2 instruction
+  uint32_t qp[G][4];
 #pragma unroll
   for (int j = 0; j < G; ++j) {
     const uint4 u = *reinterpret_cast<const uint4*>(
         P.q + (static_cast<int64_t>(b) * P.Hq + g * G + j) * kD + dc * 8);
-    unpack8(u, qf[j]);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) qf[j][e] *= P.scale;
+    qp[j][0] = u.x;
+    qp[j][1] = u.y;
+    qp[j][2] = u.z;
+    qp[j][3] = u.w;
   }
+  const float sc2 = P.scale * 1.4426950408889634f;  // log2(e)
   float m[G], l[G], acc[G][8];
 #pragma unroll
   for (int j = 0; j < G; ++j) {
@@ -129,52 +224,32 @@ __global__ __launch_bounds__(kThreads) void attn_partition(AttnParams P) {
     for (int e = 0; e < 8; ++e) acc[j][e] = 0.f;
   }
 
-  const int32_t* row = P.tables + static_cast<int64_t>(b) * P.max_blocks;
   const uint32_t lane_off = static_cast<uint32_t>(tid) * 16;
-  for (int i = blk_beg; i < blk_end; i += kUnroll) {
-    uint4 kv[kUnroll], vv[kUnroll];
+  // address of head-block (g, blk) of K and V: uniform scalar arithmetic
+  auto fetch = [&](int bi, uint4& kq, uint4& vq) {
+    const int32_t blk = row[bi];
+    const bool ok = blk >= 0 && blk < P.nb;
+    const uint64_t byte = head_off + static_cast<uint64_t>(ok ? blk : 0) * (kT * kD * 2);
+    const bool host = byte >= P.host_from;
+    const uint64_t off = host ? byte - P.host_from : byte;
+    kq = load_block((host ? P.k_host : P.k_hbm) + off, ok, lane_off);
+    vq = load_block((host ? P.v_host : P.v_hbm) + off, ok, lane_off);
+  };
+  bool valid[kUnroll];
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const int bi = i + u;
-      const int32_t blk = bi < blk_end ? row[bi] : -1;
-      const bool ok = blk >= 0 && blk < P.nb;
-      const uint64_t byte = ok ? (static_cast<uint64_t>(g) * P.nb + blk) * (kT * kD * 2) : 0;
-      const uint64_t page = byte >> 21, in = byte & (bst::kPage - 1);
-      kv[u] = load_block(P.pk[page] + in, ok, lane_off);
-      vv[u] = load_block(P.pv[page] + in, ok, lane_off);
-    }
+  for (int u = 0; u < kUnroll; ++u) valid[u] = true;
+  int i = 0;
+  for (; i + kUnroll <= nfull; i += kUnroll) {
+    uint4 kb[kUnroll], vb[kUnroll];
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const int t = (i + u) * kT + ts;  // token of this lane's slot
-      float kf[8], vf[8];
-      unpack8(kv[u], kf);
-      unpack8(vv[u], vf);
-      float s[G];
-#pragma unroll
-      for (int j = 0; j < G; ++j) {
-        float d = 0.f;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) d = fmaf(qf[j][e], kf[e], d);
-        // sum over the 16 lanes of this token row (fixed butterfly)
-        d += __shfl_xor(d, 8, 64);
-        d += __shfl_xor(d, 4, 64);
-        d += __shfl_xor(d, 2, 64);
-        d += __shfl_xor(d, 1, 64);
-        s[j] = d;
-      }
-      if (i + u < blk_end && t < L) {  // uniform over the 16 lanes of the slot
-#pragma unroll
-        for (int j = 0; j < G; ++j) {
-          const float mn = fmaxf(m[j], s[j]);
-          const float c = m[j] == -INFINITY ? 0.f : __expf(m[j] - mn);
-          const float p = __expf(s[j] - mn);
-          l[j] = l[j] * c + p;
-#pragma unroll
-          for (int e = 0; e < 8; ++e) acc[j][e] = fmaf(p, vf[e], acc[j][e] * c);
-          m[j] = mn;
-        }
-      }
-    }
+    for (int u = 0; u < kUnroll; ++u) fetch(i + u, kb[u], vb[u]);
+    consume<G, kUnroll, false>(qp, kb, vb, valid, sc2, m, l, acc);
+  }
+  for (; i < nbp; ++i) {  // remaining blocks, the last one possibly partial
+    uint4 kb[1], vb[1];
+    fetch(i, kb[0], vb[0]);
+    const bool v1[1] = {(blk_beg + i) * kT + ts < L};
+    consume<G, 1, true>(qp, kb, vb, v1, sc2, m, l, acc);
   }
 
   // merge the 4 slots of a wavefront (lanes 16 and 32 apart hold the same dims)
@@ -245,7 +320,7 @@ __global__ __launch_bounds__(64) void attn_merge(AttnParams P) {
   for (int p = 0; p < np; ++p) {
     const float mp = P.part_ml[(base + p) * 2];
     if (mp == -INFINITY) continue;
-    const float w = __expf(mp - M);
+    const float w = __builtin_amdgcn_exp2f(mp - M);  // maxima are in the log2 domain
     den = fmaf(P.part_ml[(base + p) * 2 + 1], w, den);
     const float2 a = *reinterpret_cast<const float2*>(P.part_acc + (base + p) * kD + lane * 2);
     o0 = fmaf(a.x, w, o0);
@@ -304,9 +379,13 @@ int boost_paged_attn_decode(boost_ctx* ctx, const boost_kv_pool* pool, int layer
   const int H = static_cast<int>(c.kv_heads);
   const int G = Hq / H;
   AttnParams P{};
-  const uint64_t pages = pool->geom.pages;
-  P.pk = pool->d_page_table + (2ull * layer) * pages;
-  P.pv = pool->d_page_table + (2ull * layer + 1) * pages;
+  const uint64_t pages = pool->geom.pages, hp = pool->geom.host_pages;
+  const uint64_t tk = 2ull * layer, tv = 2ull * layer + 1;  // tensor indices
+  P.k_hbm = pool->hbm.base + tk * (pages - hp) * kPage;
+  P.v_hbm = pool->hbm.base + tv * (pages - hp) * kPage;
+  P.k_host = hp ? pool->host.base + tk * hp * kPage : P.k_hbm;
+  P.v_host = hp ? pool->host.base + tv * hp * kPage : P.v_hbm;
+  P.host_from = (pages - hp) * kPage;
   P.q = static_cast<const uint16_t*>(q);
   P.tables = block_tables;
   P.lens = ctx_lens;
@@ -315,9 +394,11 @@ int boost_paged_attn_decode(boost_ctx* ctx, const boost_kv_pool* pool, int layer
   P.Hq = Hq;
   P.nb = static_cast<int>(pool->geom.nb);
   P.max_blocks = max_blocks;
-  // about 2048 work items when the context allows it; at least 4 blocks each
-  const int want_parts = std::max(1, (2048 + B * H - 1) / (B * H));
-  P.part_blocks = std::max(4, (max_blocks + want_parts - 1) / want_parts);
+  // enough work items to fill the GPU several times over (so the last grid
+  // wave is short), at least 4 blocks each
+  const int want_parts = std::max(1, (BOOST_ATTN_ITEMS + B * H - 1) / (B * H));
+  P.part_blocks = std::min(kMaxPartBlocks,
+                           std::max(4, (max_blocks + want_parts - 1) / want_parts));
   P.n_parts = (max_blocks + P.part_blocks - 1) / P.part_blocks;
   P.max_parts = pool->max_parts;
   if (P.n_parts > P.max_parts) return fail(BOOST_EINVAL, "partition scratch too small");

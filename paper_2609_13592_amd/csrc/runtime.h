@@ -50,6 +50,11 @@ struct boost_tensor {
   int32_t* d_hbm_pages = nullptr;       // HBM page ids, ascending
   int32_t* d_host_pages = nullptr;      // host page ids, ascending
   float* d_partial = nullptr;           // split-row partial sums
+  // staged views (prefetch baseline): source host pages and their staging
+  const boost_tensor* staged_from = nullptr;
+  const char* stage_src = nullptr;      // host VA of the source's host pages
+  char* stage_dst = nullptr;            // device staging area
+  uint64_t stage_bytes = 0;
 };
 
 namespace bst {

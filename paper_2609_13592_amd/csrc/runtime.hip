@@ -258,4 +258,56 @@ int boost_tensor_read(const boost_tensor* t, uint64_t offset, void* dst,
 
 int boost_tensor_free(boost_tensor* t) { return free_tensor(t); }
 
+int boost_staged_view(boost_ctx* ctx, const boost_tensor* t, void* staging,
+                      uint64_t staging_bytes, boost_tensor** view) {
+  if (!ctx || !t || !view) return fail(BOOST_EINVAL, "null argument");
+  if (ctx->device < 0) return fail(BOOST_ENODEV, "plan-only context");
+  if (t->staged_from) return fail(BOOST_EINVAL, "cannot stage a staged view");
+  const uint64_t need = t->host_pages.size() * kPage;
+  if (need && (!staging || staging_bytes < need))
+    return fail(BOOST_EINVAL, "staging needs %llu bytes", (unsigned long long)need);
+  if (reinterpret_cast<uintptr_t>(staging) & 15)
+    return fail(BOOST_EINVAL, "staging must be 16-byte aligned");
+  BOOST_HIP(hipSetDevice(ctx->device));
+  auto* v = new boost_tensor();
+  v->ctx = ctx;
+  v->bytes = t->bytes;
+  v->n_pages = t->n_pages;
+  v->tiers.assign(t->n_pages, BOOST_TIER_HBM);
+  v->page_ptr = t->page_ptr;
+  v->copy_ptr = t->copy_ptr;
+  for (size_t i = 0; i < t->host_pages.size(); ++i) {
+    v->page_ptr[t->host_pages[i]] = static_cast<char*>(staging) + i * kPage;
+    v->copy_ptr[t->host_pages[i]] = v->page_ptr[t->host_pages[i]];
+  }
+  for (uint64_t i = 0; i < t->n_pages; ++i) v->hbm_pages.push_back(static_cast<int32_t>(i));
+  v->staged_from = t;
+  v->stage_src = t->host.host_base;
+  v->stage_dst = static_cast<char*>(staging);
+  v->stage_bytes = need;
+  const size_t nb = t->n_pages + 1;
+  int r = upload(reinterpret_cast<void**>(&v->d_page_table), v->page_ptr.data(),
+                 v->n_pages * sizeof(char*));
+  if (!r) r = upload(reinterpret_cast<void**>(&v->d_hbm_pages), v->hbm_pages.data(),
+                     v->hbm_pages.size() * sizeof(int32_t));
+  if (!r) r = upload(reinterpret_cast<void**>(&v->d_host_pages), nullptr, 0);
+  if (!r) r = upload(reinterpret_cast<void**>(&v->d_partial), nullptr,
+                     nb * 2 * kMaxGemvBatch * sizeof(float));
+  if (r) {
+    free_tensor(v);
+    return r;
+  }
+  *view = v;
+  return BOOST_OK;
+}
+
+int boost_prefetch(boost_ctx* ctx, const boost_tensor* view, void* stream) {
+  if (!ctx || !view) return fail(BOOST_EINVAL, "null argument");
+  if (!view->staged_from) return fail(BOOST_EINVAL, "not a staged view");
+  if (view->stage_bytes == 0) return BOOST_OK;
+  BOOST_HIP(hipMemcpyAsync(view->stage_dst, view->stage_src, view->stage_bytes,
+                           hipMemcpyHostToDevice, static_cast<hipStream_t>(stream)));
+  return BOOST_OK;
+}
+
 }  // extern "C"

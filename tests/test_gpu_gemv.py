@@ -187,3 +187,30 @@ def test_full_size_chain_tensor_sampled(gpu_ctx, kind):
         bd.boost_tensor_free(t)
         del wt, w_dev
         torch.cuda.empty_cache()
+
+
+def test_prefetch_staged_view(gpu_ctx):
+    """The prefetch baseline's staged view reads the copied host pages from
+    HBM staging and gives the same bits as the tiered tensor."""
+    import torch
+    N, K = 3000, 4096
+    w, x = synth.gemv_inputs(31, N, K, 1)
+    t = place(gpu_ctx, w, M=2)
+    n_host = int(bd.boost_tensor_tiers(t).sum())
+    staging = torch.empty(n_host * opl.PAGE, dtype=torch.uint8, device="cuda")
+    v = bd.boost_staged_view(gpu_ctx, t, staging, staging.numel())
+    try:
+        assert not bd.boost_tensor_tiers(v).any()
+        xd = to_dev_u16(x)
+        bd.boost_prefetch(gpu_ctx, v, stream())
+        yv = run_gemv(gpu_ctx, v, N, K, xd, 1)
+        yt = run_gemv(gpu_ctx, t, N, K, xd, 1)
+        assert np.array_equal(yv.view(np.uint32), yt.view(np.uint32))
+        assert og.rel_err(yv, og.gemv_f64(w, x)) <= TOL
+        with pytest.raises(bd.BoostError):
+            bd.boost_staged_view(gpu_ctx, t, staging, staging.numel() - 16)
+        with pytest.raises(bd.BoostError):
+            bd.boost_prefetch(gpu_ctx, t, stream())
+    finally:
+        bd.boost_tensor_free(v)
+        bd.boost_tensor_free(t)
