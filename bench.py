@@ -222,9 +222,31 @@ def attention_bench(bd, ctx, torch, M, steps, warmup):
     res["shh_requests"] = int(st["shh_requests"])
     res["alg_bytes"] = int(alg)
     res["speedup_vs_hbm_only"] = round(res["hbm"]["ms"] / res["boost"]["ms"], 4)
+    ach = alg / (res["boost"]["ms"] * 1e-3) / 1e9
+    res["roofline"] = {"bound": "hbm", "kernel": "attn_partition + attn_merge",
+                       "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                       "frac": round(ach / HBM_PEAK_GBPS, 4),
+                       "traffic": counter_traffic("attn_partition", "attn.hip")}
     for pool, _, _ in pools.values():
         bd.boost_kv_pool_destroy(pool)
     return res
+
+
+# ------------------------------------------------------------ traffic data
+def counter_traffic(kernel: str, source: str):
+    """HBM bytes per launch from the committed FETCH_SIZE / WRITE_SIZE summary
+    (profiles/traffic_counters.json), or None when the kernel source changed
+    since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "traffic_counters.json")
+    try:
+        data = json.load(open(path))[kernel]
+        src = open(os.path.join(ROOT, "paper_2609_13592_amd", "csrc", source), "rb").read()
+    except (OSError, KeyError, ValueError):
+        return None
+    if hashlib.sha256(src).hexdigest() != data["source_sha256"]:
+        return None
+    return int(data["traffic_bytes_per_launch"])
 
 
 # ----------------------------------------------------------- CPU baseline
@@ -388,10 +410,10 @@ def main():
         "attention": attn,
         "step_ms_iqr": [round(float(np.percentile(boost_ms, 25)), 4),
                         round(float(np.percentile(boost_ms, 75)), 4)],
-        "roofline": {"bound": "hbm", "kernel": "gemv_kernel<1,2,4>",
+        "roofline": {"bound": "hbm", "kernel": "gemv_kernel (batch 1) + split_fixup",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
-                     "traffic": None,
+                     "traffic": counter_traffic("gemv", "gemv.hip"),
                      "avg_launch_us": round(avg_launch_ms * 1e3, 3),
                      "bytes_per_launch": int(bytes_per_launch)},
         "cpu_baseline": cpu,

@@ -147,7 +147,7 @@ def test_brute_force_event_orders(n_shh, n_loc):
 
 
 def test_churn_keeps_host_share_near_target():
-    """§5.10: under churn the realised host share of in-use KV stays within
+    """§5.11: under churn the realised host share of in-use KV stays within
     about 1% of the configured 1/M (four KV heads, modulus 12)."""
     H, M = 4, 12
     geom = kv.kv_geometry(512 * 3 * 4, H, 128, M)
