@@ -34,8 +34,10 @@ constexpr int64_t kPageElems = static_cast<int64_t>(bst::kPage / 2);
 
 struct GemvParams {
   const char* const* page_table;
+  const uint8_t* tiers;  // tier of every page
   const int32_t* hbm_pages;
   const int32_t* host_pages;
+  int n_pages;
   int n_hbm_pages;
   int n_host_pages;
   int units_per_page;
@@ -122,52 +124,15 @@ __device__ __forceinline__ uint4 load16(__amdgpu_buffer_rsrc_t r, uint32_t off) 
 // 2 MiB, x is at most 8 * 512 K elements), so the load returns zero.
 constexpr uint32_t kOOB = 0x80000000u;
 
-// One unit: a group of rows of page `page`, restricted to the page's bytes.
-// The wavefronts of the workgroup form (kWaves / KS) row slots of RW rows;
-// the KS wavefronts of a slot split K into KS contiguous column ranges
-// (split-K inside the workgroup) and combine their partial sums through LDS
-// in a fixed order.  The page's buffer resource covers exactly its valid
-// bytes, so columns of a cut row that lie on the neighbouring page, and
-// columns past K, read as zero without a branch.
-template <int B, int RW, int UN, int KS>
-__device__ void gemv_unit(const GemvParams& P, int page, int j, float* lds) {
-  constexpr int kSlots = kWaves / KS;
-  constexpr int kRowsWg = kSlots * RW;
-  const int64_t K = P.K;
-  const int64_t total = static_cast<int64_t>(P.N) * K;
-  const int64_t pe0 = static_cast<int64_t>(page) * kPageElems;
-  const int64_t pe1 = min(pe0 + kPageElems, total);
-  const int64_t r_lo = pe0 / K;
-  const int64_t r_hi = (pe1 - 1) / K;  // inclusive
-  const int64_t rbase = r_lo + static_cast<int64_t>(j) * kRowsWg;
-  if (rbase > r_hi) return;  // uniform over the workgroup
-  const int wave = threadIdx.x >> 6;
-  const int lane = threadIdx.x & 63;
-  const int slot = wave / KS, part = wave % KS;
-  const int64_t r0 = rbase + slot * RW;
-
-  const __amdgpu_buffer_rsrc_t wr =
-      make_rsrc(P.page_table[page], static_cast<uint32_t>((pe1 - pe0) * 2));
-  const __amdgpu_buffer_rsrc_t xr =
-      make_rsrc(P.x, static_cast<uint32_t>(B * K * 2));
-  uint32_t ro[RW];  // byte offset of column 0 of each row from the page start
-#pragma unroll
-  for (int i = 0; i < RW; ++i) {
-    const int64_t r = r0 + i;
-    ro[i] = r <= r_hi ? static_cast<uint32_t>((r * K - pe0) * 2) : kOOB;
-  }
-
-  float acc[RW][B];
-#pragma unroll
-  for (int i = 0; i < RW; ++i)
-#pragma unroll
-    for (int b = 0; b < B; ++b) acc[i][b] = 0.f;
-
+// Accumulate this wavefront's columns [k_beg, k_end) of its RW rows from
+// the page behind resource wr; row i's column 0 sits at byte offset ro[i]
+// (offsets outside the page read as zero).
+template <int B, int RW, int UN>
+__device__ __forceinline__ void accumulate(__amdgpu_buffer_rsrc_t wr,
+                                           __amdgpu_buffer_rsrc_t xr, const uint32_t* ro,
+                                           int64_t K, int64_t k_beg, int64_t k_end, int lane,
+                                           float (*acc)[B]) {
   constexpr int kStep = 64 * 8;  // columns covered by one load of a wavefront
-  // this wavefront's columns: [k_beg, k_end), k_beg a multiple of kStep
-  const int64_t kper = (((K + KS - 1) / KS) + kStep - 1) / kStep * kStep;
-  const int64_t k_beg = part * kper;
-  const int64_t k_end = min(K, k_beg + kper);
   for (int64_t kb = k_beg; kb < k_end; kb += kStep * UN) {
     uint4 wv[UN][RW], xv[UN][B];
 #pragma unroll
@@ -188,31 +153,124 @@ __device__ void gemv_unit(const GemvParams& P, int page, int j, float* lds) {
 #pragma unroll
         for (int b = 0; b < B; ++b) acc[i][b] = dot8(wv[u][i], xv[u][b], acc[i][b]);
   }
+}
 
-  float v[RW][B];
+// One unit: a group of rows of page `page`, restricted to the page's bytes.
+// The wavefronts of the workgroup form (kWaves / KS) row slots of RW rows;
+// the KS wavefronts of a slot split K into KS contiguous column ranges
+// (split-K inside the workgroup) and combine their partial sums through LDS
+// in a fixed order.  The page's buffer resource covers exactly its valid
+// bytes, so columns of a cut row that lie on the neighbouring page, and
+// columns past K, read as zero without a branch.
+//
+// A row cut by a page boundary belongs to the earlier page's unit when both
+// pages are in the same tier (it reads the next page too and adds the two
+// parts itself); when the tiers differ each page's unit stores its part and
+// split_fixup adds them, so no workgroup ever reads two tiers.
+template <int B, int RW, int UN, int KS>
+__device__ void gemv_unit(const GemvParams& P, int page, int j, float* lds) {
+  constexpr int kSlots = kWaves / KS;
+  constexpr int kRowsWg = kSlots * RW;
+  const int64_t K = P.K;
+  const int64_t total = static_cast<int64_t>(P.N) * K;
+  const int64_t pe0 = static_cast<int64_t>(page) * kPageElems;
+  const int64_t pe1 = min(pe0 + kPageElems, total);
+  const int64_t r_lo = pe0 / K;
+  const int64_t r_hi = (pe1 - 1) / K;  // inclusive
+  const int64_t rbase = r_lo + static_cast<int64_t>(j) * kRowsWg;
+  if (rbase > r_hi) return;  // uniform over the workgroup
+  const int wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int slot = wave / KS, part = wave % KS;
+  const int64_t r0 = rbase + slot * RW;
+  // tiers are read only by the (few) units that hold a row cut by a page
+  // boundary, so the common unit starts its loads without waiting on them
+  const bool cut_first = rbase == r_lo && r_lo * K < pe0;
+  const bool cut_last = rbase + kRowsWg > r_hi && (r_hi + 1) * K > pe1;
+  bool prev_same = false, next_same = false;
+  if (cut_first || cut_last) {
+    const uint8_t tier = P.tiers[page];
+    prev_same = cut_first && P.tiers[page - 1] == tier;
+    next_same = cut_last && page + 1 < P.n_pages && P.tiers[page + 1] == tier;
+  }
+
+  const __amdgpu_buffer_rsrc_t wr =
+      make_rsrc(P.page_table[page], static_cast<uint32_t>((pe1 - pe0) * 2));
+  const __amdgpu_buffer_rsrc_t xr =
+      make_rsrc(P.x, static_cast<uint32_t>(B * K * 2));
+  // 0 = whole row here, 1 = tail of a row begun on the previous page,
+  // 2 = head of a row ending on the next page, 3 = skipped
+  int kind[RW];
+  uint32_t ro[RW], ro2[RW];
+  bool join = false;
+#pragma unroll
+  for (int i = 0; i < RW; ++i) {
+    const int64_t r = r0 + i;
+    const int64_t e0 = r * K;
+    kind[i] = r > r_hi ? 3 : (e0 < pe0 ? (prev_same ? 3 : 1) : (e0 + K > pe1 ? 2 : 0));
+    ro[i] = kind[i] == 3 ? kOOB : static_cast<uint32_t>((e0 - pe0) * 2);
+    ro2[i] = kOOB;
+    if (kind[i] == 2 && next_same) {
+      ro2[i] = static_cast<uint32_t>((e0 - pe1) * 2);  // wraps: columns before pe1 read 0
+      join = true;
+    }
+  }
+
+  float acc[RW][B], acc2[RW][B];
 #pragma unroll
   for (int i = 0; i < RW; ++i)
 #pragma unroll
-    for (int b = 0; b < B; ++b) v[i][b] = wave_sum(acc[i][b]);
+    for (int b = 0; b < B; ++b) acc[i][b] = acc2[i][b] = 0.f;
+
+  constexpr int kStep = 64 * 8;
+  // this wavefront's columns: [k_beg, k_end), k_beg a multiple of kStep
+  const int64_t kper = (((K + KS - 1) / KS) + kStep - 1) / kStep * kStep;
+  const int64_t k_beg = part * kper;
+  const int64_t k_end = min(K, k_beg + kper);
+  accumulate<B, RW, UN>(wr, xr, ro, K, k_beg, k_end, lane, acc);
+  if (join) {  // uniform over the slot (same rows, same page): the next page's part
+    const int64_t pe2 = min(pe1 + kPageElems, total);
+    const __amdgpu_buffer_rsrc_t wr2 =
+        make_rsrc(P.page_table[page + 1], static_cast<uint32_t>((pe2 - pe1) * 2));
+    accumulate<B, RW, UN>(wr2, xr, ro2, K, k_beg, k_end, lane, acc2);
+  }
+
+  float v[RW][B], v2[RW][B];
+#pragma unroll
+  for (int i = 0; i < RW; ++i)
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+      v[i][b] = wave_sum(acc[i][b]);
+      v2[i][b] = join ? wave_sum(acc2[i][b]) : 0.f;
+    }
 
   if constexpr (KS > 1) {
     // partial sums of the KS column ranges meet in LDS; the slot's first
-    // wavefront adds them in range order
+    // wavefront adds them in range order (each page part separately)
+    float* l1 = lds;
+    float* l2 = lds + kWaves * RW * B;
     if (lane == 0)
 #pragma unroll
       for (int i = 0; i < RW; ++i)
 #pragma unroll
-        for (int b = 0; b < B; ++b) lds[(wave * RW + i) * B + b] = v[i][b];
+        for (int b = 0; b < B; ++b) {
+          l1[(wave * RW + i) * B + b] = v[i][b];
+          l2[(wave * RW + i) * B + b] = v2[i][b];
+        }
     __syncthreads();
     if (part == 0 && lane == 0)
 #pragma unroll
       for (int i = 0; i < RW; ++i)
 #pragma unroll
         for (int b = 0; b < B; ++b) {
-          float s = lds[(wave * RW + i) * B + b];
+          float s1 = l1[(wave * RW + i) * B + b], s2 = l2[(wave * RW + i) * B + b];
 #pragma unroll
-          for (int q = 1; q < KS; ++q) s += lds[((wave + q) * RW + i) * B + b];
-          v[i][b] = s;
+          for (int q = 1; q < KS; ++q) {
+            s1 += l1[((wave + q) * RW + i) * B + b];
+            s2 += l2[((wave + q) * RW + i) * B + b];
+          }
+          v[i][b] = s1;
+          v2[i][b] = s2;
         }
     __syncthreads();  // LDS is reused by the next unit of a persistent worker
   }
@@ -220,22 +278,25 @@ __device__ void gemv_unit(const GemvParams& P, int page, int j, float* lds) {
 #pragma unroll
   for (int i = 0; i < RW; ++i) {
     const int64_t r = r0 + i;
-    if (r > r_hi) continue;
-    const int64_t e0 = r * K;
-    if (e0 >= pe0 && e0 + K <= pe1) {
+    if (kind[i] == 0) {
 #pragma unroll
       for (int b = 0; b < B; ++b) store_y(P, b, r, v[i][b]);
-    } else if (e0 < pe0) {
-      store_split<B>(P, page, 1, v[i]);  // tail of a row begun on page-1
-    } else {
-      store_split<B>(P, page + 1, 0, v[i]);  // head of a row ending on page+1
+    } else if (kind[i] == 1) {
+      store_split<B>(P, page, 1, v[i]);  // tail of a row begun on a page of the other tier
+    } else if (kind[i] == 2) {
+      if (ro2[i] != kOOB) {
+#pragma unroll
+        for (int b = 0; b < B; ++b) store_y(P, b, r, v[i][b] + v2[i][b]);
+      } else {
+        store_split<B>(P, page + 1, 0, v[i]);  // head of a row ending on the other tier
+      }
     }
   }
 }
 
 template <int B, int RW, int UN, int KS>
 __global__ __launch_bounds__(kThreads) void gemv_kernel(GemvParams P) {
-  __shared__ float lds[kWaves * RW * B];
+  __shared__ float lds[2 * kWaves * RW * B];
   const int bid = blockIdx.x;
   const int U = P.units_per_page;
   if (P.address_order) {
@@ -258,6 +319,7 @@ __global__ __launch_bounds__(256) void split_fixup(GemvParams P, int n_pages, in
   if (bnd >= n_pages) return;
   const int64_t e = static_cast<int64_t>(bnd) * kPageElems;
   if (e % P.K == 0) return;  // this boundary falls between rows
+  if (P.tiers[bnd - 1] == P.tiers[bnd]) return;  // summed by one workgroup
   const float* s0 = P.partial + static_cast<int64_t>(bnd) * 2 * bst::kMaxGemvBatch;
   store_y(P, b, e / P.K, s0[b] + s0[bst::kMaxGemvBatch + b]);
 }
@@ -284,7 +346,7 @@ inline int k_splits(int K) {
 }
 
 template <int B, int KS>
-int launch(GemvParams& P, int n_pages, const boost_ctx* ctx, hipStream_t s) {
+int launch(GemvParams& P, int n_pages, bool need_fixup, const boost_ctx* ctx, hipStream_t s) {
   constexpr int RW = Shape<B>::RW, UN = Shape<B>::UN;
   const int rows_wg = RW * (kWaves / KS);
   // units per page: enough for the page that meets the most rows
@@ -312,7 +374,7 @@ int launch(GemvParams& P, int n_pages, const boost_ctx* ctx, hipStream_t s) {
   hipLaunchKernelGGL((gemv_kernel<B, RW, UN, KS>), dim3(static_cast<unsigned>(grid)),
                      dim3(kThreads), 0, s, P);
   BOOST_HIP(hipGetLastError());
-  if (n_pages > 1 && kPageElems % P.K != 0) {
+  if (need_fixup) {
     const int lanes = (n_pages - 1) * B;
     hipLaunchKernelGGL(split_fixup, dim3((lanes + 255) / 256), dim3(256), 0, s, P,
                        n_pages, B);
@@ -322,11 +384,12 @@ int launch(GemvParams& P, int n_pages, const boost_ctx* ctx, hipStream_t s) {
 }
 
 template <int B>
-int launch_b(GemvParams& P, int n_pages, const boost_ctx* ctx, hipStream_t s) {
+int launch_b(GemvParams& P, int n_pages, bool need_fixup, const boost_ctx* ctx,
+             hipStream_t s) {
   switch (k_splits(P.K)) {
-    case 1: return launch<B, 1>(P, n_pages, ctx, s);
-    case 2: return launch<B, 2>(P, n_pages, ctx, s);
-    default: return launch<B, 4>(P, n_pages, ctx, s);
+    case 1: return launch<B, 1>(P, n_pages, need_fixup, ctx, s);
+    case 2: return launch<B, 2>(P, n_pages, need_fixup, ctx, s);
+    default: return launch<B, 4>(P, n_pages, need_fixup, ctx, s);
   }
 }
 
@@ -377,15 +440,22 @@ int boost_decode_gemv(boost_ctx* ctx, const boost_tensor* W, int N, int K, const
   P.partial = W->d_partial;
   auto s = static_cast<hipStream_t>(stream);
   const int n = static_cast<int>(W->n_pages);
+  P.n_pages = n;
+  P.tiers = W->d_tiers;
+  // split_fixup is needed only where a cut row crosses a tier boundary
+  bool fix = false;
+  if (kPageElems % K != 0)
+    for (int b = 1; b < n && !fix; ++b)
+      fix = (static_cast<int64_t>(b) * kPageElems) % K != 0 && W->tiers[b - 1] != W->tiers[b];
   switch (B) {
-    case 1: return launch_b<1>(P, n, ctx, s);
-    case 2: return launch_b<2>(P, n, ctx, s);
-    case 3: return launch_b<3>(P, n, ctx, s);
-    case 4: return launch_b<4>(P, n, ctx, s);
-    case 5: return launch_b<5>(P, n, ctx, s);
-    case 6: return launch_b<6>(P, n, ctx, s);
-    case 7: return launch_b<7>(P, n, ctx, s);
-    default: return launch_b<8>(P, n, ctx, s);
+    case 1: return launch_b<1>(P, n, fix, ctx, s);
+    case 2: return launch_b<2>(P, n, fix, ctx, s);
+    case 3: return launch_b<3>(P, n, fix, ctx, s);
+    case 4: return launch_b<4>(P, n, fix, ctx, s);
+    case 5: return launch_b<5>(P, n, fix, ctx, s);
+    case 6: return launch_b<6>(P, n, fix, ctx, s);
+    case 7: return launch_b<7>(P, n, fix, ctx, s);
+    default: return launch_b<8>(P, n, fix, ctx, s);
   }
 }
 

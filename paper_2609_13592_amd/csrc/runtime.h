@@ -47,6 +47,7 @@ struct boost_tensor {
   bst::Slab hbm, host;
   // device-side copies
   char** d_page_table = nullptr;        // [n_pages]
+  uint8_t* d_tiers = nullptr;           // [n_pages] tier codes
   int32_t* d_hbm_pages = nullptr;       // HBM page ids, ascending
   int32_t* d_host_pages = nullptr;      // host page ids, ascending
   float* d_partial = nullptr;           // split-row partial sums

@@ -62,6 +62,7 @@ static int free_tensor(boost_tensor* t) {
   if (!t) return BOOST_OK;
   if (t->ctx && t->ctx->device >= 0) (void)hipSetDevice(t->ctx->device);
   (void)hipFree(t->d_page_table);
+  (void)hipFree(t->d_tiers);
   (void)hipFree(t->d_hbm_pages);
   (void)hipFree(t->d_host_pages);
   (void)hipFree(t->d_partial);
@@ -144,6 +145,7 @@ static int place(boost_ctx* ctx, const void* src, uint64_t bytes,
   }
   int r = upload(reinterpret_cast<void**>(&t->d_page_table), t->page_ptr.data(),
                  n_pages * sizeof(char*));
+  if (!r) r = upload(reinterpret_cast<void**>(&t->d_tiers), t->tiers.data(), n_pages);
   if (!r) r = upload(reinterpret_cast<void**>(&t->d_hbm_pages), t->hbm_pages.data(),
                      t->hbm_pages.size() * sizeof(int32_t));
   if (!r) r = upload(reinterpret_cast<void**>(&t->d_host_pages), t->host_pages.data(),
@@ -288,6 +290,7 @@ int boost_staged_view(boost_ctx* ctx, const boost_tensor* t, void* staging,
   const size_t nb = t->n_pages + 1;
   int r = upload(reinterpret_cast<void**>(&v->d_page_table), v->page_ptr.data(),
                  v->n_pages * sizeof(char*));
+  if (!r) r = upload(reinterpret_cast<void**>(&v->d_tiers), v->tiers.data(), v->n_pages);
   if (!r) r = upload(reinterpret_cast<void**>(&v->d_hbm_pages), v->hbm_pages.data(),
                      v->hbm_pages.size() * sizeof(int32_t));
   if (!r) r = upload(reinterpret_cast<void**>(&v->d_host_pages), nullptr, 0);
