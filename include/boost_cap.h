@@ -316,6 +316,56 @@ int boost_paged_attn_decode(boost_ctx *ctx, const boost_kv_pool *pool, int layer
                             const int32_t *ctx_lens, float scale, void *out,
                             int out_dtype, void *stream);
 
+/* -------------------------------------------- a6: glue of a full decode step */
+
+/* The paper measures whole decode steps of Llama-style models (§5.1) without
+ * restating the model; these operators complete a pre-norm step around the
+ * GEMV and attention calls.  The residual stream is fp32 [B, d]; operands of
+ * products and of attention are bf16.  All calls are asynchronous on
+ * `stream`, allocate nothing and fail with EINVAL on bad sizes or nulls and
+ * ENODEV on a plan-only context. */
+
+/* out[b, :] = embedding row tokens[b] of the placed [V, d] bf16 tensor E
+ * (read through its page table), as fp32.  A token outside [0, V) gives a
+ * zero row. */
+int boost_embed_gather(boost_ctx *ctx, const boost_tensor *E, int V, int d,
+                       const int32_t *tokens, int B, float *out, void *stream);
+
+/* out[b, i] = bf16(x[b, i] / sqrt(mean_i x[b, i]^2 + eps) * w[i]).
+ * x fp32 [B, d], w bf16 [d], out bf16 [B, d]. */
+int boost_rmsnorm(boost_ctx *ctx, const float *x, const void *w, int B, int d,
+                  float eps, void *out, void *stream);
+
+/* Split the fused qkv output fp32 [B, (Hq + 2H) D] (query heads, then key
+ * heads, then value heads) into bf16 q [B, Hq, D], k [B, H, D], v [B, H, D],
+ * rotating query and key heads by RoPE at positions[b]: element i pairs with
+ * i + D/2 and turns by positions[b] * theta^(-2i/D). */
+int boost_rope_qkv(boost_ctx *ctx, const float *qkv, const int32_t *positions,
+                   int B, int Hq, int H, int D, double theta, void *q, void *k,
+                   void *v, void *stream);
+
+/* Append the new token of every request to one layer of the pool: token b
+ * at position positions[b] goes to block block_tables[b][positions[b] / T],
+ * offset positions[b] % T.  k, v bf16 [B, H, D].  Positions or blocks
+ * outside the table / pool are skipped. */
+int boost_kv_append(boost_ctx *ctx, const boost_kv_pool *pool, int layer,
+                    const int32_t *block_tables, int max_blocks,
+                    const int32_t *positions, const void *k, const void *v,
+                    int B, void *stream);
+
+/* out[b, j] = bf16(silu(gu[b, j]) * gu[b, F + j]) for the fused gate_up
+ * output fp32 [B, 2F] (gate rows first). */
+int boost_silu_mul(boost_ctx *ctx, const float *gu, int B, int F, void *out,
+                   void *stream);
+
+/* x[i] += y[i] for n fp32 values. */
+int boost_residual_add(boost_ctx *ctx, float *x, const float *y, int64_t n,
+                       void *stream);
+
+/* ids[b] = argmax_j logits[b, j] (fp32 [B, V]); ties give the lowest index. */
+int boost_argmax(boost_ctx *ctx, const float *logits, int B, int V, int32_t *ids,
+                 void *stream);
+
 #ifdef __cplusplus
 }
 #endif

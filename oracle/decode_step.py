@@ -72,7 +72,7 @@ def argmax_lowest(logits: np.ndarray) -> np.ndarray:
 
 
 def decode_step(weights: dict, tokens: np.ndarray, k_cache, v_cache, lengths,
-                dims: dict):
+                dims: dict, trace: dict | None = None):
     """One decode step.
 
     weights: 'embed' [V, d]; per layer l: 'norm1.l' [d], 'qkv.l' [(Hq+2H)D, d],
@@ -83,6 +83,7 @@ def decode_step(weights: dict, tokens: np.ndarray, k_cache, v_cache, lengths,
       new token (lengths[b] = L_b counts the new token).
     dims: layers, d, hq, hkv, hd, ffn, vocab.
     Returns (logits float64 [B, V], ids [B], per-layer appended (k, v) bf16).
+    trace, when given, receives the last layer's intermediates (diagnostics).
     """
     L, d = dims["layers"], dims["d"]
     Hq, H, D, F = dims["hq"], dims["hkv"], dims["hd"], dims["ffn"]
@@ -108,6 +109,8 @@ def decode_step(weights: dict, tokens: np.ndarray, k_cache, v_cache, lengths,
         gu = f64(h2) @ f64(weights[f"gate_up.{l}"]).T
         act = to_bf16(silu(gu[:, :F]) * gu[:, F:])
         x = x + f64(act) @ f64(weights[f"down.{l}"]).T
+        if trace is not None:
+            trace.update(h=h, q=q16, k=k16, v=v16, o=o, h2=h2, act=act, x=x.copy())
     hf = to_bf16(rmsnorm(x, weights["norm_f"]))
     logits = f64(hf) @ f64(weights["lm_head"]).T
     return logits, argmax_lowest(logits), appended

@@ -78,6 +78,14 @@ _SIGS = {
     "boost_tensor_read": (_i32, [_vp, _u64, _vp, _u64]),
     "boost_tensor_free": (_i32, [_vp]),
     "boost_gemv_set_schedule": (_i32, [_vp, _i32, _i32]),
+    "boost_embed_gather": (_i32, [_vp, _vp, _i32, _i32, _vp, _i32, _vp, _vp]),
+    "boost_rmsnorm": (_i32, [_vp, _vp, _vp, _i32, _i32, C.c_float, _vp, _vp]),
+    "boost_rope_qkv": (_i32, [_vp, _vp, _vp, _i32, _i32, _i32, _i32, _dbl, _vp, _vp,
+                              _vp, _vp]),
+    "boost_kv_append": (_i32, [_vp, _vp, _i32, _vp, _i32, _vp, _vp, _vp, _i32, _vp]),
+    "boost_silu_mul": (_i32, [_vp, _vp, _i32, _i32, _vp, _vp]),
+    "boost_residual_add": (_i32, [_vp, _vp, _vp, C.c_int64, _vp]),
+    "boost_argmax": (_i32, [_vp, _vp, _i32, _i32, _vp, _vp]),
     "boost_staged_view": (_i32, [_vp, _vp, _vp, _u64, C.POINTER(_vp)]),
     "boost_prefetch": (_i32, [_vp, _vp, _vp]),
     "boost_kv_pool_create": (_i32, [_vp, C.POINTER(KVCfg), C.POINTER(_vp)]),
@@ -360,3 +368,38 @@ def boost_paged_attn_decode(ctx: int, pool: int, layer: int, q, B: int, Hq: int,
                                           _ptr(block_tables), max_blocks,
                                           _ptr(ctx_lens), scale, _ptr(out), out_dtype,
                                           _stream(stream)))
+
+
+# ---------------------------------------------------------- decode-step glue
+def boost_embed_gather(ctx: int, E: int, V: int, d: int, tokens, B: int, out, stream=None):
+    _check(load().boost_embed_gather(ctx, E, V, d, _ptr(tokens), B, _ptr(out),
+                                     _stream(stream)))
+
+
+def boost_rmsnorm(ctx: int, x, w, B: int, d: int, eps: float, out, stream=None):
+    _check(load().boost_rmsnorm(ctx, _ptr(x), _ptr(w), B, d, eps, _ptr(out),
+                                _stream(stream)))
+
+
+def boost_rope_qkv(ctx: int, qkv, positions, B: int, Hq: int, H: int, D: int,
+                   theta: float, q, k, v, stream=None):
+    _check(load().boost_rope_qkv(ctx, _ptr(qkv), _ptr(positions), B, Hq, H, D, theta,
+                                 _ptr(q), _ptr(k), _ptr(v), _stream(stream)))
+
+
+def boost_kv_append(ctx: int, pool: int, layer: int, block_tables, max_blocks: int,
+                    positions, k, v, B: int, stream=None):
+    _check(load().boost_kv_append(ctx, pool, layer, _ptr(block_tables), max_blocks,
+                                  _ptr(positions), _ptr(k), _ptr(v), B, _stream(stream)))
+
+
+def boost_silu_mul(ctx: int, gu, B: int, F: int, out, stream=None):
+    _check(load().boost_silu_mul(ctx, _ptr(gu), B, F, _ptr(out), _stream(stream)))
+
+
+def boost_residual_add(ctx: int, x, y, n: int, stream=None):
+    _check(load().boost_residual_add(ctx, _ptr(x), _ptr(y), n, _stream(stream)))
+
+
+def boost_argmax(ctx: int, logits, B: int, V: int, ids, stream=None):
+    _check(load().boost_argmax(ctx, _ptr(logits), B, V, _ptr(ids), _stream(stream)))

@@ -1,0 +1,279 @@
+// a6: the element-wise glue of a full decode step of a pre-norm Llama-style
+// model (the paper runs whole decode steps, §5.1; the operators themselves
+// are not its subject): embedding gather, RMSNorm, RoPE with the q/k/v split
+// of the fused qkv output, KV append, SiLU(gate) * up, residual add and
+// argmax.  The residual stream is fp32; operands of the matrix products and
+// of attention are bf16 (round to nearest even).
+#include <cmath>
+
+#include "runtime.h"
+
+namespace {
+
+__device__ __forceinline__ float lo_bf16(uint32_t v) { return __uint_as_float(v << 16); }
+__device__ __forceinline__ float hi_bf16(uint32_t v) {
+  return __uint_as_float(v & 0xffff0000u);
+}
+__device__ __forceinline__ uint16_t to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) return 0x7fc0;
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return static_cast<uint16_t>(u >> 16);
+}
+
+// One lane per 8 elements of one row; the row of token t is read through the
+// embedding tensor's page table.
+__global__ __launch_bounds__(256) void embed_gather_kernel(const char* const* __restrict__ pt,
+                                                           const int32_t* __restrict__ tok,
+                                                           int B, int V, int d,
+                                                           float* __restrict__ out) {
+  const int chunks = d / 8;
+  const int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (t >= static_cast<int64_t>(B) * chunks) return;
+  const int b = static_cast<int>(t / chunks), c = static_cast<int>(t % chunks);
+  const int32_t id = tok[b];
+  float4* o = reinterpret_cast<float4*>(out + static_cast<int64_t>(b) * d + c * 8);
+  if (id < 0 || id >= V) {
+    o[0] = make_float4(0.f, 0.f, 0.f, 0.f);
+    o[1] = o[0];
+    return;
+  }
+  const uint64_t byte = (static_cast<uint64_t>(id) * d + c * 8) * 2;
+  const uint4 u = *reinterpret_cast<const uint4*>(pt[byte >> 21] + (byte & (bst::kPage - 1)));
+  o[0] = make_float4(lo_bf16(u.x), hi_bf16(u.x), lo_bf16(u.y), hi_bf16(u.y));
+  o[1] = make_float4(lo_bf16(u.z), hi_bf16(u.z), lo_bf16(u.w), hi_bf16(u.w));
+}
+
+// One workgroup per row: sum of squares in a fixed order, then
+// y = bf16(x * (1 / sqrt(mean + eps)) * w).
+__global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ x,
+                                                      const uint16_t* __restrict__ w, int d,
+                                                      float eps, uint16_t* __restrict__ y) {
+  __shared__ float part[4];
+  const float* row = x + static_cast<int64_t>(blockIdx.x) * d;
+  float s = 0.f;
+  for (int i = threadIdx.x; i < d; i += 256) s = fmaf(row[i], row[i], s);
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) s += __shfl_xor(s, m, 64);
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = s;
+  __syncthreads();
+  const float tot = ((part[0] + part[1]) + part[2]) + part[3];
+  const float scale = 1.0f / sqrtf(tot / static_cast<float>(d) + eps);
+  uint16_t* out = y + static_cast<int64_t>(blockIdx.x) * d;
+  for (int i = threadIdx.x; i < d; i += 256)
+    out[i] = to_bf16(row[i] * scale * __uint_as_float(static_cast<uint32_t>(w[i]) << 16));
+}
+
+// One workgroup per (request, head of the fused qkv output), one lane per
+// rotation pair.  Query and key heads are rotated (half-split pairs, angle in
+// double precision); value heads are converted.
+__global__ __launch_bounds__(64) void rope_qkv_kernel(const float* __restrict__ qkv,
+                                                      const int32_t* __restrict__ pos,
+                                                      int Hq, int H, int D, double log2_theta,
+                                                      uint16_t* __restrict__ q,
+                                                      uint16_t* __restrict__ k,
+                                                      uint16_t* __restrict__ v) {
+  const int heads = Hq + 2 * H;
+  const int b = blockIdx.x / heads, h = blockIdx.x % heads;
+  const int half = D / 2;
+  const float* src = qkv + (static_cast<int64_t>(b) * heads + h) * D;
+  uint16_t* dst;
+  if (h < Hq)
+    dst = q + (static_cast<int64_t>(b) * Hq + h) * D;
+  else if (h < Hq + H)
+    dst = k + (static_cast<int64_t>(b) * H + (h - Hq)) * D;
+  else
+    dst = v + (static_cast<int64_t>(b) * H + (h - Hq - H)) * D;
+  for (int i = threadIdx.x; i < half; i += blockDim.x) {
+    const float a = src[i], c = src[i + half];
+    if (h >= Hq + H) {
+      dst[i] = to_bf16(a);
+      dst[i + half] = to_bf16(c);
+      continue;
+    }
+    const double inv = exp2(-(2.0 * i / D) * log2_theta);
+    const double ang = static_cast<double>(pos[b]) * inv;
+    double sn, cs;
+    sincos(ang, &sn, &cs);
+    dst[i] = to_bf16(static_cast<float>(a * cs - c * sn));
+    dst[i + half] = to_bf16(static_cast<float>(a * sn + c * cs));
+  }
+}
+
+// The new token of request b (position pos[b]) goes to slot
+// table[b][pos / T] * T + pos % T of the layer's K and V tensors.
+__global__ __launch_bounds__(256) void kv_append_kernel(
+    const char* const* __restrict__ pt_k, const char* const* __restrict__ pt_v,
+    const int32_t* __restrict__ tables, int max_blocks, const int32_t* __restrict__ pos,
+    const uint4* __restrict__ k, const uint4* __restrict__ v, int B, int H, int D, int T,
+    int nb) {
+  const int chunks = D / 8;
+  const int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (t >= static_cast<int64_t>(B) * H * chunks) return;
+  const int c = static_cast<int>(t % chunks);
+  const int h = static_cast<int>((t / chunks) % H);
+  const int b = static_cast<int>(t / (static_cast<int64_t>(chunks) * H));
+  const int p = pos[b];
+  if (p < 0 || p >= max_blocks * T) return;
+  const int32_t blk = tables[static_cast<int64_t>(b) * max_blocks + p / T];
+  if (blk < 0 || blk >= nb) return;
+  const uint64_t byte = ((static_cast<uint64_t>(h) * nb + blk) * T + p % T) * D * 2 +
+                        static_cast<uint64_t>(c) * 16;
+  const uint64_t page = byte >> 21, in = byte & (bst::kPage - 1);
+  *reinterpret_cast<uint4*>(const_cast<char*>(pt_k[page]) + in) = k[t];
+  *reinterpret_cast<uint4*>(const_cast<char*>(pt_v[page]) + in) = v[t];
+}
+
+__global__ __launch_bounds__(256) void silu_mul_kernel(const float* __restrict__ gu, int B,
+                                                       int F, uint16_t* __restrict__ out) {
+  const int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (t >= static_cast<int64_t>(B) * F) return;
+  const int64_t b = t / F, j = t % F;
+  const float g = gu[b * 2 * F + j], u = gu[b * 2 * F + F + j];
+  out[t] = to_bf16(g / (1.0f + expf(-g)) * u);
+}
+
+__global__ __launch_bounds__(256) void residual_add_kernel(float* __restrict__ x,
+                                                           const float* __restrict__ y,
+                                                           int64_t n) {
+  const int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (t < n) x[t] += y[t];
+}
+
+__device__ __forceinline__ void better(float& bv, int& bi, float v, int i) {
+  // larger value wins; equal values keep the lower index
+  if (v > bv || (v == bv && i < bi)) {
+    bv = v;
+    bi = i;
+  }
+}
+
+// One workgroup per row; ties go to the lowest index.
+__global__ __launch_bounds__(256) void argmax_kernel(const float* __restrict__ logits, int V,
+                                                     int32_t* __restrict__ ids) {
+  __shared__ float sv[4];
+  __shared__ int si[4];
+  const float* row = logits + static_cast<int64_t>(blockIdx.x) * V;
+  float bv = -INFINITY;
+  int bi = 0x7fffffff;
+  for (int i = threadIdx.x; i < V; i += 256) better(bv, bi, row[i], i);
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) {
+    const float ov = __shfl_xor(bv, m, 64);
+    const int oi = __shfl_xor(bi, m, 64);
+    better(bv, bi, ov, oi);
+  }
+  if ((threadIdx.x & 63) == 0) {
+    sv[threadIdx.x >> 6] = bv;
+    si[threadIdx.x >> 6] = bi;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int w = 1; w < 4; ++w) better(bv, bi, sv[w], si[w]);
+    ids[blockIdx.x] = bi == 0x7fffffff ? 0 : bi;
+  }
+}
+
+inline unsigned blocks_for(int64_t n, int per) { return static_cast<unsigned>((n + per - 1) / per); }
+
+}  // namespace
+
+using namespace bst;
+
+extern "C" {
+
+int boost_embed_gather(boost_ctx* ctx, const boost_tensor* E, int V, int d,
+                       const int32_t* tokens, int B, float* out, void* stream) {
+  if (!ctx || !E || !tokens || !out) return fail(BOOST_EINVAL, "null argument");
+  if (ctx->device < 0) return fail(BOOST_ENODEV, "plan-only context");
+  if (V < 1 || d < 8 || d % 8 || B < 1) return fail(BOOST_EINVAL, "V=%d d=%d B=%d", V, d, B);
+  if (static_cast<uint64_t>(V) * d * 2 != E->bytes)
+    return fail(BOOST_EINVAL, "V*d*2 does not match the tensor");
+  const int64_t n = static_cast<int64_t>(B) * (d / 8);
+  hipLaunchKernelGGL(embed_gather_kernel, dim3(blocks_for(n, 256)), dim3(256), 0,
+                     static_cast<hipStream_t>(stream), E->d_page_table, tokens, B, V, d, out);
+  BOOST_HIP(hipGetLastError());
+  return BOOST_OK;
+}
+
+int boost_rmsnorm(boost_ctx* ctx, const float* x, const void* w, int B, int d, float eps,
+                  void* out, void* stream) {
+  if (!ctx || !x || !w || !out) return fail(BOOST_EINVAL, "null argument");
+  if (ctx->device < 0) return fail(BOOST_ENODEV, "plan-only context");
+  if (B < 1 || d < 1 || !(eps >= 0.f)) return fail(BOOST_EINVAL, "B=%d d=%d eps=%g", B, d, eps);
+  hipLaunchKernelGGL(rmsnorm_kernel, dim3(B), dim3(256), 0, static_cast<hipStream_t>(stream),
+                     x, static_cast<const uint16_t*>(w), d, eps, static_cast<uint16_t*>(out));
+  BOOST_HIP(hipGetLastError());
+  return BOOST_OK;
+}
+
+int boost_rope_qkv(boost_ctx* ctx, const float* qkv, const int32_t* positions, int B, int Hq,
+                   int H, int D, double theta, void* q, void* k, void* v, void* stream) {
+  if (!ctx || !qkv || !positions || !q || !k || !v) return fail(BOOST_EINVAL, "null argument");
+  if (ctx->device < 0) return fail(BOOST_ENODEV, "plan-only context");
+  if (B < 1 || Hq < 1 || H < 1 || D < 2 || D % 2 || !(theta > 1.0))
+    return fail(BOOST_EINVAL, "B=%d Hq=%d H=%d D=%d theta=%g", B, Hq, H, D, theta);
+  hipLaunchKernelGGL(rope_qkv_kernel, dim3(B * (Hq + 2 * H)), dim3(64), 0,
+                     static_cast<hipStream_t>(stream), qkv, positions, Hq, H, D, std::log2(theta),
+                     static_cast<uint16_t*>(q), static_cast<uint16_t*>(k),
+                     static_cast<uint16_t*>(v));
+  BOOST_HIP(hipGetLastError());
+  return BOOST_OK;
+}
+
+int boost_kv_append(boost_ctx* ctx, const boost_kv_pool* p, int layer,
+                    const int32_t* block_tables, int max_blocks, const int32_t* positions,
+                    const void* k, const void* v, int B, void* stream) {
+  if (!ctx || !p || !block_tables || !positions || !k || !v)
+    return fail(BOOST_EINVAL, "null argument");
+  if (ctx->device < 0 || !p->d_page_table) return fail(BOOST_ENODEV, "plan-only pool");
+  if (layer < 0 || static_cast<uint32_t>(layer) >= p->cfg.layers)
+    return fail(BOOST_EINVAL, "layer %d", layer);
+  if (B < 1 || max_blocks < 1) return fail(BOOST_EINVAL, "B=%d max_blocks=%d", B, max_blocks);
+  if ((reinterpret_cast<uintptr_t>(k) | reinterpret_cast<uintptr_t>(v)) & 15)
+    return fail(BOOST_EINVAL, "k and v must be 16-byte aligned");
+  const uint64_t P = p->geom.pages;
+  const int H = static_cast<int>(p->cfg.kv_heads), D = static_cast<int>(p->cfg.head_dim);
+  const int64_t n = static_cast<int64_t>(B) * H * (D / 8);
+  hipLaunchKernelGGL(kv_append_kernel, dim3(blocks_for(n, 256)), dim3(256), 0,
+                     static_cast<hipStream_t>(stream), p->d_page_table + 2ull * layer * P,
+                     p->d_page_table + (2ull * layer + 1) * P, block_tables, max_blocks,
+                     positions, static_cast<const uint4*>(k), static_cast<const uint4*>(v), B,
+                     H, D, static_cast<int>(p->cfg.block_tokens), static_cast<int>(p->geom.nb));
+  BOOST_HIP(hipGetLastError());
+  return BOOST_OK;
+}
+
+int boost_silu_mul(boost_ctx* ctx, const float* gu, int B, int F, void* out, void* stream) {
+  if (!ctx || !gu || !out) return fail(BOOST_EINVAL, "null argument");
+  if (ctx->device < 0) return fail(BOOST_ENODEV, "plan-only context");
+  if (B < 1 || F < 1) return fail(BOOST_EINVAL, "B=%d F=%d", B, F);
+  const int64_t n = static_cast<int64_t>(B) * F;
+  hipLaunchKernelGGL(silu_mul_kernel, dim3(blocks_for(n, 256)), dim3(256), 0,
+                     static_cast<hipStream_t>(stream), gu, B, F, static_cast<uint16_t*>(out));
+  BOOST_HIP(hipGetLastError());
+  return BOOST_OK;
+}
+
+int boost_residual_add(boost_ctx* ctx, float* x, const float* y, int64_t n, void* stream) {
+  if (!ctx || !x || !y) return fail(BOOST_EINVAL, "null argument");
+  if (ctx->device < 0) return fail(BOOST_ENODEV, "plan-only context");
+  if (n < 1) return fail(BOOST_EINVAL, "n=%lld", (long long)n);
+  hipLaunchKernelGGL(residual_add_kernel, dim3(blocks_for(n, 256)), dim3(256), 0,
+                     static_cast<hipStream_t>(stream), x, y, n);
+  BOOST_HIP(hipGetLastError());
+  return BOOST_OK;
+}
+
+int boost_argmax(boost_ctx* ctx, const float* logits, int B, int V, int32_t* ids,
+                 void* stream) {
+  if (!ctx || !logits || !ids) return fail(BOOST_EINVAL, "null argument");
+  if (ctx->device < 0) return fail(BOOST_ENODEV, "plan-only context");
+  if (B < 1 || V < 1) return fail(BOOST_EINVAL, "B=%d V=%d", B, V);
+  hipLaunchKernelGGL(argmax_kernel, dim3(B), dim3(256), 0, static_cast<hipStream_t>(stream),
+                     logits, V, ids);
+  BOOST_HIP(hipGetLastError());
+  return BOOST_OK;
+}
+
+}  // extern "C"

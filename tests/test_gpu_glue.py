@@ -1,0 +1,114 @@
+"""Per-operator parity of the decode-step glue at Llama-3-70B dimensions
+(batch 8): each kernel gets the same inputs as the oracle function it
+implements."""
+import numpy as np
+import pytest
+
+import synth
+from oracle import decode_step as ods
+from oracle.gemv import bf16_to_f32, f32_to_bf16
+from paper_2609_13592_amd import binding as bd
+from tests.gpu_util import host_u16, stream, sync, to_dev_u16
+
+pytestmark = pytest.mark.gpu
+B, D_MODEL, HQ, HKV, HD, FFN, VOCAB = 8, 8192, 64, 8, 128, 28672, 128256
+
+
+def dev(a):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def assert_bf16_close(got_u16, want_u16, frac_exact=0.995):
+    """bf16 outputs: every value within one bf16 ulp of the oracle's, and
+    almost all bit-identical (the two sides round fp32 and fp64 values that
+    can straddle a rounding boundary)."""
+    g = bf16_to_f32(got_u16).astype(np.float64)
+    w = bf16_to_f32(want_u16).astype(np.float64)
+    ulp = np.maximum(np.abs(w), 1e-30) * 2.0 ** -7
+    assert np.all(np.abs(g - w) <= ulp)
+    assert np.mean(got_u16 == want_u16) >= frac_exact
+
+
+def test_rmsnorm_70b(gpu_ctx):
+    import torch
+    rng = np.random.default_rng(0)
+    x = (rng.standard_normal((B, D_MODEL)) * 3).astype(np.float32)
+    w = synth.round_bf16((1 + 0.1 * rng.standard_normal(D_MODEL)).astype(np.float32))
+    out = torch.empty((B, D_MODEL), dtype=torch.int16, device="cuda")
+    bd.boost_rmsnorm(gpu_ctx, dev(x), to_dev_u16(w), B, D_MODEL, 1e-5, out, stream())
+    sync()
+    assert_bf16_close(host_u16(out), ods.to_bf16(ods.rmsnorm(x.astype(np.float64), w)))
+
+
+def test_rope_qkv_70b(gpu_ctx):
+    import torch
+    rng = np.random.default_rng(1)
+    heads = HQ + 2 * HKV
+    qkv = rng.standard_normal((B, heads * HD)).astype(np.float32)
+    pos = np.array([0, 1, 15, 16, 1000, 2047, 4095, 8191], dtype=np.int32)
+    q = torch.empty((B, HQ, HD), dtype=torch.int16, device="cuda")
+    k = torch.empty((B, HKV, HD), dtype=torch.int16, device="cuda")
+    v = torch.empty((B, HKV, HD), dtype=torch.int16, device="cuda")
+    bd.boost_rope_qkv(gpu_ctx, dev(qkv), dev(pos), B, HQ, HKV, HD, 500000.0, q, k, v, stream())
+    sync()
+    x = qkv.astype(np.float64)
+    want_q = ods.to_bf16(ods.rope(x[:, :HQ * HD].reshape(B, HQ, HD), pos))
+    want_k = ods.to_bf16(ods.rope(x[:, HQ * HD:(HQ + HKV) * HD].reshape(B, HKV, HD), pos))
+    want_v = ods.to_bf16(x[:, (HQ + HKV) * HD:].reshape(B, HKV, HD))
+    assert_bf16_close(host_u16(q), want_q)
+    assert_bf16_close(host_u16(k), want_k)
+    assert np.array_equal(host_u16(v), want_v)
+
+
+def test_silu_mul_70b(gpu_ctx):
+    import torch
+    rng = np.random.default_rng(2)
+    gu = (rng.standard_normal((B, 2 * FFN)) * 4).astype(np.float32)
+    out = torch.empty((B, FFN), dtype=torch.int16, device="cuda")
+    bd.boost_silu_mul(gpu_ctx, dev(gu), B, FFN, out, stream())
+    sync()
+    g = gu[:, :FFN].astype(np.float64)
+    u = gu[:, FFN:].astype(np.float64)
+    assert_bf16_close(host_u16(out), ods.to_bf16(ods.silu(g) * u))
+
+
+def test_embed_gather_through_tiered_pages(gpu_ctx):
+    import torch
+    g = torch.Generator(device="cuda")
+    g.manual_seed(3)
+    e = torch.randn((VOCAB, D_MODEL), generator=g, device="cuda").to(torch.bfloat16)
+    E = bd.boost_place_weights(gpu_ctx, e.view(torch.int16), VOCAB * D_MODEL * 2, 6)
+    try:
+        assert bd.boost_tensor_tiers(E).sum() > 0
+        tok = np.array([0, 1, 127, 128, 640, 65535, VOCAB - 1, VOCAB], dtype=np.int32)
+        out = torch.empty((B, D_MODEL), dtype=torch.float32, device="cuda")
+        bd.boost_embed_gather(gpu_ctx, E, VOCAB, D_MODEL, dev(tok), B, out, stream())
+        sync()
+        got = out.cpu().numpy()
+        rows = e.view(torch.int16)[torch.from_numpy(tok[:-1].astype(np.int64)).cuda()]
+        want = bf16_to_f32(rows.cpu().numpy().view(np.uint16))
+        assert np.array_equal(got[:-1], want)
+        assert np.all(got[-1] == 0)          # token outside the vocabulary
+    finally:
+        bd.boost_tensor_free(E)
+
+
+def test_residual_and_argmax(gpu_ctx):
+    rng = np.random.default_rng(4)
+    x = rng.standard_normal((B, VOCAB)).astype(np.float32)
+    y = rng.standard_normal((B, VOCAB)).astype(np.float32)
+    xd = dev(x)
+    bd.boost_residual_add(gpu_ctx, xd, dev(y), B * VOCAB, stream())
+    sync()
+    s = xd.cpu().numpy()
+    assert np.array_equal(s, x + y)
+    # ties: plant equal maxima, the lowest index must win
+    s[0, 5] = s[0, 77] = s[0, 100000] = 1e6
+    s[1, :] = 0.0
+    s[2, VOCAB - 1] = 1e7
+    ids = dev(np.zeros(B, np.int32))
+    bd.boost_argmax(gpu_ctx, dev(s), B, VOCAB, ids, stream())
+    sync()
+    assert ids.cpu().numpy().tolist() == ods.argmax_lowest(s.astype(np.float64)).tolist()
+    assert ids.cpu().numpy()[:3].tolist() == [5, 0, VOCAB - 1]
