@@ -48,6 +48,9 @@ def parse():
                    help="replay each step as a captured HIP graph")
     p.add_argument("--pmc-ref", action="store_true",
                    help="also run a plain 1 GiB device copy (counter scale reference)")
+    p.add_argument("--workload", default="chain8b", choices=("chain8b", "llama70b"),
+                   help="chain8b: decode weight chain (default); llama70b: full 70B-"
+                        "shaped decode step under a 120 GB HBM weight budget")
     return p.parse_args()
 
 
@@ -280,6 +283,124 @@ def cpu_baseline(seconds: float):
                       f"{spent:.1f} s of compute"}
 
 
+# ------------------------------------------------------ 70B full decode step
+def llama70b(args, bd, ctx, torch, bw_hbm, bw_host, alpha):
+    """Llama-3-70B-shaped full decode step (80 layers, d 8192, FFN 28672,
+    GQA 64/8, head_dim 128, vocab 128256, bf16 ~N(0, 0.02) random init),
+    batch 8, context 2048, weights placed by modulo placement at the modulus
+    that fits a 120e9-byte HBM weight budget; KV in HBM.  Timed against the
+    same step with every weight in HBM (uncapped)."""
+    import synth
+    from paper_2609_13592_amd.step import DecodeModel, Dims
+    dims = Dims(layers=args.layers, d=8192, hq=64, hkv=8, hd=128, ffn=28672, vocab=128256)
+    B, L = 8, 2048
+    M_alpha = bd.boost_modulus_from_alpha(alpha)
+    sizes = [N * K * 2 for _, N, K in dims.shapes()] * dims.layers + \
+        [dims.vocab * dims.d * 2] * 2
+    M = args.modulus or bd.boost_modulus_from_budget(sizes, 120 * 10 ** 9, M_alpha)
+    log(f"  M_alpha {M_alpha} budget modulus {M}")
+    names = [("embed", dims.vocab, dims.d, 9998), ("lm_head", dims.vocab, dims.d, 9999)] + \
+        [(f"{n}.{l}", N, K, synth.chain_seed(l, i)) for l in range(dims.layers)
+         for i, (n, N, K) in enumerate(dims.shapes())]
+
+    def place(tier_fn):
+        mats, host = {}, 0
+        for name, N, K, seed in names:
+            g = torch.Generator(device="cuda")
+            g.manual_seed(seed)
+            w = torch.randn((N, K), generator=g, device="cuda")
+            w.mul_(1.0 if name == "embed" else 0.02)
+            w = w.to(torch.bfloat16).view(torch.int16)
+            mats[name] = tier_fn(w, N * K * 2)
+            host += int(bd.boost_tensor_tiers(mats[name]).sum())
+            del w
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        return mats, host
+
+    rng = np.random.default_rng(4)
+    norms = {}
+    for k in ["norm_f"] + [f"norm{j}.{l}" for l in range(dims.layers) for j in (1, 2)]:
+        v = synth.round_bf16((1 + 0.1 * rng.standard_normal(dims.d)).astype(np.float32))
+        norms[k] = torch.from_numpy(v.view(np.int16)).cuda()
+    need = L // 16
+    pool = bd.boost_kv_pool_create(ctx, dims.layers, dims.hkv, dims.hd, B * need, 0,
+                                   bd.KV_ALL_HBM, q_heads=dims.hq, max_batch=B,
+                                   max_blocks_per_seq=need)
+    tables = np.zeros((B, need), np.int32)
+    for b in range(B):
+        tables[b] = bd.boost_kv_alloc(pool, b, need)
+    sp = torch.cuda.current_stream().cuda_stream
+    g = torch.Generator(device="cuda")
+    g.manual_seed(12)
+    t = np.arange(L - 1)
+    slots = torch.from_numpy(np.concatenate([tables[b, t // 16] * 16 + t % 16
+                                             for b in range(B)]).astype(np.int32)).cuda()
+    for l in range(dims.layers):
+        k = torch.randn((B * (L - 1), dims.hkv, dims.hd), generator=g, device="cuda").to(torch.bfloat16)
+        v = torch.randn((B * (L - 1), dims.hkv, dims.hd), generator=g, device="cuda").to(torch.bfloat16)
+        bd.boost_kv_write(ctx, pool, l, slots, k, v, B * (L - 1), sp)
+    del k, v
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).cuda()
+    tokens = dev(synth.context_lengths(5, B, 0, dims.vocab - 1))
+    lens = dev(np.full(B, L))
+    pos = dev(np.full(B, L - 1))
+    td = dev(tables)
+
+    def run(mats, steps, warmup):
+        model = DecodeModel(ctx, dims, B, need, pool, mats, norms)
+        for _ in range(warmup):
+            model.step(tokens, pos, lens, td, sp)
+        torch.cuda.synchronize()
+        ms = time_steps(torch, lambda: model.step(tokens, pos, lens, td, sp), steps)
+        return float(np.median(ms)), model.ids.cpu().numpy().tolist()
+
+    log("step: place weights (tiered)")
+    mats, host_pages = place(lambda w, n: bd.boost_place_weights(ctx, w, n, M))
+    log(f"  host pages {host_pages} ({host_pages * 2 / 1024:.2f} GiB)")
+    log("step: timed (tiered)")
+    ms_boost, ids_boost = run(mats, args.steps, args.warmup)
+    for t_ in mats.values():
+        bd.boost_tensor_free(t_)
+    log("step: place weights (all HBM)")
+    mats, _ = place(lambda w, n: bd.boost_place_weights_map(
+        ctx, w, n, np.zeros((n + bd.PAGE_BYTES - 1) // bd.PAGE_BYTES, np.uint8)))
+    log("step: timed (HBM-only)")
+    ms_hbm, ids_hbm = run(mats, max(args.steps, 10), args.warmup)
+    model = DecodeModel(ctx, dims, B, need, pool, mats, norms)
+    alg = model.bytes_per_step(np.full(B, L))
+    for t_ in mats.values():
+        bd.boost_tensor_free(t_)
+    bd.boost_kv_pool_destroy(pool)
+    host_bytes = host_pages * bd.PAGE_BYTES
+    hbm_bytes = alg - host_bytes
+    bound_ms = max(hbm_bytes / (bw_hbm * 1e9), host_bytes / (bw_host * 1e9)) * 1e3
+    return {
+        "metric": METRIC, "value": round(alg / (ms_boost * 1e-3) / 1e9, 2), "unit": "GB/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_boost, 3), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded random-init weights, K/V and tokens)",
+        "config": {"workload": "Llama-3-70B-shaped full decode step, batch 8, context 2048, "
+                               "120 GB HBM weight budget (overflow pages on host by modulo "
+                               "placement), KV in HBM",
+                   "layers": dims.layers, "d": 8192, "ffn": 28672, "q_heads": 64,
+                   "kv_heads": 8, "head_dim": 128, "vocab": 128256, "batch": B,
+                   "context": L, "modulus": M, "modulus_from_alpha": M_alpha,
+                   "host_weight_bytes": host_bytes},
+        "tokens_per_s": round(B * 1000.0 / ms_boost, 3),
+        "calibration": {"hbm_gbps": round(bw_hbm, 1), "host_gbps": round(bw_host, 2),
+                        "alpha": round(alpha, 6)},
+        "placement_bound_ms": round(bound_ms, 3),
+        "pct_of_placement_bound": round(100 * bound_ms / ms_boost, 2),
+        "hbm_only": {"ms_per_step": round(ms_hbm, 3),
+                     "tokens_per_s": round(B * 1000.0 / ms_hbm, 2),
+                     "value": round(alg / (ms_hbm * 1e-3) / 1e9, 2)},
+        "argmax_equal": ids_boost == ids_hbm,
+        "bytes_per_step": int(alg),
+    }
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -295,6 +416,13 @@ def main():
     M = args.modulus or bd.boost_modulus_from_alpha(alpha)
     log(f"  hbm {bw_hbm:.1f} GB/s host {bw_host:.2f} GB/s alpha {alpha:.5f} M {M}")
     bd.boost_gemv_set_schedule(ctx, bd.SCHED_CAP, args.host_workers)
+    if args.workload == "llama70b":
+        if args.layers == 32:
+            args.layers = 80
+        out = llama70b(args, bd, ctx, torch, bw_hbm, bw_host, alpha)
+        bd.boost_shutdown(ctx)
+        print(json.dumps(out), flush=True)
+        return
 
     log("step: place weights")
     chain = Chain(bd, ctx, torch, args.layers, M)

@@ -56,15 +56,21 @@ __device__ __forceinline__ float hi_bf16(uint32_t v) {
   return __uint_as_float(v & 0xffff0000u);
 }
 
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
+// a.lo * b.lo + a.hi * b.hi + c for two packed bf16 pairs (products of bf16
+// values are exact in fp32; the sum is accumulated in fp32)
+__device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a),
+                                         __builtin_bit_cast(bf16x2_t, b), c, false);
+}
+
+// 8-element dot product of two 16-byte bf16 vectors, accumulated into acc in
+// element order
 __device__ __forceinline__ float dot8(const uint4& w, const uint4& x, float acc) {
-  acc = fmaf(lo_bf16(w.x), lo_bf16(x.x), acc);
-  acc = fmaf(hi_bf16(w.x), hi_bf16(x.x), acc);
-  acc = fmaf(lo_bf16(w.y), lo_bf16(x.y), acc);
-  acc = fmaf(hi_bf16(w.y), hi_bf16(x.y), acc);
-  acc = fmaf(lo_bf16(w.z), lo_bf16(x.z), acc);
-  acc = fmaf(hi_bf16(w.z), hi_bf16(x.z), acc);
-  acc = fmaf(lo_bf16(w.w), lo_bf16(x.w), acc);
-  acc = fmaf(hi_bf16(w.w), hi_bf16(x.w), acc);
+  acc = dot2(w.x, x.x, acc);
+  acc = dot2(w.y, x.y, acc);
+  acc = dot2(w.z, x.z, acc);
+  acc = dot2(w.w, x.w, acc);
   return acc;
 }
 
@@ -328,10 +334,19 @@ __global__ __launch_bounds__(256) void split_fixup(GemvParams P, int n_pages, in
 #define BOOST_GEMV_UN1 8
 #endif
 // Rows per wavefront and loads in flight per row, by batch size.
+// Rows per wavefront (an x chunk is reused for every row) and load steps in
+// flight, by batch size: more rows per wavefront as the batch grows keeps the
+// x loads per weight load, and the registers, bounded.
+#ifndef BOOST_GEMV_RW_BIG
+#define BOOST_GEMV_RW_BIG 4
+#endif
+#ifndef BOOST_GEMV_UN_BIG
+#define BOOST_GEMV_UN_BIG 1
+#endif
 template <int B>
 struct Shape {
-  static constexpr int RW = B == 1 ? 1 : (B <= 4 ? 2 : 1);
-  static constexpr int UN = B == 1 ? BOOST_GEMV_UN1 : (B <= 4 ? 4 : 2);
+  static constexpr int RW = B == 1 ? 1 : (B == 2 ? 2 : (B <= 4 ? 4 : BOOST_GEMV_RW_BIG));
+  static constexpr int UN = B == 1 ? BOOST_GEMV_UN1 : (B <= 4 ? 2 : BOOST_GEMV_UN_BIG);
 };
 
 // Wavefronts per row (split-K inside the workgroup) for a row of K columns:
