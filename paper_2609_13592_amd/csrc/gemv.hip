@@ -48,6 +48,8 @@ struct GemvParams {
   const uint16_t* x;
   void* y;
   int y_bf16;
+  int B;     // batch rows of x and y
+  int join;  // 1: a cut row between two pages of one tier is summed by one unit
   float* partial;  // [(n_pages + 1) boundaries][2 sides][kMaxGemvBatch]
 };
 
@@ -325,9 +327,165 @@ __global__ __launch_bounds__(256) void split_fixup(GemvParams P, int n_pages, in
   if (bnd >= n_pages) return;
   const int64_t e = static_cast<int64_t>(bnd) * kPageElems;
   if (e % P.K == 0) return;  // this boundary falls between rows
-  if (P.tiers[bnd - 1] == P.tiers[bnd]) return;  // summed by one workgroup
+  if (P.join && P.tiers[bnd - 1] == P.tiers[bnd]) return;  // summed by one workgroup
   const float* s0 = P.partial + static_cast<int64_t>(bnd) * 2 * bst::kMaxGemvBatch;
   store_y(P, b, e / P.K, s0[b] + s0[bst::kMaxGemvBatch + b]);
+}
+
+// ---------------------------------------------------------------------------
+// Skinny GEMM on the matrix cores for batches above the GEMV's range.
+//
+// Same page-confined units, schedules and split-row handling as the GEMV; the
+// contraction runs on v_mfma_f32_16x16x32_bf16.  A unit is 16*RT rows of one
+// page; the four wavefronts of the workgroup split K into four contiguous
+// ranges.  Per 32-column step a wavefront loads, for each 16-row tile, one
+// A fragment (lane l: row l % 16, columns 8 (l / 16) .. +8 of the step, 16
+// bytes) and, for each 16-wide batch tile, one B fragment of x with the same
+// column mapping (lane l: batch row l % 16), then issues RT * BT MFMAs.  The
+// column order inside a step is the instruction's, identical for both
+// operands, so every product pairs W[n, k] with x[b, k].
+//
+// The four partial tiles meet in LDS in wavefront order (0, 1, 2, 3), so the
+// reduction order is fixed.  Every row cut by a page boundary stores its part
+// in the split buffer (no joining across pages here) and split_fixup adds the
+// two parts.
+// Cache policy of the matrix-core path's weight loads: 0 = default.  A
+// fragment covers 64 bytes of each of 16 rows, so the other half of every
+// 128-byte line is read by the next column step; streaming (non-temporal)
+// loads lose that half before it is used and fetch it from HBM again.
+#ifndef BOOST_MFMA_W_AUX
+#define BOOST_MFMA_W_AUX 0
+#endif
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
+typedef __attribute__((ext_vector_type(4))) float f32x4_t;
+
+__device__ __forceinline__ bf16x8_t as_bf16x8(const uint4& v) {
+  return __builtin_bit_cast(bf16x8_t, v);
+}
+
+template <int BT, int RT>
+constexpr int mfma_lds_floats() { return 16 * BT * (16 * RT + 1); }
+
+template <int BT, int RT, int UN>
+__device__ void mfma_unit(const GemvParams& P, int page, int j, float* lds) {
+  constexpr int R = 16 * RT;  // rows of a unit
+  constexpr int LS = R + 1;   // LDS stride between batch rows (floats)
+  const int64_t K = P.K;
+  const int64_t total = static_cast<int64_t>(P.N) * K;
+  const int64_t pe0 = static_cast<int64_t>(page) * kPageElems;
+  const int64_t pe1 = min(pe0 + kPageElems, total);
+  const int64_t r_lo = pe0 / K;
+  const int64_t r_hi = (pe1 - 1) / K;  // inclusive
+  const int64_t rbase = r_lo + static_cast<int64_t>(j) * R;
+  if (rbase > r_hi) return;  // uniform over the workgroup
+  const int wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int lrow = lane & 15, lgrp = lane >> 4;
+
+  const __amdgpu_buffer_rsrc_t wr =
+      make_rsrc(P.page_table[page], static_cast<uint32_t>((pe1 - pe0) * 2));
+  const __amdgpu_buffer_rsrc_t xr =
+      make_rsrc(P.x, static_cast<uint32_t>(static_cast<int64_t>(P.B) * K * 2));
+  // byte offset of column 0 of this lane's row in every row tile; a row begun
+  // on the previous page gets a wrapped (huge) offset, so its columns before
+  // the page read as zero and those on the page land at the right place
+  uint32_t ro[RT];
+#pragma unroll
+  for (int t = 0; t < RT; ++t) {
+    const int64_t r = rbase + 16 * t + lrow;
+    ro[t] = r > r_hi ? kOOB : static_cast<uint32_t>((r * K - pe0) * 2);
+  }
+  uint32_t xo[BT];
+#pragma unroll
+  for (int t = 0; t < BT; ++t) {
+    const int b = 16 * t + lrow;
+    xo[t] = b < P.B ? static_cast<uint32_t>(b * K * 2) : kOOB;
+  }
+
+  f32x4_t acc[RT][BT];
+#pragma unroll
+  for (int a = 0; a < RT; ++a)
+#pragma unroll
+    for (int t = 0; t < BT; ++t) acc[a][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  constexpr int kStep = 32;
+  const int64_t kper = ((K + kWaves - 1) / kWaves + kStep - 1) / kStep * kStep;
+  const int64_t k_beg = wave * kper;
+  const int64_t k_end = min(K, k_beg + kper);
+  for (int64_t kb = k_beg; kb < k_end; kb += kStep * UN) {
+    uint4 wv[UN][RT];
+#pragma unroll
+    for (int u = 0; u < UN; ++u) {
+      const int64_t kc = kb + u * kStep + 8 * lgrp;
+      const uint32_t oob = kc < k_end ? 0u : kOOB;
+      const uint32_t kc2 = static_cast<uint32_t>(kc * 2);
+#pragma unroll
+      for (int a = 0; a < RT; ++a) wv[u][a] = load16<BOOST_MFMA_W_AUX>(wr, (ro[a] + kc2) | oob);
+    }
+#pragma unroll
+    for (int u = 0; u < UN; ++u) {
+      const int64_t kc = kb + u * kStep + 8 * lgrp;
+      const uint32_t oob = kc < k_end ? 0u : kOOB;
+      const uint32_t kc2 = static_cast<uint32_t>(kc * 2);
+#pragma unroll
+      for (int t = 0; t < BT; ++t) {
+        const uint4 xv = load16(xr, (xo[t] + kc2) | oob);
+#pragma unroll
+        for (int a = 0; a < RT; ++a)
+          acc[a][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+              as_bf16x8(wv[u][a]), as_bf16x8(xv), acc[a][t], 0, 0, 0);
+      }
+    }
+  }
+
+  // output element (row 16a + 4 lgrp + e, batch 16t + lrow) of every tile;
+  // LDS holds the unit's [batch][row] tile, summed over wavefronts in order
+#pragma unroll 1
+  for (int w = 0; w < kWaves; ++w) {
+    if (wave == w) {
+#pragma unroll
+      for (int a = 0; a < RT; ++a)
+#pragma unroll
+        for (int t = 0; t < BT; ++t)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            float* q = lds + (16 * t + lrow) * LS + 16 * a + 4 * lgrp + e;
+            *q = w == 0 ? acc[a][t][e] : *q + acc[a][t][e];
+          }
+    }
+    __syncthreads();
+  }
+  for (int idx = threadIdx.x; idx < R * 16 * BT; idx += kThreads) {
+    const int b = idx / R, i = idx % R;
+    const int64_t r = rbase + i;
+    if (b >= P.B || r > r_hi) continue;
+    const float v = lds[b * LS + i];
+    const int64_t e0 = r * K;
+    if (e0 < pe0)
+      P.partial[(static_cast<int64_t>(page) * 2 + 1) * bst::kMaxGemvBatch + b] = v;
+    else if (e0 + K > pe1)
+      P.partial[(static_cast<int64_t>(page + 1) * 2) * bst::kMaxGemvBatch + b] = v;
+    else
+      store_y(P, b, r, v);
+  }
+  __syncthreads();  // LDS is reused by the next unit of a persistent worker
+}
+
+template <int BT, int RT, int UN>
+__global__ __launch_bounds__(kThreads) void mfma_kernel(GemvParams P) {
+  __shared__ float lds[mfma_lds_floats<BT, RT>()];
+  const int bid = blockIdx.x;
+  const int U = P.units_per_page;
+  if (P.address_order) {
+    mfma_unit<BT, RT, UN>(P, bid / U, bid % U, lds);
+  } else if (bid < P.host_workers) {
+    const int n_host_units = P.n_host_pages * U;
+    for (int v = bid; v < n_host_units; v += P.host_workers)
+      mfma_unit<BT, RT, UN>(P, P.host_pages[v / U], v % U, lds);
+  } else {
+    const int u = bid - P.host_workers;
+    mfma_unit<BT, RT, UN>(P, P.hbm_pages[u / U], u % U, lds);
+  }
 }
 
 #ifndef BOOST_GEMV_UN1
@@ -360,10 +518,10 @@ inline int k_splits(int K) {
   return ks < BOOST_GEMV_KS_MAX ? ks : BOOST_GEMV_KS_MAX;
 }
 
-template <int B, int KS>
-int launch(GemvParams& P, int n_pages, bool need_fixup, const boost_ctx* ctx, hipStream_t s) {
-  constexpr int RW = Shape<B>::RW, UN = Shape<B>::UN;
-  const int rows_wg = RW * (kWaves / KS);
+// Units per page and grid size for units of rows_wg rows; fills in
+// P.units_per_page, P.host_workers and P.address_order.  Returns -1 if the
+// grid is too large.
+int64_t plan_grid(GemvParams& P, int n_pages, int rows_wg, const boost_ctx* ctx) {
   // units per page: enough for the page that meets the most rows
   const int64_t K = P.K, total = static_cast<int64_t>(P.N) * K;
   int64_t most = 0;
@@ -385,18 +543,55 @@ int launch(GemvParams& P, int n_pages, bool need_fixup, const boost_ctx* ctx, hi
     P.host_workers = static_cast<int>(std::min<int64_t>(h, host_units));
     grid = P.host_workers + static_cast<int64_t>(P.n_hbm_pages) * P.units_per_page;
   }
-  if (grid > 0x7fffffff) return bst::fail(BOOST_EINVAL, "grid too large");
-  hipLaunchKernelGGL((gemv_kernel<B, RW, UN, KS>), dim3(static_cast<unsigned>(grid)),
-                     dim3(kThreads), 0, s, P);
-  BOOST_HIP(hipGetLastError());
+  return grid > 0x7fffffff ? -1 : grid;
+}
+
+int launch_fixup(GemvParams& P, int n_pages, bool need_fixup, hipStream_t s) {
   if (need_fixup) {
-    const int lanes = (n_pages - 1) * B;
+    const int lanes = (n_pages - 1) * P.B;
     hipLaunchKernelGGL(split_fixup, dim3((lanes + 255) / 256), dim3(256), 0, s, P,
-                       n_pages, B);
+                       n_pages, P.B);
     BOOST_HIP(hipGetLastError());
   }
   return BOOST_OK;
 }
+
+template <int B, int KS>
+int launch(GemvParams& P, int n_pages, bool need_fixup, const boost_ctx* ctx, hipStream_t s) {
+  constexpr int RW = Shape<B>::RW, UN = Shape<B>::UN;
+  const int64_t grid = plan_grid(P, n_pages, RW * (kWaves / KS), ctx);
+  if (grid < 0) return bst::fail(BOOST_EINVAL, "grid too large");
+  hipLaunchKernelGGL((gemv_kernel<B, RW, UN, KS>), dim3(static_cast<unsigned>(grid)),
+                     dim3(kThreads), 0, s, P);
+  BOOST_HIP(hipGetLastError());
+  return launch_fixup(P, n_pages, need_fixup, s);
+}
+
+// Row tiles per unit and column steps in flight by batch tiles (16 rows of x
+// each): more accumulators as the batch grows, fewer loads in flight.
+template <int BT>
+struct MShape {
+  static constexpr int RT = BT <= 2 ? 1 : 2;
+  static constexpr int UN = BT == 1 ? 8 : (BT == 2 ? 4 : (BT <= 8 ? 2 : 1));
+};
+
+template <int BT>
+int launch_mfma(GemvParams& P, int n_pages, bool need_fixup, const boost_ctx* ctx,
+                hipStream_t s) {
+  constexpr int RT = MShape<BT>::RT, UN = MShape<BT>::UN;
+  const int64_t grid = plan_grid(P, n_pages, 16 * RT, ctx);
+  if (grid < 0) return bst::fail(BOOST_EINVAL, "grid too large");
+  hipLaunchKernelGGL((mfma_kernel<BT, RT, UN>), dim3(static_cast<unsigned>(grid)),
+                     dim3(kThreads), 0, s, P);
+  BOOST_HIP(hipGetLastError());
+  return launch_fixup(P, n_pages, need_fixup, s);
+}
+
+// Smallest batch that runs on the matrix cores (smaller ones use the GEMV).
+#ifndef BOOST_MFMA_MIN_B
+#define BOOST_MFMA_MIN_B 9
+#endif
+constexpr int kMfmaMinBatch = BOOST_MFMA_MIN_B;
 
 template <int B>
 int launch_b(GemvParams& P, int n_pages, bool need_fixup, const boost_ctx* ctx,
@@ -431,7 +626,8 @@ int boost_decode_gemv(boost_ctx* ctx, const boost_tensor* W, int N, int K, const
   if (N < 1 || K < 8 || K % 8) return fail(BOOST_EINVAL, "N=%d K=%d (K %% 8 == 0)", N, K);
   if (static_cast<uint64_t>(K) * 2 > kPage)
     return fail(BOOST_EINVAL, "row of %d elements exceeds a page", K);
-  if (B < 1 || B > kMaxGemvBatch) return fail(BOOST_EINVAL, "B=%d outside [1, 8]", B);
+  if (B < 1 || B > kMaxGemvBatch)
+    return fail(BOOST_EINVAL, "B=%d outside [1, %d]", B, kMaxGemvBatch);
   if (y_dtype != BOOST_DTYPE_F32 && y_dtype != BOOST_DTYPE_BF16)
     return fail(BOOST_EINVAL, "y_dtype %d", y_dtype);
   if (static_cast<uint64_t>(N) * K * 2 != W->bytes)
@@ -453,11 +649,30 @@ int boost_decode_gemv(boost_ctx* ctx, const boost_tensor* W, int N, int K, const
   P.y = y;
   P.y_bf16 = y_dtype == BOOST_DTYPE_BF16;
   P.partial = W->d_partial;
+  P.B = B;
   auto s = static_cast<hipStream_t>(stream);
   const int n = static_cast<int>(W->n_pages);
   P.n_pages = n;
   P.tiers = W->d_tiers;
+  if (B >= kMfmaMinBatch) {
+    // every row cut by a page boundary goes through split_fixup
+    P.join = 0;
+    bool fix = false;
+    for (int b = 1; b < n && !fix; ++b) fix = (static_cast<int64_t>(b) * kPageElems) % K != 0;
+    switch ((B + 15) / 16) {
+      case 1: return launch_mfma<1>(P, n, fix, ctx, s);
+      case 2: return launch_mfma<2>(P, n, fix, ctx, s);
+      case 3:
+      case 4: return launch_mfma<4>(P, n, fix, ctx, s);
+      case 5:
+      case 6:
+      case 7:
+      case 8: return launch_mfma<8>(P, n, fix, ctx, s);
+      default: return launch_mfma<16>(P, n, fix, ctx, s);
+    }
+  }
   // split_fixup is needed only where a cut row crosses a tier boundary
+  P.join = 1;
   bool fix = false;
   if (kPageElems % K != 0)
     for (int b = 1; b < n && !fix; ++b)

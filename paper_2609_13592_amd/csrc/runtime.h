@@ -59,7 +59,7 @@ struct boost_tensor {
 };
 
 namespace bst {
-constexpr int kMaxGemvBatch = 8;
+constexpr int kMaxGemvBatch = 256;   // largest B of boost_decode_gemv
 }
 
 #include "dsr.h"

@@ -105,6 +105,54 @@ def test_placement_invariance_and_parity(gpu_ctx, N, K, B):
         assert np.array_equal(y.view(np.uint32), outs[0].view(np.uint32))
 
 
+@pytest.mark.parametrize("N,K,B", [(300, 14336, 9), (5000, 520, 16), (257, 4104, 33),
+                                   (77, 28672, 64), (1000, 8, 100), (600, 4096, 128),
+                                   (130, 14336, 256), (40, 56, 200)])
+def test_mfma_placement_invariance_and_parity(gpu_ctx, N, K, B):
+    """Batches above 8 run on the matrix cores: bitwise-equal y under every
+    map and schedule, every result within the bar of the oracle (ragged
+    batch tiles, rows cut by page boundaries, pages of both tiers)."""
+    w, x = synth.gemv_inputs(17 + N + K + B, N, K, B)
+    n = opl.n_pages(w.nbytes)
+    maps = {"hbm": np.zeros(n, np.uint8), "host": np.ones(n, np.uint8),
+            "alt": (np.arange(n) % 2).astype(np.uint8),
+            "mpp3": opl.mpp_tier_map(w.nbytes, 3)}
+    xd = to_dev_u16(x)
+    r64 = og.gemv_f64(w, x)
+    outs = []
+    for name, tiers in maps.items():
+        t = place(gpu_ctx, w, tiers=tiers)
+        try:
+            for sched in (bd.SCHED_CAP, bd.SCHED_ADDRESS):
+                bd.boost_gemv_set_schedule(gpu_ctx, sched, 3)
+                y = run_gemv(gpu_ctx, t, N, K, xd, B)
+                assert og.rel_err(y, r64) <= TOL, (name, sched)
+                assert_f32_bound(y, w, x)
+                outs.append(y)
+        finally:
+            bd.boost_gemv_set_schedule(gpu_ctx, bd.SCHED_CAP)
+            bd.boost_tensor_free(t)
+    for y in outs[1:]:
+        assert np.array_equal(y.view(np.uint32), outs[0].view(np.uint32))
+
+
+@pytest.mark.parametrize("B", [9, 16, 256])
+def test_mfma_exact_pins(gpu_ctx, B):
+    """W = I gives x back exactly on the matrix-core path; bf16 output of it
+    is x's bits."""
+    n = 1024
+    eye = synth.round_bf16(np.eye(n, dtype=np.float32))
+    rng = np.random.default_rng(B)
+    x = synth.normal_bf16(rng, (B, n), 1.0)
+    t = place(gpu_ctx, eye, tiers=(np.arange(opl.n_pages(eye.nbytes)) % 2).astype(np.uint8))
+    try:
+        xd = to_dev_u16(x)
+        assert np.array_equal(run_gemv(gpu_ctx, t, n, n, xd, B), og.bf16_to_f32(x))
+        assert np.array_equal(run_gemv(gpu_ctx, t, n, n, xd, B, bd.DTYPE_BF16), x)
+    finally:
+        bd.boost_tensor_free(t)
+
+
 def test_exact_pins(gpu_ctx):
     """W = I gives x back, all-ones gives K: exact in fp32."""
     n = 1024
@@ -146,9 +194,9 @@ def test_bad_arguments(gpu_ctx):
     w, x = synth.gemv_inputs(1, 64, 512, 1)
     t = place(gpu_ctx, w, M=2)
     xd = to_dev_u16(x)
-    y = dev_f32(9, 64)
+    y = dev_f32(257, 64)
     try:
-        for args in ((64, 520, 1), (63, 512, 1), (64, 512, 9), (64, 512, 0)):
+        for args in ((64, 520, 1), (63, 512, 1), (64, 512, 257), (64, 512, 0)):
             N, K, B = args
             with pytest.raises(bd.BoostError) as e:
                 bd.boost_decode_gemv(gpu_ctx, t, N, K, xd, B, y, bd.DTYPE_F32, stream())
@@ -159,10 +207,12 @@ def test_bad_arguments(gpu_ctx):
         bd.boost_tensor_free(t)
 
 
-@pytest.mark.parametrize("kind", [0, 1, 2, 3, 9])
-def test_full_size_chain_tensor_sampled(gpu_ctx, kind):
+@pytest.mark.parametrize("kind,B", [(0, 1), (1, 1), (2, 1), (3, 1), (9, 1),
+                                    (0, 256), (3, 256), (2, 64)])
+def test_full_size_chain_tensor_sampled(gpu_ctx, kind, B):
     """Full-size Llama-3-8B-shaped tensors (fused qkv, o, gate_up, down,
-    lm_head) placed by MPP at M = 11: sampled rows against the oracle."""
+    lm_head) placed by MPP at M = 11, at batch 1 (GEMV) and at the
+    high-throughput batches (matrix cores): sampled rows against the oracle."""
     import torch
     per_layer, head = synth.chain_shapes(synth.LLAMA8B)
     shapes = {k: (n, kk) for _, k, n, kk in per_layer}
@@ -171,12 +221,12 @@ def test_full_size_chain_tensor_sampled(gpu_ctx, kind):
     wt = synth.chain_weight_torch(3, kind, N, K, "cuda")
     w_dev = wt.view(torch.int16)
     rng = np.random.default_rng(kind)
-    x = synth.normal_bf16(rng, (1, K), 1.0)
+    x = synth.normal_bf16(rng, (B, K), 1.0)
     t = bd.boost_place_weights(gpu_ctx, w_dev, N * K * 2, 11)
     try:
         tiers = bd.boost_tensor_tiers(t)
         assert np.array_equal(tiers, opl.mpp_tier_map(N * K * 2, 11))
-        y = run_gemv(gpu_ctx, t, N, K, to_dev_u16(x), 1)
+        y = run_gemv(gpu_ctx, t, N, K, to_dev_u16(x), B)
         rows = np.unique(np.concatenate([rng.integers(0, N, 200), [0, N - 1],
                                          (np.arange(0, N * K, opl.PAGE // 2) // K)]))
         w_rows = w_dev[torch.from_numpy(rows).cuda()].cpu().numpy().view(np.uint16)
