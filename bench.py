@@ -48,9 +48,15 @@ def parse():
                    help="replay each step as a captured HIP graph")
     p.add_argument("--pmc-ref", action="store_true",
                    help="also run a plain 1 GiB device copy (counter scale reference)")
-    p.add_argument("--workload", default="chain8b", choices=("chain8b", "llama70b"),
+    p.add_argument("--workload", default="chain8b",
+                   choices=("chain8b", "llama70b", "throughput8b"),
                    help="chain8b: decode weight chain (default); llama70b: full 70B-"
-                        "shaped decode step under a 120 GB HBM weight budget")
+                        "shaped decode step under a 120 GB HBM weight budget; "
+                        "throughput8b: 8B-shaped decode at up to 256 requests under a "
+                        "40 GB HBM KV budget")
+    p.add_argument("--no-literal", action="store_true",
+                   help="throughput8b: skip the 256-request variant (~115 GB of "
+                        "pinned host KV)")
     return p.parse_args()
 
 
@@ -161,6 +167,47 @@ def time_steps(torch, fn, steps):
         b.record()
     torch.cuda.synchronize()
     return np.array([a.elapsed_time(b) for a, b in ev])
+
+
+# ------------------------------------------------------------ single layer
+def single_layer_bench(bd, ctx, torch, bw_hbm, bw_host, reps=200):
+    """One bf16 layer W[4096 x 4096] (16 pages) with page 15 on host (M = 16),
+    batch 1: tiered vs all-HBM vs prefetch-then-GEMV, each rotating over 16
+    placed copies (512 MiB) so the last-level cache does not serve the HBM
+    pages."""
+    import synth
+    w, x = synth.single_layer_inputs()
+    N = K = 4096
+    nbytes = w.nbytes
+    copies = 16
+    tiered = [bd.boost_place_weights(ctx, w, nbytes, 16) for _ in range(copies)]
+    hbm = [bd.boost_place_weights_map(ctx, w, nbytes, np.zeros(16, np.uint8))
+           for _ in range(copies)]
+    stage = torch.empty(bd.PAGE_BYTES, dtype=torch.uint8, device="cuda")
+    views = [bd.boost_staged_view(ctx, t, stage, stage.numel()) for t in tiered]
+    xd = torch.from_numpy(x.view(np.int16)).cuda()
+    y = torch.empty((1, N), dtype=torch.float32, device="cuda")
+    sp = torch.cuda.current_stream().cuda_stream
+
+    def run(handles, pre=False):
+        for i in range(copies):
+            if pre:
+                bd.boost_prefetch(ctx, views[i], sp)
+            bd.boost_decode_gemv(ctx, handles[i], N, K, xd, 1, y, bd.DTYPE_F32, sp)
+    out = {}
+    for name, fn in (("boost", lambda: run(tiered)), ("hbm", lambda: run(hbm)),
+                     ("prefetch", lambda: run(views, True))):
+        fn()
+        torch.cuda.synchronize()
+        us = float(np.median(time_steps(torch, fn, max(5, reps // copies)))) * 1e3 / copies
+        out[name] = {"us": round(us, 2), "gbps": round(nbytes / (us * 1e-6) / 1e9, 1)}
+    for t in views + tiered + hbm:
+        bd.boost_tensor_free(t)
+    bound_us = max(15 * bd.PAGE_BYTES / (bw_hbm * 1e9), bd.PAGE_BYTES / (bw_host * 1e9)) * 1e6
+    out["placement_bound_us"] = round(bound_us, 2)
+    out["pct_of_placement_bound"] = round(100 * bound_us / out["boost"]["us"], 2)
+    out["host_pages"] = [15]
+    return out
 
 
 # --------------------------------------------------------------- attention
@@ -284,6 +331,151 @@ def cpu_baseline(seconds: float):
 
 
 # ------------------------------------------------------ 70B full decode step
+# ------------------------------------------------- full decode-step workloads
+def model_names(dims, synth):
+    """(name, N, K, seed) of every matrix of a Llama-style model: embedding and
+    lm_head, then the four fused matrices of every layer."""
+    return [("embed", dims.vocab, dims.d, 9998), ("lm_head", dims.vocab, dims.d, 9999)] + \
+        [(f"{n}.{l}", N, K, synth.chain_seed(l, i)) for l in range(dims.layers)
+         for i, (n, N, K) in enumerate(dims.shapes())]
+
+
+def place_model(bd, torch, names, tier_fn):
+    """Generate every matrix on the GPU (seeded, bf16 ~N(0, 0.02), embedding
+    ~N(0, 1)) and place it with tier_fn(w, bytes).  Returns (handles, host
+    pages)."""
+    mats, host = {}, 0
+    for name, N, K, seed in names:
+        g = torch.Generator(device="cuda")
+        g.manual_seed(seed)
+        w = torch.randn((N, K), generator=g, device="cuda")
+        w.mul_(1.0 if name == "embed" else 0.02)
+        w = w.to(torch.bfloat16).view(torch.int16)
+        mats[name] = tier_fn(w, N * K * 2)
+        host += int(bd.boost_tensor_tiers(mats[name]).sum())
+        del w
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return mats, host
+
+
+def all_hbm(bd, ctx):
+    return lambda w, n: bd.boost_place_weights_map(
+        ctx, w, n, np.zeros((n + bd.PAGE_BYTES - 1) // bd.PAGE_BYTES, np.uint8))
+
+
+def model_norms(torch, dims, synth):
+    rng = np.random.default_rng(4)
+    norms = {}
+    for k in ["norm_f"] + [f"norm{j}.{l}" for l in range(dims.layers) for j in (1, 2)]:
+        v = synth.round_bf16((1 + 0.1 * rng.standard_normal(dims.d)).astype(np.float32))
+        norms[k] = torch.from_numpy(v.view(np.int16)).cuda()
+    return norms
+
+
+def fill_kv(bd, ctx, torch, pool, dims, tables, lens):
+    """K/V of the context before each request's new token, ~N(0, 1) bf16,
+    generated on the GPU per (layer, request) so a request's content does not
+    depend on the batch it is in."""
+    sp = torch.cuda.current_stream().cuda_stream
+    for i, L in enumerate(lens):
+        n = int(L) - 1
+        if n <= 0:
+            continue
+        t = np.arange(n)
+        slots = torch.from_numpy((tables[i, t // 16] * 16 + t % 16).astype(np.int32)).cuda()
+        for l in range(dims.layers):
+            g = torch.Generator(device="cuda")
+            g.manual_seed(1_000_003 * l + i)
+            k = torch.randn((n, dims.hkv, dims.hd), generator=g, device="cuda").to(torch.bfloat16)
+            v = torch.randn((n, dims.hkv, dims.hd), generator=g, device="cuda").to(torch.bfloat16)
+            bd.boost_kv_write(ctx, pool, l, slots, k, v, n, sp)
+    torch.cuda.synchronize()
+
+
+class LayerPrefetch:
+    """Prefetch-to-HBM baseline for a full decode step: the host pages of
+    every layer's matrices are copied into one of two HBM staging slots on a
+    copy stream, one layer ahead, and the layer's GEMVs read staged views
+    (all HBM).  lm_head's host pages have a staging area of their own, copied
+    after the last layer's; the embedding stays tiered (a step reads B rows of
+    it)."""
+
+    def __init__(self, bd, ctx, torch, dims, mats):
+        self.bd, self.ctx, self.torch, self.dims = bd, ctx, torch, dims
+        kinds = [k for k, _, _ in dims.shapes()]
+        host = lambda name: int(bd.boost_tensor_tiers(mats[name]).sum())
+        per_layer = max(sum(host(f"{k}.{l}") for k in kinds) for l in range(dims.layers))
+        self.slots = [torch.empty(max(1, per_layer) * bd.PAGE_BYTES, dtype=torch.uint8,
+                                  device="cuda") for _ in range(2)]
+        self.head = torch.empty(max(1, host("lm_head")) * bd.PAGE_BYTES, dtype=torch.uint8,
+                                device="cuda")
+        self.views = {}             # name -> staged view
+        self.layer_views = []       # per layer: views to copy
+        for l in range(dims.layers):
+            off, vs = 0, []
+            buf = self.slots[l % 2]
+            for k in kinds:
+                name = f"{k}.{l}"
+                n = host(name) * bd.PAGE_BYTES
+                if n == 0:
+                    continue
+                v = bd.boost_staged_view(ctx, mats[name], buf[off:off + n], n)
+                self.views[name] = v
+                vs.append(v)
+                off += n
+            self.layer_views.append(vs)
+        self.head_views = []
+        if host("lm_head"):
+            v = bd.boost_staged_view(ctx, mats["lm_head"], self.head, self.head.numel())
+            self.views["lm_head"] = v
+            self.head_views.append(v)
+        self.mats = dict(mats)
+        self.mats.update(self.views)
+        self.staged_bytes = sum(host(n) for n in self.views) * bd.PAGE_BYTES
+        self.copy = torch.cuda.Stream()
+        self.ready = [torch.cuda.Event() for _ in range(dims.layers + 1)]
+        self.free = [torch.cuda.Event(), torch.cuda.Event()]
+
+    def _issue(self, l):
+        cs = self.copy
+        if l < self.dims.layers:
+            cs.wait_event(self.free[l % 2])
+            for v in self.layer_views[l]:
+                self.bd.boost_prefetch(self.ctx, v, cs.cuda_stream)
+        else:
+            for v in self.head_views:
+                self.bd.boost_prefetch(self.ctx, v, cs.cuda_stream)
+        self.ready[l].record(cs)
+
+    def begin(self, stream_obj):
+        self.main = stream_obj
+        for l in range(min(2, self.dims.layers)):
+            self._issue(l)
+        return self
+
+    def before_layer(self, l):
+        self.main.wait_event(self.ready[l])
+
+    def after_layer(self, l):
+        self.free[l % 2].record(self.main)
+        nxt = l + 2
+        if nxt < self.dims.layers:
+            self._issue(nxt)
+        elif nxt == self.dims.layers:
+            self._issue(self.dims.layers)       # lm_head
+
+    def before_head(self):
+        if self.dims.layers < 2:
+            self._issue(self.dims.layers)
+        self.main.wait_event(self.ready[self.dims.layers])
+
+    def close(self):
+        self.main.wait_stream(self.copy)
+        for v in self.views.values():
+            self.bd.boost_tensor_free(v)
+
+
 def llama70b(args, bd, ctx, torch, bw_hbm, bw_host, alpha):
     """Llama-3-70B-shaped full decode step (80 layers, d 8192, FFN 28672,
     GQA 64/8, head_dim 128, vocab 128256, bf16 ~N(0, 0.02) random init),
@@ -299,30 +491,8 @@ def llama70b(args, bd, ctx, torch, bw_hbm, bw_host, alpha):
         [dims.vocab * dims.d * 2] * 2
     M = args.modulus or bd.boost_modulus_from_budget(sizes, 120 * 10 ** 9, M_alpha)
     log(f"  M_alpha {M_alpha} budget modulus {M}")
-    names = [("embed", dims.vocab, dims.d, 9998), ("lm_head", dims.vocab, dims.d, 9999)] + \
-        [(f"{n}.{l}", N, K, synth.chain_seed(l, i)) for l in range(dims.layers)
-         for i, (n, N, K) in enumerate(dims.shapes())]
-
-    def place(tier_fn):
-        mats, host = {}, 0
-        for name, N, K, seed in names:
-            g = torch.Generator(device="cuda")
-            g.manual_seed(seed)
-            w = torch.randn((N, K), generator=g, device="cuda")
-            w.mul_(1.0 if name == "embed" else 0.02)
-            w = w.to(torch.bfloat16).view(torch.int16)
-            mats[name] = tier_fn(w, N * K * 2)
-            host += int(bd.boost_tensor_tiers(mats[name]).sum())
-            del w
-        torch.cuda.synchronize()
-        torch.cuda.empty_cache()
-        return mats, host
-
-    rng = np.random.default_rng(4)
-    norms = {}
-    for k in ["norm_f"] + [f"norm{j}.{l}" for l in range(dims.layers) for j in (1, 2)]:
-        v = synth.round_bf16((1 + 0.1 * rng.standard_normal(dims.d)).astype(np.float32))
-        norms[k] = torch.from_numpy(v.view(np.int16)).cuda()
+    names = model_names(dims, synth)
+    norms = model_norms(torch, dims, synth)
     need = L // 16
     pool = bd.boost_kv_pool_create(ctx, dims.layers, dims.hkv, dims.hd, B * need, 0,
                                    bd.KV_ALL_HBM, q_heads=dims.hq, max_batch=B,
@@ -330,41 +500,46 @@ def llama70b(args, bd, ctx, torch, bw_hbm, bw_host, alpha):
     tables = np.zeros((B, need), np.int32)
     for b in range(B):
         tables[b] = bd.boost_kv_alloc(pool, b, need)
+    fill_kv(bd, ctx, torch, pool, dims, tables, np.full(B, L))
     sp = torch.cuda.current_stream().cuda_stream
-    g = torch.Generator(device="cuda")
-    g.manual_seed(12)
-    t = np.arange(L - 1)
-    slots = torch.from_numpy(np.concatenate([tables[b, t // 16] * 16 + t % 16
-                                             for b in range(B)]).astype(np.int32)).cuda()
-    for l in range(dims.layers):
-        k = torch.randn((B * (L - 1), dims.hkv, dims.hd), generator=g, device="cuda").to(torch.bfloat16)
-        v = torch.randn((B * (L - 1), dims.hkv, dims.hd), generator=g, device="cuda").to(torch.bfloat16)
-        bd.boost_kv_write(ctx, pool, l, slots, k, v, B * (L - 1), sp)
-    del k, v
     dev = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).cuda()
     tokens = dev(synth.context_lengths(5, B, 0, dims.vocab - 1))
     lens = dev(np.full(B, L))
     pos = dev(np.full(B, L - 1))
     td = dev(tables)
 
-    def run(mats, steps, warmup):
-        model = DecodeModel(ctx, dims, B, need, pool, mats, norms)
+    def run(mats, steps, warmup, pre=None):
+        model = DecodeModel(ctx, dims, B, need, pool, mats if pre is None else pre.mats, norms)
+        main = torch.cuda.current_stream()
+
+        def one():
+            if pre is None:
+                model.step(tokens, pos, lens, td, sp)
+            else:
+                model.step(tokens, pos, lens, td, sp, hooks=pre.begin(main))
+                main.wait_stream(pre.copy)
         for _ in range(warmup):
-            model.step(tokens, pos, lens, td, sp)
+            one()
         torch.cuda.synchronize()
-        ms = time_steps(torch, lambda: model.step(tokens, pos, lens, td, sp), steps)
+        ms = time_steps(torch, one, steps)
         return float(np.median(ms)), model.ids.cpu().numpy().tolist()
 
     log("step: place weights (tiered)")
-    mats, host_pages = place(lambda w, n: bd.boost_place_weights(ctx, w, n, M))
+    mats, host_pages = place_model(bd, torch, names,
+                                   lambda w, n: bd.boost_place_weights(ctx, w, n, M))
     log(f"  host pages {host_pages} ({host_pages * 2 / 1024:.2f} GiB)")
     log("step: timed (tiered)")
     ms_boost, ids_boost = run(mats, args.steps, args.warmup)
+    log("step: timed (prefetch to HBM)")
+    pre = LayerPrefetch(bd, ctx, torch, dims, mats)
+    ms_pre, ids_pre = run(mats, args.steps, args.warmup, pre)
+    pre.close()
+    staged_bytes = pre.staged_bytes
+    del pre
     for t_ in mats.values():
         bd.boost_tensor_free(t_)
     log("step: place weights (all HBM)")
-    mats, _ = place(lambda w, n: bd.boost_place_weights_map(
-        ctx, w, n, np.zeros((n + bd.PAGE_BYTES - 1) // bd.PAGE_BYTES, np.uint8)))
+    mats, _ = place_model(bd, torch, names, all_hbm(bd, ctx))
     log("step: timed (HBM-only)")
     ms_hbm, ids_hbm = run(mats, max(args.steps, 10), args.warmup)
     model = DecodeModel(ctx, dims, B, need, pool, mats, norms)
@@ -396,8 +571,135 @@ def llama70b(args, bd, ctx, torch, bw_hbm, bw_host, alpha):
         "hbm_only": {"ms_per_step": round(ms_hbm, 3),
                      "tokens_per_s": round(B * 1000.0 / ms_hbm, 2),
                      "value": round(alg / (ms_hbm * 1e-3) / 1e9, 2)},
+        "prefetch": {"ms_per_step": round(ms_pre, 3),
+                     "tokens_per_s": round(B * 1000.0 / ms_pre, 3),
+                     "staged_bytes_per_step": int(staged_bytes),
+                     "argmax_equal": ids_pre == ids_boost},
         "argmax_equal": ids_boost == ids_hbm,
         "bytes_per_step": int(alg),
+    }
+
+
+def throughput8b(args, bd, ctx, torch, bw_hbm, bw_host, alpha):
+    """High-throughput Llama-3-8B-shaped decode: up to 256 requests with
+    contexts uniform in [1024, 8192] (seed 0), an HBM KV budget of 40e9 bytes.
+
+      literal -- all 256 requests; the pool keeps the budget's share of every
+                 K/V tensor in HBM and the overflow on host (BOOST_KV_BUDGET);
+      paper   -- the largest batch prefix whose pool, split by LPP at the
+                 modulus from the measured ratio, keeps its HBM part within the
+                 budget (host share ~ alpha / (1 + alpha));
+      hbm     -- HBM-only: the largest prefix whose whole pool fits the budget.
+
+    Weights: modulo placement at the measured ratio for literal/paper, all
+    HBM for the baseline.  Each variant times the full decode step."""
+    import synth
+    from paper_2609_13592_amd.step import DecodeModel, Dims
+    dims = Dims(layers=args.layers, d=4096, hq=32, hkv=8, hd=128, ffn=14336, vocab=128256)
+    B_max, budget = 256, 40 * 10 ** 9
+    lens_all = synth.context_lengths(0, B_max, 1024, 8192)
+    M = args.modulus or bd.boost_modulus_from_alpha(alpha)
+    mb = 8192 // 16
+    bpp = bd.PAGE_BYTES // (16 * dims.hd * 2)
+    blocks = np.cumsum([(int(L) + 15) // 16 for L in lens_all])
+
+    def pages(b):          # pages of one K (or V) tensor of a pool for b requests
+        nb = -(-int(blocks[b - 1]) // bpp) * bpp
+        return dims.hkv * nb // bpp
+
+    per = 2 * dims.layers * bd.PAGE_BYTES
+    b_hbm = max(b for b in range(1, B_max + 1) if pages(b) * per <= budget)
+    b_paper = max(b for b in range(1, B_max + 1) if (pages(b) - pages(b) // M) * per <= budget)
+    log(f"  batches: hbm-only {b_hbm}, paper-style {b_paper}, literal {B_max}; M {M}")
+    names = model_names(dims, synth)
+    norms = model_norms(torch, dims, synth)
+    sp = torch.cuda.current_stream().cuda_stream
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).cuda()
+    tokens_all = synth.context_lengths(5, B_max, 0, dims.vocab - 1)
+
+    def variant(tag, b, mode, mats, host_w_pages):
+        lens = lens_all[:b]
+        need = int(blocks[b - 1])
+        log(f"step: {tag}: pool for {b} requests ({need} blocks)")
+        pool = bd.boost_kv_pool_create(ctx, dims.layers, dims.hkv, dims.hd, need,
+                                       M if mode == bd.KV_LPP else 0, mode,
+                                       q_heads=dims.hq, max_batch=b, max_blocks_per_seq=mb,
+                                       hbm_budget_bytes=budget)
+        try:
+            info = bd.boost_kv_pool_info(pool)
+            tables = np.zeros((b, mb), np.int32)
+            for i, L in enumerate(lens):
+                ids = bd.boost_kv_alloc(pool, i, (int(L) + 15) // 16)
+                assert ids != bd.EAGAIN
+                tables[i, :len(ids)] = ids
+            st = bd.boost_kv_stats(pool)
+            log(f"step: {tag}: fill K/V")
+            fill_kv(bd, ctx, torch, pool, dims, tables, lens)
+            model = DecodeModel(ctx, dims, b, mb, pool, mats, norms)
+            args_ = (dev(tokens_all[:b]), dev(lens - 1), dev(lens), dev(tables), sp)
+            log(f"step: {tag}: timed")
+            for _ in range(args.warmup):
+                model.step(*args_)
+            torch.cuda.synchronize()
+            steps = args.steps if mode != bd.KV_BUDGET else max(2, min(args.steps, 3))
+            ms = float(np.median(time_steps(torch, lambda: model.step(*args_), steps)))
+            alg = model.bytes_per_step(lens)
+            kv_bytes = int(sum(int(L) for L in lens)) * dims.hkv * dims.hd * 2 * 2 * dims.layers
+            host_kv = st["used_host_head_blocks"] / max(1, st["used_blocks"] * dims.hkv)
+            host_bytes = host_w_pages * bd.PAGE_BYTES + host_kv * kv_bytes
+            bound = max((alg - host_bytes) / (bw_hbm * 1e9), host_bytes / (bw_host * 1e9)) * 1e3
+            return {"batch": b, "ms_per_step": round(ms, 3),
+                    "tokens_per_s": round(b * 1000.0 / ms, 1),
+                    "gbps": round(alg / (ms * 1e-3) / 1e9, 1),
+                    "bytes_per_step": int(alg), "kv_host_share": round(host_kv, 5),
+                    "kv_host_pages_per_tensor": int(info["host_pages_per_tensor"]),
+                    "host_weight_pages": int(host_w_pages),
+                    "placement_bound_ms": round(bound, 3),
+                    "pct_of_placement_bound": round(100 * bound / ms, 2),
+                    "ids": model.ids.cpu().numpy().tolist()}
+        finally:
+            bd.boost_kv_pool_destroy(pool)
+
+    out = {}
+    log("step: place weights (all HBM)")
+    mats, _ = place_model(bd, torch, names, all_hbm(bd, ctx))
+    out["hbm"] = variant("hbm-only", b_hbm, bd.KV_ALL_HBM, mats, 0)
+    for t_ in mats.values():
+        bd.boost_tensor_free(t_)
+    log("step: place weights (modulo placement)")
+    mats, host_w = place_model(bd, torch, names,
+                               lambda w, n: bd.boost_place_weights(ctx, w, n, M))
+    out["paper"] = variant("paper-style", b_paper, bd.KV_LPP, mats, host_w)
+    if not args.no_literal:
+        try:
+            out["literal"] = variant("literal", B_max, bd.KV_BUDGET, mats, host_w)
+        except bd.BoostError as e:        # e.g. pinned host memory exhausted
+            out["literal"] = {"skipped": str(e)}
+    for t_ in mats.values():
+        bd.boost_tensor_free(t_)
+    common = min(b_hbm, b_paper)
+    same = out["hbm"]["ids"][:common] == out["paper"]["ids"][:common]
+    for v in out.values():
+        v.pop("ids", None)
+    p = out["paper"]
+    return {
+        "metric": METRIC, "value": p["gbps"], "unit": "GB/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": p["ms_per_step"], "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded random-init weights, K/V and tokens)",
+        "config": {"workload": "Llama-3-8B-shaped high-throughput decode, contexts uniform "
+                               "in [1024, 8192], 40e9-byte HBM KV budget, overflow KV on host "
+                               "through the wave-aware pool",
+                   "layers": dims.layers, "d": 4096, "ffn": 14336, "q_heads": 32,
+                   "kv_heads": 8, "head_dim": 128, "vocab": 128256, "max_batch": B_max,
+                   "modulus": M, "kv_budget_bytes": budget},
+        "tokens_per_s": p["tokens_per_s"],
+        "calibration": {"hbm_gbps": round(bw_hbm, 1), "host_gbps": round(bw_host, 2),
+                        "alpha": round(alpha, 6)},
+        "variants": out,
+        "throughput_vs_hbm_only": round(p["tokens_per_s"] / out["hbm"]["tokens_per_s"], 4),
+        "argmax_equal_on_common_prefix": same,
     }
 
 
@@ -416,10 +718,13 @@ def main():
     M = args.modulus or bd.boost_modulus_from_alpha(alpha)
     log(f"  hbm {bw_hbm:.1f} GB/s host {bw_host:.2f} GB/s alpha {alpha:.5f} M {M}")
     bd.boost_gemv_set_schedule(ctx, bd.SCHED_CAP, args.host_workers)
-    if args.workload == "llama70b":
-        if args.layers == 32:
-            args.layers = 80
-        out = llama70b(args, bd, ctx, torch, bw_hbm, bw_host, alpha)
+    if args.workload in ("llama70b", "throughput8b"):
+        if args.workload == "llama70b":
+            if args.layers == 32:
+                args.layers = 80
+            out = llama70b(args, bd, ctx, torch, bw_hbm, bw_host, alpha)
+        else:
+            out = throughput8b(args, bd, ctx, torch, bw_hbm, bw_host, alpha)
         bd.boost_shutdown(ctx)
         print(json.dumps(out), flush=True)
         return
@@ -491,6 +796,8 @@ def main():
 
     log("step: attention")
     attn = attention_bench(bd, ctx, torch, M, max(10, args.steps), 3)
+    log("step: single layer")
+    single = single_layer_bench(bd, ctx, torch, bw_hbm, bw_host)
     eff = chain.alg_bytes / (ms * 1e-3) / 1e9
     eff_hbm = chain.alg_bytes / (ms_hbm * 1e-3) / 1e9
     host_share = chain.host_pages / chain.pages
@@ -536,6 +843,7 @@ def main():
                      "staged_tensors": len(chain.staged),
                      "staged_bytes_per_step": int(chain.staged_bytes)},
         "attention": attn,
+        "single_layer": single,
         "step_ms_iqr": [round(float(np.percentile(boost_ms, 25)), 4),
                         round(float(np.percentile(boost_ms, 75)), 4)],
         "roofline": {"bound": "hbm", "kernel": "gemv_kernel (batch 1) + split_fixup",

@@ -211,6 +211,13 @@ int boost_decode_gemv(boost_ctx *ctx, const boost_tensor *W, int N, int K,
 #define BOOST_KV_LPP 0      /* linear page placement, last 1/M of pages on host */
 #define BOOST_KV_ALL_HBM 1  /* every page in HBM (HBM-only baseline) */
 #define BOOST_KV_ALL_HOST 2 /* every page on host (stress / capacity bound) */
+/* Linear split at a capacity budget: each K (and V) tensor keeps its first
+ * floor(hbm_budget_bytes / (2 * layers * 2 MiB)) pages in HBM and the rest of
+ * its pages on host (the high-throughput setting of §5.2, where the batch
+ * grows past what HBM holds and the overflow KV lives on host).  When the
+ * tail spans several head regions, blocks carry c or c + 1 host heads, the
+ * mixing of §4.5. */
+#define BOOST_KV_BUDGET 3
 
 /* Request / block types of the allocator (§4.3). */
 #define BOOST_KV_LOCAL 0 /* all-local: no head on host (fewer host heads) */
@@ -228,6 +235,7 @@ typedef struct boost_kv_cfg {
   uint32_t q_heads;            /* Hq, a multiple of H (attention scratch) */
   uint32_t max_batch;          /* largest B of a decode call (scratch) */
   uint32_t max_blocks_per_seq; /* widest block-table row (scratch) */
+  uint64_t hbm_budget_bytes;   /* HBM bytes of the whole pool (BOOST_KV_BUDGET) */
 } boost_kv_cfg;
 
 typedef struct boost_kv_info {

@@ -52,9 +52,17 @@ class KVGeometry:
         return self.block_tokens * self.head_dim * self.elem_bytes
 
 
+def budget_hbm_pages(hbm_budget_bytes: int, layers: int, page: int = PAGE) -> int:
+    """HBM pages of each K (or V) tensor when the whole pool (K and V of every
+    layer) may hold hbm_budget_bytes in HBM: the budget split evenly over the
+    2 * layers tensors, in whole pages (reading: the capacity budget of the
+    high-throughput setting, §5.2, applied tensor by tensor)."""
+    return hbm_budget_bytes // (2 * layers * page)
+
+
 def kv_geometry(n_blocks_req: int, heads: int, head_dim: int, M: int,
                 block_tokens: int = 16, elem_bytes: int = 2,
-                page: int = PAGE) -> KVGeometry:
+                page: int = PAGE, hbm_pages: int | None = None) -> KVGeometry:
     """C4.  Pool size, LPP tail and per-block host-head counts.
 
     * head-block = block_tokens * head_dim * elem_bytes bytes; it must divide a
@@ -63,11 +71,12 @@ def kv_geometry(n_blocks_req: int, heads: int, head_dim: int, M: int,
       region starts on a page boundary (§4.5).
     * pages p = H * NB / blocks_per_page; host pages h = floor(p / M) at the
       tail of the range (§4.2 LPP, with the floor that keeps the host share at
-      or below 1/M as in §4.4).
+      or below 1/M as in §4.4).  With hbm_pages given (a capacity budget), M
+      is not used and the tail is every page past the first hbm_pages.
     * head h of block b lies in page (h * NB + b) // blocks_per_page; the block
       has one host head per such page inside the tail.
     """
-    if M < 2 or heads < 1 or head_dim < 1 or n_blocks_req < 1:
+    if (hbm_pages is None and M < 2) or heads < 1 or head_dim < 1 or n_blocks_req < 1:
         raise ValueError("bad geometry")
     hbb = block_tokens * head_dim * elem_bytes
     if page % hbb:
@@ -75,7 +84,7 @@ def kv_geometry(n_blocks_req: int, heads: int, head_dim: int, M: int,
     bpp = page // hbb
     nb = -(-n_blocks_req // bpp) * bpp
     p = heads * nb // bpp
-    h = p // M
+    h = p // M if hbm_pages is None else max(0, p - hbm_pages)
     first_host_page = p - h
     host_heads = np.zeros(nb, dtype=np.int64)
     for head in range(heads):

@@ -17,7 +17,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.environ.get("BOOST_LIB") or os.path.join(HERE, "_lib", "libboostcap.so")
 
 OK, EINVAL, ENOMEM, EAGAIN, ENODEV, EHIP = 0, -22, -12, -11, -19, -5
-KV_LPP, KV_ALL_HBM, KV_ALL_HOST = 0, 1, 2
+KV_LPP, KV_ALL_HBM, KV_ALL_HOST, KV_BUDGET = 0, 1, 2, 3
 KV_LOCAL, KV_SHH = 0, 1
 TIER_HBM, TIER_HOST = 0, 1
 DTYPE_F32, DTYPE_BF16 = 0, 1
@@ -41,7 +41,7 @@ class KVCfg(C.Structure):
     _fields_ = [("layers", _u32), ("kv_heads", _u32), ("head_dim", _u32),
                 ("block_tokens", _u32), ("n_blocks", _u32), ("M", _u32),
                 ("tier_mode", _i32), ("q_heads", _u32), ("max_batch", _u32),
-                ("max_blocks_per_seq", _u32)]
+                ("max_blocks_per_seq", _u32), ("hbm_budget_bytes", _u64)]
 
 
 class KVInfo(C.Structure):
@@ -306,9 +306,10 @@ def boost_decode_gemv(ctx: int, W: int, N: int, K: int, x, B: int, y,
 def boost_kv_pool_create(ctx: int, layers: int, kv_heads: int, head_dim: int,
                          n_blocks: int, M: int, tier_mode: int = KV_LPP,
                          q_heads: int = 0, max_batch: int = 0,
-                         max_blocks_per_seq: int = 0, block_tokens: int = 16) -> int:
+                         max_blocks_per_seq: int = 0, block_tokens: int = 16,
+                         hbm_budget_bytes: int = 0) -> int:
     cfg = KVCfg(layers, kv_heads, head_dim, block_tokens, n_blocks, M, tier_mode,
-                q_heads or kv_heads, max_batch, max_blocks_per_seq)
+                q_heads or kv_heads, max_batch, max_blocks_per_seq, hbm_budget_bytes)
     h = _vp()
     _check(load().boost_kv_pool_create(ctx, C.byref(cfg), C.byref(h)))
     return h.value

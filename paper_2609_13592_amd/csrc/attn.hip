@@ -383,8 +383,8 @@ int boost_paged_attn_decode(boost_ctx* ctx, const boost_kv_pool* pool, int layer
   const uint64_t tk = 2ull * layer, tv = 2ull * layer + 1;  // tensor indices
   P.k_hbm = pool->hbm.base + tk * (pages - hp) * kPage;
   P.v_hbm = pool->hbm.base + tv * (pages - hp) * kPage;
-  P.k_host = hp ? pool->host.base + tk * hp * kPage : P.k_hbm;
-  P.v_host = hp ? pool->host.base + tv * hp * kPage : P.v_hbm;
+  P.k_host = hp ? pool->host[layer].base : P.k_hbm;
+  P.v_host = hp ? pool->host[layer].base + hp * kPage : P.v_hbm;
   P.host_from = (pages - hp) * kPage;
   P.q = static_cast<const uint16_t*>(q);
   P.tables = block_tables;

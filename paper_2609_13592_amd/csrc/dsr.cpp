@@ -8,11 +8,13 @@
 namespace bst {
 
 int kv_geometry(uint32_t n_blocks, uint32_t H, uint32_t D, uint32_t T, uint32_t M,
-                int mode, KvGeom& g) {
+                int mode, uint32_t layers, uint64_t hbm_budget_bytes, KvGeom& g) {
   if (n_blocks == 0 || H == 0 || D == 0 || T == 0)
     return fail(BOOST_EINVAL, "empty KV geometry");
-  if (mode != BOOST_KV_LPP && mode != BOOST_KV_ALL_HBM && mode != BOOST_KV_ALL_HOST)
+  if (mode != BOOST_KV_LPP && mode != BOOST_KV_ALL_HBM && mode != BOOST_KV_ALL_HOST &&
+      mode != BOOST_KV_BUDGET)
     return fail(BOOST_EINVAL, "tier_mode %d", mode);
+  if (mode == BOOST_KV_BUDGET && layers == 0) return fail(BOOST_EINVAL, "0 layers");
   if (mode == BOOST_KV_LPP && M < 2) return fail(BOOST_EINVAL, "M=%u < 2", M);
   const uint64_t hbb = static_cast<uint64_t>(T) * D * 2;  // one head of one block
   if (kPage % hbb) return fail(BOOST_EINVAL, "head-block of %llu B does not divide a page",
@@ -28,8 +30,14 @@ int kv_geometry(uint32_t n_blocks, uint32_t H, uint32_t D, uint32_t T, uint32_t 
   g.nb = static_cast<uint32_t>(nb);
   const uint64_t pages_per_head = nb / g.blocks_per_page;
   g.pages = H * pages_per_head;
-  g.host_pages = mode == BOOST_KV_LPP ? g.pages / M
-                                      : (mode == BOOST_KV_ALL_HOST ? g.pages : 0);
+  if (mode == BOOST_KV_LPP) {
+    g.host_pages = g.pages / M;
+  } else if (mode == BOOST_KV_BUDGET) {
+    const uint64_t hbm = hbm_budget_bytes / (2ull * layers * kPage);  // per K or V tensor
+    g.host_pages = g.pages > hbm ? g.pages - hbm : 0;
+  } else {
+    g.host_pages = mode == BOOST_KV_ALL_HOST ? g.pages : 0;
+  }
   const uint64_t first_host = g.pages - g.host_pages;
   // head h of block b sits in page h * pages_per_head + b / blocks_per_page
   g.host_heads.assign(g.nb, 0);

@@ -22,9 +22,11 @@ struct KvGeom {
 };
 
 // Geometry of §4.2 / §4.5: every head's region is whole pages; the last
-// `host_pages` pages of a tensor are on host.
+// `host_pages` pages of a tensor are on host (1/M of them for LPP; all pages
+// past a per-tensor share of hbm_budget_bytes over `layers` layers of K and V
+// for BOOST_KV_BUDGET).
 int kv_geometry(uint32_t n_blocks, uint32_t H, uint32_t D, uint32_t T, uint32_t M,
-                int mode, KvGeom& g);
+                int mode, uint32_t layers, uint64_t hbm_budget_bytes, KvGeom& g);
 
 // §4.3 wave-aware block fulfillment over two free lists.
 class Dsr {

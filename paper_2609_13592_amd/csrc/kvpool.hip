@@ -41,7 +41,7 @@ int destroy(boost_kv_pool* p) {
   (void)hipFree(p->d_part_acc);
   (void)hipFree(p->d_part_ml);
   bst::slab_free(p->hbm);
-  bst::slab_free(p->host);
+  for (auto& h : p->host) bst::slab_free(h);
   delete p;
   return BOOST_OK;
 }
@@ -73,7 +73,7 @@ int boost_kv_pool_create(boost_ctx* ctx, const boost_kv_cfg* cfg, boost_kv_pool*
   p->ctx = ctx;
   p->cfg = *cfg;
   int rc = kv_geometry(cfg->n_blocks, cfg->kv_heads, cfg->head_dim, cfg->block_tokens,
-                       cfg->M, cfg->tier_mode, p->geom);
+                       cfg->M, cfg->tier_mode, cfg->layers, cfg->hbm_budget_bytes, p->geom);
   if (rc) {
     delete p;
     return rc;
@@ -93,8 +93,15 @@ int boost_kv_pool_create(boost_ctx* ctx, const boost_kv_cfg* cfg, boost_kv_pool*
   }
   const uint64_t tensors = 2ull * cfg->layers;
   const uint64_t P = p->geom.pages, Hp = p->geom.host_pages;
+  // one HBM slab for every tensor's HBM pages; the host tails in one pinned
+  // slab per layer (K's tail then V's), which keeps each pinned allocation a
+  // few GB even when most of a large pool lives on host
   rc = slab_alloc(ctx, tensors * (P - Hp), false, p->hbm);
-  if (!rc) rc = slab_alloc(ctx, tensors * Hp, true, p->host);
+  if (!rc && Hp) {
+    p->host.resize(cfg->layers);
+    for (uint32_t l = 0; l < cfg->layers && !rc; ++l)
+      rc = slab_alloc(ctx, 2 * Hp, true, p->host[l]);
+  }
   if (rc) {
     destroy(p);
     return rc;
@@ -102,8 +109,9 @@ int boost_kv_pool_create(boost_ctx* ctx, const boost_kv_cfg* cfg, boost_kv_pool*
   std::vector<char*> table(tensors * P);
   for (uint64_t t = 0; t < tensors; ++t)
     for (uint64_t pg = 0; pg < P; ++pg)
-      table[t * P + pg] = pg < P - Hp ? p->hbm.base + (t * (P - Hp) + pg) * kPage
-                                      : p->host.base + (t * Hp + (pg - (P - Hp))) * kPage;
+      table[t * P + pg] = pg < P - Hp
+                              ? p->hbm.base + (t * (P - Hp) + pg) * kPage
+                              : p->host[t / 2].base + ((t % 2) * Hp + (pg - (P - Hp))) * kPage;
   p->max_parts = kv_parts_for(p, static_cast<int>(cfg->max_blocks_per_seq));
   const uint64_t rows = static_cast<uint64_t>(cfg->max_batch) * cfg->q_heads * p->max_parts;
   hipError_t e = hipMalloc(&p->d_page_table, table.size() * sizeof(char*));
@@ -114,7 +122,8 @@ int boost_kv_pool_create(boost_ctx* ctx, const boost_kv_cfg* cfg, boost_kv_pool*
   if (e == hipSuccess) e = hipMalloc(&p->d_part_ml, rows * 2 * sizeof(float));
   // zero the pool so unwritten slots hold defined values
   if (e == hipSuccess && p->hbm.pages) e = hipMemset(p->hbm.base, 0, p->hbm.pages * kPage);
-  if (e == hipSuccess && p->host.pages) std::memset(p->host.host_base, 0, p->host.pages * kPage);
+  for (auto& h : p->host)
+    if (e == hipSuccess) std::memset(h.host_base, 0, h.pages * kPage);
   if (e == hipSuccess) e = hipDeviceSynchronize();
   if (e != hipSuccess) {
     destroy(p);

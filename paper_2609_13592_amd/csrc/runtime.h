@@ -70,7 +70,8 @@ struct boost_kv_pool {
   bst::KvGeom geom;
   bst::Dsr dsr;
   // device backing (absent on a plan-only context)
-  bst::Slab hbm, host;
+  bst::Slab hbm;
+  std::vector<bst::Slab> host;    // per layer: K's host tail, then V's
   char** d_page_table = nullptr;  // [layers][2 (K, V)][pages]
   float* d_part_acc = nullptr;    // [max_batch][q_heads][max_parts][D]
   float* d_part_ml = nullptr;     // [max_batch][q_heads][max_parts][2] (max, sum)

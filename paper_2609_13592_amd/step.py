@@ -66,16 +66,21 @@ class DecodeModel:
         self.logits = torch.zeros((B, D.vocab), dtype=f32, device=dev)
         self.ids = torch.zeros((B,), dtype=torch.int32, device=dev)
 
-    def step(self, tokens, positions, lens, tables, stream=None):
+    def step(self, tokens, positions, lens, tables, stream=None, hooks=None):
         """One decode step for the batch.  tokens, positions (= lens - 1),
         lens: device int32 [B]; tables: device int32 [B, max_blocks] holding
         the blocks of every request including the new token's.  Returns the
-        device ids and logits buffers (valid once the stream reaches them)."""
+        device ids and logits buffers (valid once the stream reaches them).
+
+        hooks (optional) gets before_layer(l), after_layer(l) and before_head()
+        calls as the launches are issued (e.g. to order staging copies)."""
         c, D, B, s = self.ctx, self.dims, self.B, stream
         F32, BF16 = bd.DTYPE_F32, bd.DTYPE_BF16
         bd.boost_embed_gather(c, self.mat["embed"], D.vocab, D.d, tokens, B, self.x, s)
         qkv_n = (D.hq + 2 * D.hkv) * D.hd
         for l in range(D.layers):
+            if hooks is not None:
+                hooks.before_layer(l)
             bd.boost_rmsnorm(c, self.x, self.norms[f"norm1.{l}"], B, D.d, EPS, self.h, s)
             bd.boost_decode_gemv(c, self.mat[f"qkv.{l}"], qkv_n, D.d, self.h, B, self.qkv, F32, s)
             bd.boost_rope_qkv(c, self.qkv, positions, B, D.hq, D.hkv, D.hd, THETA,
@@ -92,7 +97,11 @@ class DecodeModel:
             bd.boost_silu_mul(c, self.gu, B, D.ffn, self.act, s)
             bd.boost_decode_gemv(c, self.mat[f"down.{l}"], D.d, D.ffn, self.act, B,
                                  self.tmp, F32, s)
+            if hooks is not None:
+                hooks.after_layer(l)
             bd.boost_residual_add(c, self.x, self.tmp, B * D.d, s)
+        if hooks is not None:
+            hooks.before_head()
         bd.boost_rmsnorm(c, self.x, self.norms["norm_f"], B, D.d, EPS, self.h, s)
         bd.boost_decode_gemv(c, self.mat["lm_head"], D.vocab, D.d, self.h, B, self.logits,
                              F32, s)

@@ -26,9 +26,11 @@ def run_attn(ctx, pool, layer, q, tables, lens, out_dtype=bd.DTYPE_F32, scale=0.
     return out.cpu().numpy() if out_dtype == bd.DTYPE_F32 else host_u16(out)
 
 
-def new_pool(ctx, H, Hq, nb, M, mode, layers=1, max_batch=64, max_blocks=256):
+def new_pool(ctx, H, Hq, nb, M, mode, layers=1, max_batch=64, max_blocks=256,
+             budget=0):
     return bd.boost_kv_pool_create(ctx, layers, H, 128, nb, M, mode, q_heads=Hq,
-                                   max_batch=max_batch, max_blocks_per_seq=max_blocks)
+                                   max_batch=max_batch, max_blocks_per_seq=max_blocks,
+                                   hbm_budget_bytes=budget)
 
 
 @pytest.mark.parametrize("Hq,H", [(32, 8), (64, 8), (8, 8), (16, 8)])
@@ -38,9 +40,17 @@ def test_small_parity_and_placement_invariance(gpu_ctx, Hq, H):
                                           kv_seed=5, lengths=lengths)
     ref = oa.decode_attention(q, ks, vs)
     outs = []
-    for mode, M in ((bd.KV_ALL_HBM, 0), (bd.KV_LPP, 3), (bd.KV_ALL_HOST, 0)):
-        pool = new_pool(gpu_ctx, H, Hq, 2000, M, mode, max_blocks=160)
+    # the budget leaves 9 of each tensor's 32 pages in HBM: blocks carry 5 or
+    # 6 host heads of 8
+    budget = 2 * 9 * bd.PAGE_BYTES
+    for mode, M in ((bd.KV_ALL_HBM, 0), (bd.KV_LPP, 3), (bd.KV_ALL_HOST, 0),
+                    (bd.KV_BUDGET, 0)):
+        pool = new_pool(gpu_ctx, H, Hq, 2000, M, mode, max_blocks=160, budget=budget)
         try:
+            if mode == bd.KV_BUDGET:
+                info = bd.boost_kv_pool_info(pool)
+                assert info["host_pages_per_tensor"] == 23
+                assert (info["local_host_heads"], info["shh_host_heads"]) == (5, 6)
             tables = fill_pool(bd, gpu_ctx, pool, 0, lengths, ks, vs)
             o = run_attn(gpu_ctx, pool, 0, q, tables, lengths)
             assert og.rel_err(o, ref) <= TOL

@@ -50,6 +50,28 @@ def test_geometry_matches_oracle(plan_ctx, nb_req, H, D, M):
         bd.boost_kv_pool_destroy(pool)
 
 
+@given(st.integers(1, 5000), st.sampled_from([1, 2, 8]), st.sampled_from([64, 128]),
+       st.integers(1, 8), st.integers(0, 400))
+@settings(max_examples=80, deadline=None)
+def test_budget_geometry_matches_oracle(plan_ctx, nb_req, H, D, layers, budget_pages):
+    """BOOST_KV_BUDGET: per-block host heads bit-exact against the oracle for
+    budgets from zero to more than the pool."""
+    budget = budget_pages * bd.PAGE_BYTES + 12345
+    pool = bd.boost_kv_pool_create(plan_ctx, layers, H, D, nb_req, 0, bd.KV_BUDGET,
+                                   q_heads=H, hbm_budget_bytes=budget)
+    try:
+        info = bd.boost_kv_pool_info(pool)
+        g = okv.kv_geometry(nb_req, H, D, 0,
+                            hbm_pages=okv.budget_hbm_pages(budget, layers))
+        assert info["nb_pool"] == g.nb_pool
+        assert info["host_pages_per_tensor"] == g.host_pages
+        assert np.array_equal(host_heads(pool, g.nb_pool), g.host_heads)
+        shh, _ = okv.block_lists(g)
+        assert info["n_shh"] == len(shh)
+    finally:
+        bd.boost_kv_pool_destroy(pool)
+
+
 def test_all_hbm_and_all_host_modes(plan_ctx):
     for mode, expect in ((bd.KV_ALL_HBM, 0), (bd.KV_ALL_HOST, 8)):
         pool = make(plan_ctx, 1000, 8, 128, 0, mode)

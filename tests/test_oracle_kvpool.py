@@ -63,6 +63,43 @@ def test_more_heads_than_modulus_mixes_floor_and_ceil():
     assert abs(geom.host_heads.mean() - H / M) < 1e-12
 
 
+def test_budget_split_extremes():
+    """Capacity-budget split: a budget that holds the pool puts nothing on
+    host (the all-HBM map); a zero budget puts every head of every block on
+    host."""
+    H, D, layers = 8, 128, 4
+    full = kv.kv_geometry(3000, H, D, 2, hbm_pages=10 ** 9)
+    assert full.host_pages == 0 and not full.host_heads.any()
+    pages = full.pages
+    assert kv.budget_hbm_pages(2 * layers * pages * kv.PAGE, layers) == pages
+    assert kv.budget_hbm_pages(2 * layers * pages * kv.PAGE - 1, layers) == pages - 1
+    none = kv.kv_geometry(3000, H, D, 2, hbm_pages=kv.budget_hbm_pages(0, layers))
+    assert none.host_pages == pages and set(none.host_heads.tolist()) == {H}
+
+
+def test_budget_split_high_throughput_shape():
+    """The batch-256, 40e9-byte KV budget shape (8 KV heads, head_dim 128, 32
+    layers, contexts uniform in [1024, 8192]): about three quarters of the KV
+    bytes overflow to host, the tail covers whole heads H-1, H-2, ... and part
+    of one more, so blocks carry c or c + 1 host heads (§4.5), with
+    c = floor(h / pages_per_head) and the last (h mod pages_per_head) pages'
+    blocks of the partly covered head one more."""
+    rng = np.random.default_rng(0)
+    lens = rng.integers(1024, 8192, 256, endpoint=True)
+    nb_req = int(sum(-(-int(L) // 16) for L in lens))
+    hbm = kv.budget_hbm_pages(40 * 10 ** 9, 32)
+    g = kv.kv_geometry(nb_req, 8, 128, 2, hbm_pages=hbm)
+    pph = g.nb_pool // g.blocks_per_page           # pages per head region
+    assert g.host_pages == g.pages - hbm
+    c, rem = divmod(g.host_pages, pph)
+    expect = np.full(g.nb_pool, c)
+    expect[g.nb_pool - rem * g.blocks_per_page:] += 1
+    assert np.array_equal(g.host_heads, expect)
+    assert g.host_heads.sum() * g.head_block_bytes == g.host_pages * kv.PAGE
+    share = g.host_pages / g.pages
+    assert 0.70 < share < 0.78
+
+
 def _run(alloc, steps):
     out = []
     for st in steps:
