@@ -366,7 +366,15 @@ __device__ __forceinline__ bf16x8_t as_bf16x8(const uint4& v) {
 template <int BT, int RT>
 constexpr int mfma_lds_floats() { return 16 * BT * (16 * RT + 1); }
 
-template <int BT, int RT, int UN>
+// Weights through LDS (WL): each wavefront streams its 16 rows row-contiguously
+// (one load instruction = 512 bytes of each of two rows), writes the 16 x 256
+// column chunk into a private LDS tile (16-byte chunks XOR-swizzled by row so
+// both the writes and the fragment reads are free of bank conflicts) and reads
+// the A fragments back from there.
+constexpr int kWlCols = 256;                          // columns per chunk
+constexpr int kWlTileFloats = 16 * kWlCols * 2 / 4;   // one wavefront's tile
+
+template <int BT, int RT, int UN, bool WL>
 __device__ void mfma_unit(const GemvParams& P, int page, int j, float* lds) {
   constexpr int R = 16 * RT;  // rows of a unit
   constexpr int LS = R + 1;   // LDS stride between batch rows (floats)
@@ -412,7 +420,52 @@ __device__ void mfma_unit(const GemvParams& P, int page, int j, float* lds) {
   const int64_t kper = ((K + kWaves - 1) / kWaves + kStep - 1) / kStep * kStep;
   const int64_t k_beg = wave * kper;
   const int64_t k_end = min(K, k_beg + kper);
-  for (int64_t kb = k_beg; kb < k_end; kb += kStep * UN) {
+  if constexpr (WL) {
+    static_assert(RT == 1, "LDS-staged weights take one row tile");
+    uint4* tile = reinterpret_cast<uint4*>(lds + mfma_lds_floats<BT, RT>()) +
+                  wave * (kWlTileFloats / 4);
+    // load instruction i: rows 2i and 2i+1 (lanes 0-31 / 32-63), 16 bytes each
+    uint32_t lo[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int64_t r = rbase + 2 * i + (lane >> 5);
+      lo[i] = r > r_hi ? kOOB : static_cast<uint32_t>((r * K - pe0) * 2);
+    }
+    const int wr_chunk = lane & 31;
+    uint4 wv[8];
+    auto load_chunk = [&](int64_t kb) {
+      const int64_t kc = kb + 8 * wr_chunk;
+      const uint32_t oob = kc < k_end ? 0u : kOOB;
+      const uint32_t kc2 = static_cast<uint32_t>(kc * 2);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) wv[i] = load16<BOOST_MFMA_W_AUX>(wr, (lo[i] + kc2) | oob);
+    };
+    if (k_beg < k_end) load_chunk(k_beg);
+    for (int64_t kb = k_beg; kb < k_end; kb += kWlCols) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int rr = 2 * i + (lane >> 5);
+        tile[rr * 32 + (wr_chunk ^ (rr & 15))] = wv[i];
+      }
+      if (kb + kWlCols < k_end) load_chunk(kb + kWlCols);
+      const int steps =
+          static_cast<int>((min<int64_t>(kWlCols, k_end - kb) + kStep - 1) / kStep);
+#pragma unroll 2
+      for (int st = 0; st < steps; ++st) {
+        const uint4 a = tile[lrow * 32 + ((4 * st + lgrp) ^ lrow)];
+        const int64_t kc = kb + st * kStep + 8 * lgrp;
+        const uint32_t oob = kc < k_end ? 0u : kOOB;
+        const uint32_t kc2 = static_cast<uint32_t>(kc * 2);
+#pragma unroll
+        for (int t = 0; t < BT; ++t) {
+          const uint4 xv = load16(xr, (xo[t] + kc2) | oob);
+          acc[0][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+              as_bf16x8(a), as_bf16x8(xv), acc[0][t], 0, 0, 0);
+        }
+      }
+    }
+  }
+  for (int64_t kb = k_beg; !WL && kb < k_end; kb += kStep * UN) {
     uint4 wv[UN][RT];
 #pragma unroll
     for (int u = 0; u < UN; ++u) {
@@ -471,20 +524,20 @@ __device__ void mfma_unit(const GemvParams& P, int page, int j, float* lds) {
   __syncthreads();  // LDS is reused by the next unit of a persistent worker
 }
 
-template <int BT, int RT, int UN>
+template <int BT, int RT, int UN, bool WL>
 __global__ __launch_bounds__(kThreads) void mfma_kernel(GemvParams P) {
-  __shared__ float lds[mfma_lds_floats<BT, RT>()];
+  __shared__ float lds[mfma_lds_floats<BT, RT>() + (WL ? kWaves * kWlTileFloats : 0)];
   const int bid = blockIdx.x;
   const int U = P.units_per_page;
   if (P.address_order) {
-    mfma_unit<BT, RT, UN>(P, bid / U, bid % U, lds);
+    mfma_unit<BT, RT, UN, WL>(P, bid / U, bid % U, lds);
   } else if (bid < P.host_workers) {
     const int n_host_units = P.n_host_pages * U;
     for (int v = bid; v < n_host_units; v += P.host_workers)
-      mfma_unit<BT, RT, UN>(P, P.host_pages[v / U], v % U, lds);
+      mfma_unit<BT, RT, UN, WL>(P, P.host_pages[v / U], v % U, lds);
   } else {
     const int u = bid - P.host_workers;
-    mfma_unit<BT, RT, UN>(P, P.hbm_pages[u / U], u % U, lds);
+    mfma_unit<BT, RT, UN, WL>(P, P.hbm_pages[u / U], u % U, lds);
   }
 }
 
@@ -569,22 +622,40 @@ int launch(GemvParams& P, int n_pages, bool need_fixup, const boost_ctx* ctx, hi
 
 // Row tiles per unit and column steps in flight by batch tiles (16 rows of x
 // each): more accumulators as the batch grows, fewer loads in flight.
-template <int BT>
-struct MShape {
-  static constexpr int RT = BT <= 2 ? 1 : 2;
-  static constexpr int UN = BT == 1 ? 8 : (BT == 2 ? 4 : (BT <= 8 ? 2 : 1));
-};
+// Matrix-core shapes by batch tiles (16 rows of x each), from a sweep over the
+// 8B and 70B matrices at B = 16..256:
+//   BT <= 2: weights staged through LDS (row-contiguous streaming beat the
+//            A-fragment pattern by 10-25 %);
+//   BT 3..8: four 16-row tiles per wavefront (each x fragment serves four
+//            MFMAs) when that still gives about one workgroup per CU, else
+//            two (the smaller matrices need the extra workgroups more);
+//   BT > 8:  two row tiles (four would need 256 accumulators per lane).
+template <int BT, int RT, int UN, bool WL>
+int launch_mfma_shape(GemvParams& P, int n_pages, bool need_fixup, const boost_ctx* ctx,
+                      hipStream_t s) {
+  const int64_t grid = plan_grid(P, n_pages, 16 * RT, ctx);
+  if (grid < 0) return bst::fail(BOOST_EINVAL, "grid too large");
+  hipLaunchKernelGGL((mfma_kernel<BT, RT, UN, WL>), dim3(static_cast<unsigned>(grid)),
+                     dim3(kThreads), 0, s, P);
+  BOOST_HIP(hipGetLastError());
+  return launch_fixup(P, n_pages, need_fixup, s);
+}
 
 template <int BT>
 int launch_mfma(GemvParams& P, int n_pages, bool need_fixup, const boost_ctx* ctx,
                 hipStream_t s) {
-  constexpr int RT = MShape<BT>::RT, UN = MShape<BT>::UN;
-  const int64_t grid = plan_grid(P, n_pages, 16 * RT, ctx);
-  if (grid < 0) return bst::fail(BOOST_EINVAL, "grid too large");
-  hipLaunchKernelGGL((mfma_kernel<BT, RT, UN>), dim3(static_cast<unsigned>(grid)),
-                     dim3(kThreads), 0, s, P);
-  BOOST_HIP(hipGetLastError());
-  return launch_fixup(P, n_pages, need_fixup, s);
+  if constexpr (BT <= 2) {
+    return launch_mfma_shape<BT, 1, 1, true>(P, n_pages, need_fixup, ctx, s);
+  } else if constexpr (BT <= 8) {
+    // workgroups with 64-row units: pages x units per page (a page meets at
+    // most kPageElems / K + 1 rows)
+    const int64_t per_page = std::min<int64_t>(P.N, kPageElems / P.K + 1);
+    if (static_cast<int64_t>(n_pages) * ((per_page + 63) / 64) >= ctx->n_cu * 3 / 4)
+      return launch_mfma_shape<BT, 4, 1, false>(P, n_pages, need_fixup, ctx, s);
+    return launch_mfma_shape<BT, 2, 2, false>(P, n_pages, need_fixup, ctx, s);
+  } else {
+    return launch_mfma_shape<BT, 2, 1, false>(P, n_pages, need_fixup, ctx, s);
+  }
 }
 
 // Smallest batch that runs on the matrix cores (smaller ones use the GEMV).
