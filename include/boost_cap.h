@@ -198,7 +198,7 @@ int boost_gemv_set_schedule(boost_ctx *ctx, int schedule, int host_workers);
  * bf16 rounded to nearest even (BOOST_DTYPE_BF16).  Accumulation is fp32 and
  * the reduction order is fixed, so results are bitwise reproducible and do
  * not depend on the placement or the schedule.  1 <= B <= 256, K % 8 == 0,
- * N >= 1.  Batches up to 8 run as a GEMV on the vector units; larger ones as a
+ * N >= 1.  Batches up to 6 run as a GEMV on the vector units; larger ones as a
  * skinny GEMM on the matrix cores (the batch sizes of §5.10), with
  * the same page-confined work units.  x must be 16-byte aligned, y 4-byte.
  * Errors: EINVAL, ENODEV, EHIP (launch failure). */

@@ -38,8 +38,20 @@ constexpr int kLanesTok = kD / 8;  // lanes per token row (16)
 #ifndef BOOST_ATTN_ITEMS
 #define BOOST_ATTN_ITEMS 2048
 #endif
-constexpr int kUnroll = BOOST_ATTN_UNROLL;  // blocks in flight per workgroup
+#ifndef BOOST_ATTN_UNROLL8
+#define BOOST_ATTN_UNROLL8 BOOST_ATTN_UNROLL
+#endif
 constexpr int kMaxPartBlocks = 256;         // blocks per partition, at most
+// A work item of fewer than 16 blocks spends as long on its start (q loads)
+// and end (slot merge, partial stores) as on its K/V (batch 8 at 2048 tokens:
+// 1.2 TB/s with 4-block items, 2.2 TB/s with 16).
+#ifndef BOOST_ATTN_PART_MIN
+#define BOOST_ATTN_PART_MIN 16
+#endif
+#ifndef BOOST_ATTN_PART_MAX
+#define BOOST_ATTN_PART_MAX 256
+#endif
+constexpr int kPartMin = BOOST_ATTN_PART_MIN, kPartMax = BOOST_ATTN_PART_MAX;
 
 struct AttnParams {
   // Linear placement makes the tier of a pool page a fixed function of its
@@ -184,6 +196,7 @@ __device__ __forceinline__ void consume(const uint32_t (*qp)[4], const uint4* kb
 
 template <int G>
 __global__ __launch_bounds__(kThreads) void attn_partition(AttnParams P) {
+  constexpr int kUnroll = G == 8 ? BOOST_ATTN_UNROLL8 : BOOST_ATTN_UNROLL;  // blocks in flight
   __shared__ float s_ml[4][G][2];
   __shared__ float s_acc[4][G][kD];
   const int tid = threadIdx.x;
@@ -395,10 +408,13 @@ int boost_paged_attn_decode(boost_ctx* ctx, const boost_kv_pool* pool, int layer
   P.nb = static_cast<int>(pool->geom.nb);
   P.max_blocks = max_blocks;
   // enough work items to fill the GPU several times over (so the last grid
-  // wave is short), at least 4 blocks each
+  // wave is short), each long enough to amortise its start and its merge
+  // (PART_MIN blocks) and short enough to balance (PART_MAX blocks)
   const int want_parts = std::max(1, (BOOST_ATTN_ITEMS + B * H - 1) / (B * H));
-  P.part_blocks = std::min(kMaxPartBlocks,
-                           std::max(4, (max_blocks + want_parts - 1) / want_parts));
+  P.part_blocks = std::min(
+      {kMaxPartBlocks, max_blocks,
+       std::max(kPartMin, std::min(kPartMax, (max_blocks + want_parts - 1) / want_parts))});
+  P.part_blocks = std::max(P.part_blocks, 4);
   P.n_parts = (max_blocks + P.part_blocks - 1) / P.part_blocks;
   P.max_parts = pool->max_parts;
   if (P.n_parts > P.max_parts) return fail(BOOST_EINVAL, "partition scratch too small");

@@ -658,9 +658,11 @@ int launch_mfma(GemvParams& P, int n_pages, bool need_fixup, const boost_ctx* ct
   }
 }
 
-// Smallest batch that runs on the matrix cores (smaller ones use the GEMV).
+// Smallest batch that runs on the matrix cores (smaller ones use the GEMV):
+// from batch 7 the one-tile matrix-core unit beats the dot2 GEMV on every
+// 8B and 70B matrix; at 5 and 6 it depends on the shape.
 #ifndef BOOST_MFMA_MIN_B
-#define BOOST_MFMA_MIN_B 9
+#define BOOST_MFMA_MIN_B 7
 #endif
 constexpr int kMfmaMinBatch = BOOST_MFMA_MIN_B;
 

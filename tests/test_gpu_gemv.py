@@ -105,11 +105,11 @@ def test_placement_invariance_and_parity(gpu_ctx, N, K, B):
         assert np.array_equal(y.view(np.uint32), outs[0].view(np.uint32))
 
 
-@pytest.mark.parametrize("N,K,B", [(300, 14336, 9), (5000, 520, 16), (257, 4104, 33),
+@pytest.mark.parametrize("N,K,B", [(300, 14336, 7), (5000, 520, 16), (257, 4104, 33),
                                    (77, 28672, 64), (1000, 8, 100), (600, 4096, 128),
                                    (130, 14336, 256), (40, 56, 200)])
 def test_mfma_placement_invariance_and_parity(gpu_ctx, N, K, B):
-    """Batches above 8 run on the matrix cores: bitwise-equal y under every
+    """Batches from 7 up run on the matrix cores: bitwise-equal y under every
     map and schedule, every result within the bar of the oracle (ragged
     batch tiles, rows cut by page boundaries, pages of both tiers)."""
     w, x = synth.gemv_inputs(17 + N + K + B, N, K, B)
