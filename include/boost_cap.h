@@ -200,7 +200,13 @@ int boost_gemv_set_schedule(boost_ctx *ctx, int schedule, int host_workers);
  * not depend on the placement or the schedule.  1 <= B <= 256, K % 8 == 0,
  * N >= 1.  Batches up to 6 run as a GEMV on the vector units; larger ones as a
  * skinny GEMM on the matrix cores (the batch sizes of §5.10), with
- * the same page-confined work units.  x must be 16-byte aligned, y 4-byte.
+ * the same page-confined work units; a matrix too small to fill the GPU at a
+ * large batch has K split over several workgroups whose partials go to a
+ * workspace owned by the context (64 MiB, allocated by boost_init) and are
+ * summed in slice order by a second kernel.  Calls on one context must
+ * therefore be ordered (one stream, or streams joined by events): two
+ * overlapping split calls would share the workspace.  x must be 16-byte
+ * aligned, y 4-byte.
  * Errors: EINVAL, ENODEV, EHIP (launch failure). */
 int boost_decode_gemv(boost_ctx *ctx, const boost_tensor *W, int N, int K,
                       const void *x, int B, void *y, int y_dtype, void *stream);

@@ -18,8 +18,12 @@ ROOT = os.path.dirname(HERE)
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 EXTRA = os.environ.get("BOOST_EXTRA_FLAGS", "").split()
+# -amdgpu-mfma-vgpr-form: MFMA accumulators stay in VGPRs (left to itself the
+# register allocator moved the GEMM accumulators between AGPRs and VGPRs on
+# every step, stalling each MFMA on those moves)
 HIP_FLAGS = EXTRA + ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
              "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+             "-mllvm", "-amdgpu-mfma-vgpr-form=1",
              "-Wall", "-Wno-unused-function", "-Wno-unused-command-line-argument",
              f"-I{ROOT}/include"]
 CXX_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-Wall", f"-I{ROOT}/include"]

@@ -50,6 +50,8 @@ struct GemvParams {
   int y_bf16;
   int B;     // batch rows of x and y
   int join;  // 1: a cut row between two pages of one tier is summed by one unit
+  int S;     // K slices per row group (matrix-core path; 1 = no split)
+  float* ws;  // S > 1: [S][B][N] partials, then [(n_pages + 1) * 2][S][B] of cut rows
   float* partial;  // [(n_pages + 1) boundaries][2 sides][kMaxGemvBatch]
 };
 
@@ -131,6 +133,12 @@ __device__ __forceinline__ uint4 load16(__amdgpu_buffer_rsrc_t r, uint32_t off) 
 // Offsets at or above this are outside every resource used here (a page is
 // 2 MiB, x is at most 8 * 512 K elements), so the load returns zero.
 constexpr uint32_t kOOB = 0x80000000u;
+
+// Most K slices a matrix-core call splits a row group into.
+#ifndef BOOST_MFMA_MAX_SLICES
+#define BOOST_MFMA_MAX_SLICES 8
+#endif
+constexpr int kMaxSlices = BOOST_MFMA_MAX_SLICES;
 
 // Accumulate this wavefront's columns [k_beg, k_end) of its RW rows from
 // the page behind resource wr; row i's column 0 sits at byte offset ro[i]
@@ -336,19 +344,24 @@ __global__ __launch_bounds__(256) void split_fixup(GemvParams P, int n_pages, in
 // Skinny GEMM on the matrix cores for batches above the GEMV's range.
 //
 // Same page-confined units, schedules and split-row handling as the GEMV; the
-// contraction runs on v_mfma_f32_16x16x32_bf16.  A unit is 16*RT rows of one
-// page; the four wavefronts of the workgroup split K into four contiguous
-// ranges.  Per 32-column step a wavefront loads, for each 16-row tile, one
-// A fragment (lane l: row l % 16, columns 8 (l / 16) .. +8 of the step, 16
-// bytes) and, for each 16-wide batch tile, one B fragment of x with the same
-// column mapping (lane l: batch row l % 16), then issues RT * BT MFMAs.  The
-// column order inside a step is the instruction's, identical for both
-// operands, so every product pairs W[n, k] with x[b, k].
+// contraction runs on v_mfma_f32_16x16x32_bf16.  A unit is 16 * RT rows of
+// one page and one slice of K; the four wavefronts of the workgroup split the
+// slice into four contiguous column ranges.  Per 32-column step a wavefront
+// holds, for each 16-row tile, one A fragment (lane l: row l % 16, columns
+// 8 (l / 16) .. +8 of the step, 16 bytes) and, for each 16-wide batch tile,
+// one B fragment of x with the same column mapping (lane l: batch row
+// l % 16), and issues RT * BT MFMAs.  The column order inside a step is the
+// instruction's, identical for both operands, so every product pairs
+// W[n, k] with x[b, k].
 //
 // The four partial tiles meet in LDS in wavefront order (0, 1, 2, 3), so the
-// reduction order is fixed.  Every row cut by a page boundary stores its part
-// in the split buffer (no joining across pages here) and split_fixup adds the
-// two parts.
+// reduction order is fixed.  Rows cut by a page boundary store their part in
+// the split buffer and split_fixup adds the two parts; with K split over S
+// workgroups every part goes to the context workspace and split_reduce adds
+// the slices in order.  (Wavefronts that each own rows over the whole slice,
+// sharing x through L1, measured 25-30 % slower: four times longer
+// wavefronts and a quarter of the units.)
+//
 // Cache policy of the matrix-core path's weight loads: 0 = default.  A
 // fragment covers 64 bytes of each of 16 rows, so the other half of every
 // 128-byte line is read by the next column step; streaming (non-temporal)
@@ -363,19 +376,20 @@ __device__ __forceinline__ bf16x8_t as_bf16x8(const uint4& v) {
   return __builtin_bit_cast(bf16x8_t, v);
 }
 
-template <int BT, int RT>
-constexpr int mfma_lds_floats() { return 16 * BT * (16 * RT + 1); }
-
-// Weights through LDS (WL): each wavefront streams its 16 rows row-contiguously
-// (one load instruction = 512 bytes of each of two rows), writes the 16 x 256
-// column chunk into a private LDS tile (16-byte chunks XOR-swizzled by row so
-// both the writes and the fragment reads are free of bank conflicts) and reads
-// the A fragments back from there.
+// Weights through LDS (WL, one row tile per wavefront): each wavefront
+// streams its 16 rows row-contiguously (one load instruction = 512 bytes of
+// each of two rows), writes the 16 x 256 column chunk into a private LDS tile
+// (16-byte chunks XOR-swizzled by row so both the writes and the fragment
+// reads are free of bank conflicts) and reads the A fragments back from there.
 constexpr int kWlCols = 256;                          // columns per chunk
 constexpr int kWlTileFloats = 16 * kWlCols * 2 / 4;   // one wavefront's tile
 
+template <int BT, int RT>
+constexpr int mfma_lds_floats() { return 16 * BT * (16 * RT + 1); }
+
 template <int BT, int RT, int UN, bool WL>
-__device__ void mfma_unit(const GemvParams& P, int page, int j, float* lds) {
+__device__ void mfma_unit(const GemvParams& P, int page, int unit, float* lds) {
+  const int j = unit / P.S, slice = unit % P.S;
   constexpr int R = 16 * RT;  // rows of a unit
   constexpr int LS = R + 1;   // LDS stride between batch rows (floats)
   const int64_t K = P.K;
@@ -394,15 +408,6 @@ __device__ void mfma_unit(const GemvParams& P, int page, int j, float* lds) {
       make_rsrc(P.page_table[page], static_cast<uint32_t>((pe1 - pe0) * 2));
   const __amdgpu_buffer_rsrc_t xr =
       make_rsrc(P.x, static_cast<uint32_t>(static_cast<int64_t>(P.B) * K * 2));
-  // byte offset of column 0 of this lane's row in every row tile; a row begun
-  // on the previous page gets a wrapped (huge) offset, so its columns before
-  // the page read as zero and those on the page land at the right place
-  uint32_t ro[RT];
-#pragma unroll
-  for (int t = 0; t < RT; ++t) {
-    const int64_t r = rbase + 16 * t + lrow;
-    ro[t] = r > r_hi ? kOOB : static_cast<uint32_t>((r * K - pe0) * 2);
-  }
   uint32_t xo[BT];
 #pragma unroll
   for (int t = 0; t < BT; ++t) {
@@ -417,14 +422,22 @@ __device__ void mfma_unit(const GemvParams& P, int page, int j, float* lds) {
     for (int t = 0; t < BT; ++t) acc[a][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
   constexpr int kStep = 32;
-  const int64_t kper = ((K + kWaves - 1) / kWaves + kStep - 1) / kStep * kStep;
-  const int64_t k_beg = wave * kper;
-  const int64_t k_end = min(K, k_beg + kper);
+  // this unit's K slice, then this wavefront's quarter of it
+  const int64_t ksl = (K + P.S - 1) / P.S;
+  const int64_t kslice = (ksl + kWaves * kStep - 1) / (kWaves * kStep) * (kWaves * kStep);
+  const int64_t s_beg = slice * kslice;
+  const int64_t s_end = min(K, s_beg + kslice);
+  const int64_t kper = kslice / kWaves;
+  const int64_t k_beg = min(s_end, s_beg + wave * kper);
+  const int64_t k_end = min(s_end, k_beg + kper);
+
   if constexpr (WL) {
     static_assert(RT == 1, "LDS-staged weights take one row tile");
     uint4* tile = reinterpret_cast<uint4*>(lds + mfma_lds_floats<BT, RT>()) +
                   wave * (kWlTileFloats / 4);
-    // load instruction i: rows 2i and 2i+1 (lanes 0-31 / 32-63), 16 bytes each
+    // load instruction i: rows 2i and 2i+1 (lanes 0-31 / 32-63), 16 bytes
+    // each; a row begun on the previous page gets a wrapped (huge) offset,
+    // so its columns before the page read as zero
     uint32_t lo[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
@@ -441,53 +454,90 @@ __device__ void mfma_unit(const GemvParams& P, int page, int j, float* lds) {
       for (int i = 0; i < 8; ++i) wv[i] = load16<BOOST_MFMA_W_AUX>(wr, (lo[i] + kc2) | oob);
     };
     if (k_beg < k_end) load_chunk(k_beg);
+    constexpr int kChunkSteps = kWlCols / kStep;
+#pragma unroll 1
     for (int64_t kb = k_beg; kb < k_end; kb += kWlCols) {
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
         const int rr = 2 * i + (lane >> 5);
         tile[rr * 32 + (wr_chunk ^ (rr & 15))] = wv[i];
       }
-      if (kb + kWlCols < k_end) load_chunk(kb + kWlCols);
-      const int steps =
-          static_cast<int>((min<int64_t>(kWlCols, k_end - kb) + kStep - 1) / kStep);
-#pragma unroll 2
-      for (int st = 0; st < steps; ++st) {
-        const uint4 a = tile[lrow * 32 + ((4 * st + lgrp) ^ lrow)];
+      // this chunk's x fragments, then the next chunk's weights: the MFMAs
+      // below wait only for the former (the wait counter is in order)
+      uint4 xv[kChunkSteps][BT];
+#pragma unroll
+      for (int st = 0; st < kChunkSteps; ++st) {
         const int64_t kc = kb + st * kStep + 8 * lgrp;
         const uint32_t oob = kc < k_end ? 0u : kOOB;
         const uint32_t kc2 = static_cast<uint32_t>(kc * 2);
 #pragma unroll
-        for (int t = 0; t < BT; ++t) {
-          const uint4 xv = load16(xr, (xo[t] + kc2) | oob);
+        for (int t = 0; t < BT; ++t) xv[st][t] = load16(xr, (xo[t] + kc2) | oob);
+      }
+      load_chunk(kb + kWlCols);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int st = 0; st < kChunkSteps; ++st) {
+        const uint4 a = tile[lrow * 32 + ((4 * st + lgrp) ^ lrow)];
+#pragma unroll
+        for (int t = 0; t < BT; ++t)
           acc[0][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-              as_bf16x8(a), as_bf16x8(xv), acc[0][t], 0, 0, 0);
-        }
+              as_bf16x8(a), as_bf16x8(xv[st][t]), acc[0][t], 0, 0, 0);
       }
     }
-  }
-  for (int64_t kb = k_beg; !WL && kb < k_end; kb += kStep * UN) {
-    uint4 wv[UN][RT];
+  } else {
+    // byte offset of column 0 of this lane's row in every row tile (wrapped
+    // for a row begun on the previous page, as above)
+    uint32_t ro[RT];
 #pragma unroll
-    for (int u = 0; u < UN; ++u) {
-      const int64_t kc = kb + u * kStep + 8 * lgrp;
-      const uint32_t oob = kc < k_end ? 0u : kOOB;
-      const uint32_t kc2 = static_cast<uint32_t>(kc * 2);
-#pragma unroll
-      for (int a = 0; a < RT; ++a) wv[u][a] = load16<BOOST_MFMA_W_AUX>(wr, (ro[a] + kc2) | oob);
+    for (int a = 0; a < RT; ++a) {
+      const int64_t r = rbase + 16 * a + lrow;
+      ro[a] = r > r_hi ? kOOB : static_cast<uint32_t>((r * K - pe0) * 2);
     }
+    // Column groups (UN steps of 32) with their weight and x fragments are
+    // loaded one group ahead: the group a step consumes is always the oldest
+    // set of outstanding loads, so the in-order wait counter lets the next
+    // group stay in flight while its MFMAs run.  Loads past k_end read zero.
+    constexpr int64_t kGroup = kStep * UN;
+    struct Group {
+      uint4 w[UN][RT];
+      uint4 x[UN][BT];
+    };
+    auto load_group = [&](int64_t kb, Group& g) {
 #pragma unroll
-    for (int u = 0; u < UN; ++u) {
-      const int64_t kc = kb + u * kStep + 8 * lgrp;
-      const uint32_t oob = kc < k_end ? 0u : kOOB;
-      const uint32_t kc2 = static_cast<uint32_t>(kc * 2);
-#pragma unroll
-      for (int t = 0; t < BT; ++t) {
-        const uint4 xv = load16(xr, (xo[t] + kc2) | oob);
+      for (int u = 0; u < UN; ++u) {
+        const int64_t kc = kb + u * kStep + 8 * lgrp;
+        const uint32_t oob = kc < k_end ? 0u : kOOB;
+        const uint32_t kc2 = static_cast<uint32_t>(kc * 2);
 #pragma unroll
         for (int a = 0; a < RT; ++a)
-          acc[a][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-              as_bf16x8(wv[u][a]), as_bf16x8(xv), acc[a][t], 0, 0, 0);
+          g.w[u][a] = load16<BOOST_MFMA_W_AUX>(wr, (ro[a] + kc2) | oob);
+#pragma unroll
+        for (int t = 0; t < BT; ++t) g.x[u][t] = load16(xr, (xo[t] + kc2) | oob);
       }
+    };
+    auto mma = [&](const Group& g) {
+#pragma unroll
+      for (int u = 0; u < UN; ++u)
+#pragma unroll
+        for (int t = 0; t < BT; ++t)
+#pragma unroll
+          for (int a = 0; a < RT; ++a)
+            acc[a][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                as_bf16x8(g.w[u][a]), as_bf16x8(g.x[u][t]), acc[a][t], 0, 0, 0);
+    };
+    // fixed register roles (copying a group whose loads are outstanding
+    // would wait for them); both halves always run, a group past k_end being
+    // zeros, so the loop has one exit and the accumulators one register set
+    Group ga, gb;
+    if (k_beg < k_end) load_group(k_beg, ga);
+#pragma unroll 1
+    for (int64_t kb = k_beg; kb < k_end; kb += 2 * kGroup) {
+      load_group(kb + kGroup, gb);
+      __builtin_amdgcn_sched_barrier(0);  // keep the prefetch ahead of the MFMAs
+      mma(ga);
+      load_group(kb + 2 * kGroup, ga);
+      __builtin_amdgcn_sched_barrier(0);
+      mma(gb);
     }
   }
 
@@ -514,12 +564,21 @@ __device__ void mfma_unit(const GemvParams& P, int page, int j, float* lds) {
     if (b >= P.B || r > r_hi) continue;
     const float v = lds[b * LS + i];
     const int64_t e0 = r * K;
-    if (e0 < pe0)
-      P.partial[(static_cast<int64_t>(page) * 2 + 1) * bst::kMaxGemvBatch + b] = v;
-    else if (e0 + K > pe1)
-      P.partial[(static_cast<int64_t>(page + 1) * 2) * bst::kMaxGemvBatch + b] = v;
-    else
-      store_y(P, b, r, v);
+    const int side = e0 < pe0 ? 1 : (e0 + K > pe1 ? 0 : -1);  // cut row: its part's side
+    if (P.S == 1) {
+      if (side == 1)
+        P.partial[(static_cast<int64_t>(page) * 2 + 1) * bst::kMaxGemvBatch + b] = v;
+      else if (side == 0)
+        P.partial[(static_cast<int64_t>(page + 1) * 2) * bst::kMaxGemvBatch + b] = v;
+      else
+        store_y(P, b, r, v);
+    } else if (side < 0) {
+      P.ws[(static_cast<int64_t>(slice) * P.B + b) * P.N + r] = v;
+    } else {
+      const int64_t bnd = side ? page : page + 1;
+      P.ws[static_cast<int64_t>(P.S) * P.B * P.N +
+           ((bnd * 2 + side) * P.S + slice) * P.B + b] = v;
+    }
   }
   __syncthreads();  // LDS is reused by the next unit of a persistent worker
 }
@@ -539,6 +598,29 @@ __global__ __launch_bounds__(kThreads) void mfma_kernel(GemvParams P) {
     const int u = bid - P.host_workers;
     mfma_unit<BT, RT, UN, WL>(P, P.hbm_pages[u / U], u % U, lds);
   }
+}
+
+// y of a split-K call: the S slice partials of every (batch row, row) in
+// slice order; a row cut by a page boundary adds its earlier page's slices,
+// then its later page's.  One lane per (b, n).
+__global__ __launch_bounds__(256) void split_reduce(GemvParams P) {
+  const int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (t >= static_cast<int64_t>(P.B) * P.N) return;
+  const int b = static_cast<int>(t / P.N);
+  const int64_t r = t % P.N;
+  const int64_t e0 = r * P.K;
+  const int64_t p0 = e0 / kPageElems, p1 = (e0 + P.K - 1) / kPageElems;
+  float v = 0.f;
+  if (p0 == p1) {
+    for (int s = 0; s < P.S; ++s) v += P.ws[(static_cast<int64_t>(s) * P.B + b) * P.N + r];
+  } else {
+    const float* cut = P.ws + static_cast<int64_t>(P.S) * P.B * P.N;
+    float v1 = 0.f;
+    for (int s = 0; s < P.S; ++s) v += cut[((p1 * 2 + 0) * P.S + s) * P.B + b];
+    for (int s = 0; s < P.S; ++s) v1 += cut[((p1 * 2 + 1) * P.S + s) * P.B + b];
+    v += v1;
+  }
+  store_y(P, b, r, v);
 }
 
 #ifndef BOOST_GEMV_UN1
@@ -630,17 +712,48 @@ int launch(GemvParams& P, int n_pages, bool need_fixup, const boost_ctx* ctx, hi
 //            MFMAs) when that still gives about one workgroup per CU, else
 //            two (the smaller matrices need the extra workgroups more);
 //   BT > 8:  two row tiles (four would need 256 accumulators per lane).
+// Split K over S workgroups when the row groups alone give fewer than two
+// workgroups per CU (small matrices at large batch); each slice keeps at
+// least 512 columns, and the partials must fit the context's workspace.
 template <int BT, int RT, int UN, bool WL>
 int launch_mfma_shape(GemvParams& P, int n_pages, bool need_fixup, const boost_ctx* ctx,
                       hipStream_t s) {
-  const int64_t grid = plan_grid(P, n_pages, 16 * RT, ctx);
+  P.S = 1;
+  int64_t grid = plan_grid(P, n_pages, 16 * RT, ctx);
   if (grid < 0) return bst::fail(BOOST_EINVAL, "grid too large");
+  const int64_t units = static_cast<int64_t>(n_pages) * P.units_per_page;
+  int S = 1;
+  while (S < kMaxSlices && units * S < 2 * ctx->n_cu && P.K / (2 * S) >= 512) S *= 2;
+  while (S > 1 && static_cast<uint64_t>(S) * P.B * (P.N + 2ull * (n_pages + 1)) >
+                      ctx->gemm_ws_floats)
+    S /= 2;
+  if (S > 1) {
+    P.S = S;
+    P.ws = ctx->gemm_ws;
+    P.units_per_page *= S;
+    grid = P.address_order ? static_cast<int64_t>(n_pages) * P.units_per_page
+                           : P.host_workers + static_cast<int64_t>(P.n_hbm_pages) *
+                                                  P.units_per_page;
+  }
   hipLaunchKernelGGL((mfma_kernel<BT, RT, UN, WL>), dim3(static_cast<unsigned>(grid)),
                      dim3(kThreads), 0, s, P);
   BOOST_HIP(hipGetLastError());
-  return launch_fixup(P, n_pages, need_fixup, s);
+  if (S == 1) return launch_fixup(P, n_pages, need_fixup, s);
+  const int64_t lanes = static_cast<int64_t>(P.B) * P.N;
+  hipLaunchKernelGGL(split_reduce, dim3(static_cast<unsigned>((lanes + 255) / 256)), dim3(256),
+                     0, s, P);
+  BOOST_HIP(hipGetLastError());
+  return BOOST_OK;
 }
 
+// Matrix-core shapes by batch tiles (16 rows of x each), from a sweep over the
+// 8B and 70B matrices at B = 16..256:
+//   BT <= 2: weights staged through LDS (row-contiguous streaming beat the
+//            A-fragment pattern by 10-25 %);
+//   BT 3..8: four 16-row tiles per wavefront (each x fragment serves four
+//            MFMAs) when that still gives about one workgroup per CU, else
+//            two (the smaller matrices need the extra workgroups more);
+//   BT > 8:  two row tiles (four would need 256 accumulators per lane).
 template <int BT>
 int launch_mfma(GemvParams& P, int n_pages, bool need_fixup, const boost_ctx* ctx,
                 hipStream_t s) {

@@ -18,6 +18,10 @@ struct boost_ctx {
   int host_coherent = 1;
   int gemv_schedule = BOOST_SCHED_CAP;
   int gemv_host_workers = 0;  // 0: default
+  // split-K partials of the matrix-core GEMM (slices of K run by different
+  // workgroups; a second kernel sums them in slice order)
+  float* gemm_ws = nullptr;
+  uint64_t gemm_ws_floats = 0;
 };
 
 namespace bst {
@@ -60,6 +64,7 @@ struct boost_tensor {
 
 namespace bst {
 constexpr int kMaxGemvBatch = 256;   // largest B of boost_decode_gemv
+constexpr uint64_t kGemmWsFloats = 16ull << 20;  // split-K workspace per context (64 MiB)
 }
 
 #include "dsr.h"

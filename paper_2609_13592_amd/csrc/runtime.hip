@@ -191,6 +191,12 @@ int boost_init(int device, boost_ctx** out) {
     }
     c->device = device;
     c->n_cu = p.multiProcessorCount;
+    c->gemm_ws_floats = kGemmWsFloats;
+    e = hipMalloc(&c->gemm_ws, c->gemm_ws_floats * sizeof(float));
+    if (e != hipSuccess) {
+      delete c;
+      return fail(BOOST_ENOMEM, "GEMM workspace: %s", hipGetErrorString(e));
+    }
   } else if (device != -1) {
     delete c;
     return fail(BOOST_EINVAL, "device %d", device);
@@ -200,6 +206,10 @@ int boost_init(int device, boost_ctx** out) {
 }
 
 int boost_shutdown(boost_ctx* ctx) {
+  if (ctx && ctx->gemm_ws) {
+    (void)hipSetDevice(ctx->device);
+    (void)hipFree(ctx->gemm_ws);
+  }
   delete ctx;
   return BOOST_OK;
 }
