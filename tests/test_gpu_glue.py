@@ -41,6 +41,36 @@ def test_rmsnorm_70b(gpu_ctx):
     assert_bf16_close(host_u16(out), ods.to_bf16(ods.rmsnorm(x.astype(np.float64), w)))
 
 
+@pytest.mark.parametrize("d", [4096, 12288, 1026, 36])
+def test_rmsnorm_widths(gpu_ctx, d):
+    """Vector path (d % 4 == 0, d <= 8192) and the plain loop (wider rows,
+    d % 4 != 0), ragged against 256 lanes."""
+    import torch
+    rng = np.random.default_rng(d)
+    x = (rng.standard_normal((3, d)) * 2).astype(np.float32)
+    w = synth.round_bf16((1 + 0.1 * rng.standard_normal(d)).astype(np.float32))
+    out = torch.empty((3, d), dtype=torch.int16, device="cuda")
+    bd.boost_rmsnorm(gpu_ctx, dev(x), to_dev_u16(w), 3, d, 1e-5, out, stream())
+    sync()
+    assert_bf16_close(host_u16(out), ods.to_bf16(ods.rmsnorm(x.astype(np.float64), w)))
+
+
+@pytest.mark.parametrize("V", [1001, 7, 4100])
+def test_argmax_lengths(gpu_ctx, V):
+    """Plain loop (V % 4 != 0) and the float4 path with a ragged tail; the
+    maximum planted at the last index and a tie planted early."""
+    rng = np.random.default_rng(V)
+    s = rng.standard_normal((4, V)).astype(np.float32)
+    s[0, V - 1] = 50.0
+    s[1, 2] = s[1, V - 2] = 60.0
+    ids = dev(np.zeros(4, np.int32))
+    bd.boost_argmax(gpu_ctx, dev(s), 4, V, ids, stream())
+    sync()
+    got = ids.cpu().numpy().tolist()
+    assert got == ods.argmax_lowest(s.astype(np.float64)).tolist()
+    assert got[:2] == [V - 1, 2]
+
+
 def test_rope_qkv_70b(gpu_ctx):
     import torch
     rng = np.random.default_rng(1)
