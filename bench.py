@@ -49,11 +49,15 @@ def parse():
     p.add_argument("--pmc-ref", action="store_true",
                    help="also run a plain 1 GiB device copy (counter scale reference)")
     p.add_argument("--workload", default="chain8b",
-                   choices=("chain8b", "llama70b", "throughput8b"),
+                   choices=("chain8b", "llama70b", "throughput8b", "host_share_sweep",
+                            "batch_sweep", "placements", "dsr_churn"),
                    help="chain8b: decode weight chain (default); llama70b: full 70B-"
                         "shaped decode step under a 120 GB HBM weight budget; "
                         "throughput8b: 8B-shaped decode at up to 256 requests under a "
-                        "40 GB HBM KV budget")
+                        "40 GB HBM KV budget; host_share_sweep, batch_sweep, "
+                        "placements, dsr_churn: the follow-up experiments (modulus "
+                        "sweep, batch sensitivity, contrast placements, allocator "
+                        "under Poisson arrivals)")
     p.add_argument("--no-literal", action="store_true",
                    help="throughput8b: skip the 256-request variant (~115 GB of "
                         "pinned host KV)")
@@ -703,6 +707,419 @@ def throughput8b(args, bd, ctx, torch, bw_hbm, bw_host, alpha):
     }
 
 
+# ------------------------------------------------------------ experiments
+def _gemv_us(bd, ctx, torch, handles, N, K, x, B, y, reps):
+    """Median microseconds of one GEMV over a rotation of placed copies."""
+    sp = torch.cuda.current_stream().cuda_stream
+
+    def run():
+        for h in handles:
+            bd.boost_decode_gemv(ctx, h, N, K, x, B, y, bd.DTYPE_F32, sp)
+    run()
+    torch.cuda.synchronize()
+    return float(np.median(time_steps(torch, run, reps))) * 1e3 / len(handles)
+
+
+def _seeded_weight(torch, N, K, seed):
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    w = torch.randn((N, K), generator=g, device="cuda").mul_(0.02)
+    return w.to(torch.bfloat16).view(torch.int16)
+
+
+def host_share_sweep(args, bd, ctx, torch, bw_hbm, bw_host, alpha, M_alpha):
+    """Speedup of a tiered GEMV over all-HBM as the host share grows (the
+    host-share sweep of §3): one 2 GiB bf16 matrix [131072 x 8192] (1024
+    pages), batch 1, modulo placement at a range of moduli; the best one is
+    the measured-optimal modulus, set beside the one from the measured alpha."""
+    N, K = 131072, 8192
+    nbytes = N * K * 2
+    n = nbytes // bd.PAGE_BYTES
+    w = _seeded_weight(torch, N, K, 4242)
+    x = torch.from_numpy(np.random.default_rng(7).standard_normal(
+        (1, K)).astype(np.float32)).cuda().to(torch.bfloat16).view(torch.int16)
+    y = torch.empty((1, N), dtype=torch.float32, device="cuda")
+    hbm = bd.boost_place_weights_map(ctx, w, nbytes, np.zeros(n, np.uint8))
+    mods = sorted({1025, 512, 400, 300, 250, 200, 160, 140, M_alpha, 120, 111, 100,
+                   90, 80, 64, 50, 32}, reverse=True)
+    placed = {m: bd.boost_place_weights(ctx, w, nbytes, m) for m in mods}
+    del w
+    torch.cuda.empty_cache()
+    rows = {m: [] for m in mods}
+    ref = []
+    for _ in range(max(3, args.steps // 5)):
+        ref.append(_gemv_us(bd, ctx, torch, [hbm], N, K, x, 1, y, 5))
+        for m in mods:
+            rows[m].append(_gemv_us(bd, ctx, torch, [placed[m]], N, K, x, 1, y, 5))
+    t_hbm = float(np.median(ref))
+    out = []
+    for m in mods:
+        h = int(bd.boost_tensor_tiers(placed[m]).sum())
+        t = float(np.median(rows[m]))
+        f = h / n
+        bound = max((1 - f) * nbytes / (bw_hbm * 1e3), f * nbytes / (bw_host * 1e3))
+        out.append({"M": m, "host_pages": h, "host_share": round(f, 5), "us": round(t, 2),
+                    "speedup_vs_hbm_only": round(t_hbm / t, 4),
+                    "placement_bound_us": round(bound, 2),
+                    "ideal_combined_us": round(nbytes / ((bw_hbm + bw_host) * 1e3), 2)})
+        bd.boost_tensor_free(placed[m])
+    bd.boost_tensor_free(hbm)
+    best = max(out, key=lambda r: (r["speedup_vs_hbm_only"], r["M"]))
+    return {"metric": "tiered GEMV speedup over all-HBM vs host share (modulus sweep)",
+            "value": best["speedup_vs_hbm_only"], "unit": "x", "n_gpus": 1,
+            "higher_is_better": True, "dtype": "bf16", "data": "synthetic",
+            "config": {"workload": "host-share sweep: bf16 GEMV [131072 x 8192] (2 GiB, "
+                                   "1024 pages), batch 1, modulo placement, CAP schedule"},
+            "calibration": {"hbm_gbps": round(bw_hbm, 1), "host_gbps": round(bw_host, 2),
+                            "alpha": round(alpha, 6), "M_from_alpha": M_alpha},
+            "hbm_only_us": round(t_hbm, 2), "best_M": best["M"], "sweep": out}
+
+
+def batch_sweep(args, bd, ctx, torch, bw_hbm, bw_host, alpha, M):
+    """Tiered (modulo placement at the measured modulus) vs all-HBM GEMV/GEMM
+    time as the batch grows (the batch sensitivity study of §5.10): the
+    tensors of the 8B and 70B shapes large enough to hold host pages at this
+    modulus, batches 1..256."""
+    shapes = {"8b_lm_head": (128256, 4096), "70b_gate_up": (57344, 8192),
+              "70b_down": (8192, 28672), "70b_lm_head": (128256, 8192)}
+    batches = [1, 2, 4, 8, 16, 32, 64, 128, 256]
+    res = {}
+    for si, (name, (N, K)) in enumerate(shapes.items()):
+        nbytes = N * K * 2
+        n = -(-nbytes // bd.PAGE_BYTES)
+        w = _seeded_weight(torch, N, K, 777 + si)
+        hbm = bd.boost_place_weights_map(ctx, w, nbytes, np.zeros(n, np.uint8))
+        tiered = bd.boost_place_weights(ctx, w, nbytes, M)
+        host = int(bd.boost_tensor_tiers(tiered).sum())
+        del w
+        torch.cuda.empty_cache()
+        g = torch.Generator(device="cuda")
+        g.manual_seed(9)
+        xs = torch.randn((max(batches), K), generator=g, device="cuda").to(
+            torch.bfloat16).view(torch.int16)
+        y = torch.empty((max(batches), N), dtype=torch.float32, device="cuda")
+        rows = []
+        for B in batches:
+            x = xs[:B].contiguous()
+            a, b = [], []
+            for _ in range(max(3, args.steps // 5)):
+                a.append(_gemv_us(bd, ctx, torch, [hbm], N, K, x, B, y, 3))
+                b.append(_gemv_us(bd, ctx, torch, [tiered], N, K, x, B, y, 3))
+            ta, tb = float(np.median(a)), float(np.median(b))
+            alg = nbytes + B * K * 2 + B * N * 4
+            rows.append({"B": B, "hbm_us": round(ta, 2), "tiered_us": round(tb, 2),
+                         "speedup_vs_hbm_only": round(ta / tb, 4),
+                         "tiered_gbps": round(alg / tb / 1e3, 1),
+                         "tiered_tflops": round(2 * N * K * B / tb / 1e6, 2),
+                         "path": "gemv" if B < 7 else "mfma"})
+        res[name] = {"N": N, "K": K, "pages": n, "host_pages": host, "rows": rows}
+        bd.boost_tensor_free(hbm)
+        bd.boost_tensor_free(tiered)
+        del xs, y
+        torch.cuda.empty_cache()
+    sp = [r["speedup_vs_hbm_only"] for v in res.values() for r in v["rows"]]
+    return {"metric": "tiered vs all-HBM GEMV/GEMM speedup by batch size",
+            "value": round(float(np.exp(np.mean(np.log(sp)))), 4), "unit": "x (geomean)",
+            "n_gpus": 1, "higher_is_better": True, "dtype": "bf16", "data": "synthetic",
+            "config": {"workload": "batch sweep 1..256 of the 8B/70B tensors that hold host "
+                                   "pages at the measured modulus", "modulus": M},
+            "calibration": {"hbm_gbps": round(bw_hbm, 1), "host_gbps": round(bw_host, 2),
+                            "alpha": round(alpha, 6)},
+            "shapes": res}
+
+
+def _window_stats(tiers, P):
+    """Host-page fraction of every full window of P consecutive pages of the
+    chain in launch order: mean, standard deviation and largest deviation."""
+    t = np.asarray(tiers, dtype=np.float64)
+    nw = len(t) // P
+    if nw == 0:
+        return {"windows": 0}
+    f = t[:nw * P].reshape(nw, P).mean(axis=1)
+    return {"windows": nw, "pages_per_window": P, "mean": round(float(f.mean()), 6),
+            "sd": round(float(f.std()), 6), "max_dev": round(float(np.abs(f - f.mean()).max()), 6)}
+
+
+def placements_bench(args, bd, ctx, torch, bw_hbm, bw_host, alpha, M):
+    """The 8B decode weight chain (batch 1) under the contrast placements
+    (§2.6, §5.6, §5.7): all-HBM, modulo placement restarted per tensor (the
+    method), modulo pattern continued across tensors (an interleave blind to
+    kernel boundaries), a linear split per tensor, and random placement
+    (BAPP-R, seeded draws); each with the CAP and the address-order
+    schedule."""
+    import synth
+    per_layer, head = synth.chain_shapes(synth.LLAMA8B)
+    specs = [(l, kind, n, k) for l in range(args.layers) for _, kind, n, k in per_layer]
+    specs.append((0, head[1], head[2], head[3]))
+    kinds = {"hbm": None, "mpp": bd.PLACE_MPP, "mpp_global": bd.PLACE_MPP_GLOBAL,
+             "linear": bd.PLACE_LINEAR, "bapp_r": bd.PLACE_RANDOM}
+    rng = np.random.default_rng(7)
+    xs = {K: torch.from_numpy(synth.normal_bf16(rng, (1, K), 1.0).view(np.int16)).cuda()
+          for K in sorted({s[3] for s in specs})}
+    ops = {k: [] for k in kinds}
+    tiers = {k: [] for k in kinds}
+    phase = 0
+    for t, (l, kind, N, K) in enumerate(specs):
+        w = synth.chain_weight_torch(l, kind, N, K, "cuda").view(torch.int16)
+        nbytes = N * K * 2
+        n = -(-nbytes // bd.PAGE_BYTES)
+        for name, pk in kinds.items():
+            if pk is None:
+                tm = np.zeros(n, np.uint8)
+            else:
+                tm = bd.boost_plan_contrast(pk, nbytes, M, phase,
+                                            synth.uniforms(5000 + t, n))
+            ops[name].append((bd.boost_place_weights_map(ctx, w, nbytes, tm), N, K))
+            tiers[name].append(tm)
+        phase += n
+        del w
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    ys = {N: torch.empty((1, N), dtype=torch.float32, device="cuda")
+          for N in {s[2] for s in specs}}
+    sp = torch.cuda.current_stream().cuda_stream
+    alg = sum(N * K * 2 + K * 2 + N * 4 for _, _, N, K in specs)
+
+    def step(name):
+        for h, N, K in ops[name]:
+            bd.boost_decode_gemv(ctx, h, N, K, xs[K], 1, ys[N], bd.DTYPE_F32, sp)
+    res = {}
+    for sched in ("cap", "address"):
+        bd.boost_gemv_set_schedule(ctx, bd.SCHED_CAP if sched == "cap" else bd.SCHED_ADDRESS,
+                                   args.host_workers)
+        for name in kinds:
+            step(name)
+        torch.cuda.synchronize()
+        ms = {k: [] for k in kinds}
+        for _ in range(max(5, args.steps // 2)):
+            for name in kinds:
+                ms[name].append(time_steps(torch, lambda: step(name), 1)[0])
+        for name in kinds:
+            t = float(np.median(ms[name]))
+            res.setdefault(name, {})[sched] = {"ms_per_step": round(t, 4),
+                                               "gbps": round(alg / (t * 1e-3) / 1e9, 1)}
+    bd.boost_gemv_set_schedule(ctx, bd.SCHED_CAP, args.host_workers)
+    # one grid wave of the batch-1 GEMV covers about 2048 workgroups x 32 KiB
+    wave_pages = 32
+    for name in kinds:
+        shares = [float(tm.mean()) for tm in tiers[name]]
+        res[name].update({
+            "host_pages": int(sum(int(tm.sum()) for tm in tiers[name])),
+            "tensors_with_host_pages": int(sum(1 for tm in tiers[name] if tm.any())),
+            "max_tensor_host_share": round(max(shares), 5),
+            "waves": _window_stats(np.concatenate(tiers[name]), wave_pages)})
+        for sched in ("cap", "address"):
+            res[name][sched]["speedup_vs_hbm_only"] = round(
+                res["hbm"][sched]["ms_per_step"] / res[name][sched]["ms_per_step"], 4)
+        for h, _, _ in ops[name]:
+            bd.boost_tensor_free(h)
+    return {"metric": "decode weight-chain step ms by placement (contrast placements)",
+            "value": res["mpp"]["cap"]["ms_per_step"], "unit": "ms",
+            "n_gpus": 1, "higher_is_better": False, "dtype": "bf16", "data": "synthetic",
+            "config": {"workload": "Llama-3-8B-shaped decode weight chain, batch 1, under "
+                                   "all-HBM / modulo (per tensor) / modulo across tensors / "
+                                   "linear / random placement", "modulus": M,
+                       "layers": args.layers, "bytes_per_step": int(alg)},
+            "calibration": {"hbm_gbps": round(bw_hbm, 1), "host_gbps": round(bw_host, 2),
+                            "alpha": round(alpha, 6)},
+            "placements": res}
+
+
+def run_churn(trace, steps, max_batch, alloc, free, stats, on_step=None):
+    """Decode-serving loop over a request trace, driving a KV block allocator.
+
+    trace: (arrival step, prompt tokens, output tokens) per request, request id =
+    index.  Each step: arrivals join a FIFO queue; queued requests are admitted
+    in order while fewer than max_batch run, each allocating the blocks of its
+    prompt (a refusal leaves it and everything behind it queued: the call is
+    handed back to the scheduler, §4.3); every running request then appends
+    one token, allocating one more block when its last block is full (when
+    the pool is out of blocks the latest admitted request is preempted: freed
+    and queued again in front, to be recomputed); requests that produced their
+    output are freed.  alloc(rid, n) returns block ids or None, free(rid) releases a
+    request, stats() returns (used blocks, used host head-blocks, SHH
+    requests).  on_step(step, running) may time the step's batch.  Returns
+    per-step rows (used blocks, host head-blocks, running, queued, SHH
+    requests) and counters."""
+    queue, running = [], []
+    tokens, made, blocks = {}, {}, {}
+    nxt = 0
+    rows = []
+    refused = preempted = done = 0
+    for step in range(steps):
+        while nxt < len(trace) and trace[nxt][0] <= step:
+            queue.append(nxt)
+            nxt += 1
+        while queue and len(running) < max_batch:
+            rid = queue[0]
+            prompt = trace[rid][1]
+            ids = alloc(rid, (prompt + 15) // 16)
+            if ids is None:
+                refused += 1
+                break
+            queue.pop(0)
+            running.append(rid)
+            tokens[rid], made[rid], blocks[rid] = prompt, 0, list(ids)
+        i = 0
+        while i < len(running):
+            rid = running[i]
+            if tokens[rid] % 16 == 0:
+                ids = alloc(rid, 1)
+                while ids is None:
+                    # out of blocks: preempt the latest admitted request (its
+                    # blocks are freed and it is queued again in front, to be
+                    # recomputed), then retry unless it was this one
+                    victim = running.pop()
+                    free(victim)
+                    del tokens[victim], made[victim], blocks[victim]
+                    queue.insert(0, victim)
+                    preempted += 1
+                    if victim == rid:
+                        break
+                    ids = alloc(rid, 1)
+                if ids is None:
+                    continue
+                blocks[rid].extend(ids)
+            tokens[rid] += 1
+            made[rid] += 1
+            i += 1
+        if on_step is not None and running:
+            on_step(step, running, tokens, blocks)
+        keep = []
+        for rid in running:
+            if made[rid] >= trace[rid][2]:
+                free(rid)
+                done += 1
+                del tokens[rid], made[rid], blocks[rid]
+            else:
+                keep.append(rid)
+        running = keep
+        used, host, shh = stats()
+        rows.append((used, host, len(running), len(queue), shh))
+    return np.array(rows, dtype=np.int64), {"refused_admissions": refused,
+                                            "preemptions": preempted, "finished": done,
+                                            "arrived": nxt}
+
+
+def _rolling_median(x, w):
+    if len(x) < w:
+        return np.array([np.median(x)]) if len(x) else np.array([])
+    v = np.lib.stride_tricks.sliding_window_view(x, w)
+    return np.median(v, axis=1)
+
+
+def dsr_churn(args, bd, ctx, torch, bw_hbm, bw_host, alpha, M):
+    """The wave-aware KV allocator under Poisson arrivals (the realized host
+    ratio study of §5.11, with a synthetic arrival trace in place of the
+    paper's LongWriter requests): the realized host share of the KV in use per
+    step, its rolling median and range, against the pool's target; twice: at
+    the paper's setting (4 KV heads, modulus 12) and at this GPU's (8 KV
+    heads, measured modulus).  On the GPU, the paged-attention time of the
+    running batch (one layer, 32/8 heads) on sampled steps, wave-aware pool vs
+    an all-HBM pool fed the same trace."""
+    import synth
+    steps, warm, window = 20000, 2000, 100
+    trace = synth.poisson_arrivals(11, steps, 0.03, 256, 2048, 512, 4096)
+    NB, max_batch = 16000, 256
+    out = {}
+    for tag, H, m in (("paper_h4_m12", 4, 12), ("this_gpu", 8, M)):
+        plan = bd.boost_init(-1)
+        pool = bd.boost_kv_pool_create(plan, 1, H, 128, NB, m, bd.KV_LPP, q_heads=4 * H)
+        info = bd.boost_kv_pool_info(pool)
+
+        def alloc(rid, n):
+            ids = bd.boost_kv_alloc(pool, rid, n)
+            return None if ids == bd.EAGAIN else ids
+
+        def stats():
+            s = bd.boost_kv_stats(pool)
+            return s["used_blocks"], s["used_host_head_blocks"], s["shh_requests"]
+        rows, cnt = run_churn(trace, steps, max_batch, alloc,
+                              lambda rid: bd.boost_kv_free(pool, rid), stats)
+        bd.boost_kv_pool_destroy(pool)
+        bd.boost_shutdown(plan)
+        used, host = rows[warm:, 0].astype(np.float64), rows[warm:, 1].astype(np.float64)
+        share = np.where(used > 0, host / np.maximum(used * H, 1), 0.0)
+        rm = _rolling_median(share, window)
+        nb = int(info["nb_pool"])
+        target = (info["n_shh"] * info["shh_host_heads"] +
+                  (nb - info["n_shh"]) * info["local_host_heads"]) / (nb * H)
+        out[tag] = {"kv_heads": H, "modulus": m, "pool_blocks": nb,
+                    "shh_blocks": int(info["n_shh"]), "ideal_share": round(1 / m, 5),
+                    "pool_share": round(float(target), 5), "tau": round(info["tau"], 5),
+                    "mean_share": round(float(share.mean()), 5),
+                    "rolling_median_min": round(float(rm.min()), 5),
+                    "rolling_median_max": round(float(rm.max()), 5),
+                    "min_share": round(float(share.min()), 5),
+                    "max_share": round(float(share.max()), 5),
+                    "mean_running": round(float(rows[warm:, 2].mean()), 1),
+                    "mean_blocks_in_use": round(float(used.mean()), 1),
+                    "steps": steps, "warmup_steps": warm, "window": window, **cnt}
+    # GPU: attention time of the running batch on sampled steps
+    Hq, H, D = 32, 8, 128
+    mb = (2048 + 4096 + 15) // 16 + 1
+    g = torch.Generator(device="cuda")
+    g.manual_seed(3)
+    q = torch.randn((max_batch, Hq, D), generator=g, device="cuda").to(torch.bfloat16)
+    o = torch.empty((max_batch, Hq, D), dtype=torch.float32, device="cuda")
+    sp = torch.cuda.current_stream().cuda_stream
+    times = {}
+    for tag, mode, m in (("boost", bd.KV_LPP, M), ("hbm", bd.KV_ALL_HBM, 0)):
+        pool = bd.boost_kv_pool_create(ctx, 1, H, D, NB, m, mode, q_heads=Hq,
+                                       max_batch=max_batch, max_blocks_per_seq=mb)
+        ms = []
+
+        def alloc(rid, n):
+            ids = bd.boost_kv_alloc(pool, rid, n)
+            return None if ids == bd.EAGAIN else ids
+
+        def stats():
+            s = bd.boost_kv_stats(pool)
+            return s["used_blocks"], s["used_host_head_blocks"], s["shh_requests"]
+
+        def on_step(step, running, tokens, blocks):
+            if step < warm or step % 20:
+                return
+            B = len(running)
+            tab = np.full((B, mb), -1, np.int32)
+            for i, rid in enumerate(running):
+                tab[i, :len(blocks[rid])] = blocks[rid]
+            lens = np.array([tokens[rid] for rid in running], np.int32)
+            td = torch.from_numpy(tab).cuda()
+            ld = torch.from_numpy(lens).cuda()
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record()
+            bd.boost_paged_attn_decode(ctx, pool, 0, q, B, Hq, td, mb, ld, 0.0, o,
+                                       bd.DTYPE_F32, sp)
+            b.record()
+            torch.cuda.synchronize()
+            ms.append(a.elapsed_time(b))
+        run_churn(trace, steps, max_batch, alloc, lambda rid: bd.boost_kv_free(pool, rid),
+                  stats, on_step)
+        bd.boost_kv_pool_destroy(pool)
+        times[tag] = np.array(ms)
+    ratio = times["hbm"] / times["boost"]
+    out["attention_steps"] = {
+        "sampled_steps": int(len(ratio)),
+        "boost_ms_p50": round(float(np.percentile(times["boost"], 50)), 4),
+        "boost_ms_p99": round(float(np.percentile(times["boost"], 99)), 4),
+        "hbm_ms_p50": round(float(np.percentile(times["hbm"], 50)), 4),
+        "hbm_ms_p99": round(float(np.percentile(times["hbm"], 99)), 4),
+        "median_speedup_vs_hbm_only": round(float(np.median(ratio)), 4)}
+    p = out["paper_h4_m12"]
+    return {"metric": "realized KV host share under Poisson arrivals (wave-aware pool)",
+            "value": p["mean_share"], "unit": "fraction of KV bytes in use",
+            "n_gpus": 1, "higher_is_better": None, "dtype": "bf16", "data": "synthetic",
+            "config": {"workload": "Poisson arrivals 0.03 per step over 20000 decode steps, "
+                                   "prompts U[256, 2048], outputs U[512, 4096], at most 256 "
+                                   "running, 16000-block pool",
+                       "modulus": M},
+            "calibration": {"hbm_gbps": round(bw_hbm, 1), "host_gbps": round(bw_host, 2),
+                            "alpha": round(alpha, 6)},
+            "results": out}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -724,6 +1141,18 @@ def main():
         b.copy_(a)
         torch.cuda.synchronize()
         del a, b
+    exp = {"host_share_sweep": lambda: host_share_sweep(args, bd, ctx, torch, bw_hbm,
+                                                        bw_host, alpha, M),
+           "batch_sweep": lambda: batch_sweep(args, bd, ctx, torch, bw_hbm, bw_host,
+                                              alpha, M),
+           "placements": lambda: placements_bench(args, bd, ctx, torch, bw_hbm, bw_host,
+                                                  alpha, M),
+           "dsr_churn": lambda: dsr_churn(args, bd, ctx, torch, bw_hbm, bw_host, alpha, M)}
+    if args.workload in exp:
+        out = exp[args.workload]()
+        bd.boost_shutdown(ctx)
+        print(json.dumps(out), flush=True)
+        return
     if args.workload in ("llama70b", "throughput8b"):
         if args.workload == "llama70b":
             if args.layers == 32:

@@ -50,6 +50,12 @@ extern "C" {
 #define BOOST_DTYPE_F32 0
 #define BOOST_DTYPE_BF16 1
 
+/* Placement kinds of boost_plan_contrast */
+#define BOOST_PLACE_MPP 0        /* modulo placement, restarted per tensor  */
+#define BOOST_PLACE_MPP_GLOBAL 1 /* modulo pattern continued across tensors */
+#define BOOST_PLACE_LINEAR 2     /* first pages HBM, last floor(n/M) host   */
+#define BOOST_PLACE_RANDOM 3     /* BAPP-R: each page host w.p. 1/M         */
+
 #define BOOST_PAGE_BYTES (2ull * 1024ull * 1024ull)
 
 typedef struct boost_ctx boost_ctx;
@@ -119,6 +125,27 @@ int boost_superpage_pages(uint64_t footprint_bytes, uint32_t *S);
  * *n_pages.  Pure CPU.  Errors: EINVAL (bytes 0, M < 2, null n_pages). */
 int boost_plan_mpp(uint64_t bytes, uint32_t M, uint64_t footprint_bytes,
                    uint8_t *tier_out, uint64_t tier_cap, uint64_t *n_pages);
+
+/* Contrast placements of one tensor for the comparisons the paper draws
+ * against modulo placement (§2.6 bandwidth-aware random placement BAPP-R and
+ * Linux weighted interleaving, §5.6, §5.7 proportional interleave).  n =
+ * ceil(bytes / 2 MiB) pages; page i is on host iff
+ *   BOOST_PLACE_MPP         i mod M == M - 1 (same map as boost_plan_mpp, S=1);
+ *   BOOST_PLACE_MPP_GLOBAL  (phase + i) mod M == M - 1, where phase is the
+ *                           number of pages of the tensors placed before this
+ *                           one: the modulo pattern is not restarted per tensor
+ *                           (an interleave blind to kernel boundaries, §2.6);
+ *   BOOST_PLACE_LINEAR      i >= n - floor(n / M) (the linear split of §4.2
+ *                           applied to a weight tensor);
+ *   BOOST_PLACE_RANDOM      uniforms[i] * M < 1 (fp64), with uniforms[0..n) in
+ *                           [0, 1) drawn by the caller (BAPP-R, §2.6).
+ * phase and uniforms are ignored by the kinds that do not use them (uniforms
+ * may then be NULL).  Writes min(n, tier_cap) codes to tier_out (may be NULL)
+ * and n to *n_pages.  Pure CPU.  Errors: EINVAL (bytes 0, M < 2, unknown
+ * kind, null n_pages, RANDOM without uniforms). */
+int boost_plan_contrast(int kind, uint64_t bytes, uint32_t M, uint64_t phase,
+                        const double *uniforms, uint8_t *tier_out,
+                        uint64_t tier_cap, uint64_t *n_pages);
 
 /* C3: modulus under an HBM budget.  The paper always places about an alpha
  * share on host; when the weights exceed a budget we keep the modulo rule and

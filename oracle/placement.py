@@ -12,7 +12,10 @@ Paper passages followed:
   * §4.4: when 1/alpha is not an integer, K = ceil(1/alpha), keeping the host
     share below alpha.
   * §2.6 "Bandwidth-Aware Page Placement": BAPP-R, a random alpha share of pages
-    on host (contrast only).
+    on host (contrast only); Linux weighted interleaving stripes pages over
+    the tiers without regard to kernel (tensor) boundaries (contrast only).
+  * §5.7: proportional interleaving, i.e. a linear split, on weights
+    (contrast only).
   * §4.2 "LPP": the first 1/(1+alpha) of pages in HBM, the rest on host.
 """
 from __future__ import annotations
@@ -107,6 +110,27 @@ def bapp_r_map(n: int, share: float, seed: int) -> np.ndarray:
     probability ``share`` (seeded)."""
     rng = np.random.default_rng(seed)
     return (rng.random(n) < share).astype(np.uint8)
+
+
+def bapp_r_from_uniforms(u, M: int) -> np.ndarray:
+    """BAPP-R (§2.6) with the random draws given: page i on host iff
+    u[i] * M < 1, i.e. u[i] < 1/M written without the rounded reciprocal.
+    The draws are inputs (uniform on [0, 1)), so any implementation fed the
+    same draws makes the same decisions."""
+    u = np.asarray(u, dtype=np.float64)
+    return (u * float(M) < 1.0).astype(np.uint8)
+
+
+def mpp_global_map(n: int, M: int, phase: int) -> np.ndarray:
+    """Modulo placement that is NOT restarted per tensor (the contrast to
+    §3.1's per-tensor allocation; an interleave blind to tensor boundaries,
+    §2.6): a tensor whose first page has global index ``phase`` (pages of
+    the tensors placed before it) puts page i on host iff
+    (phase + i) mod M == M - 1."""
+    if M < 2:
+        raise ValueError("M must be >= 2")
+    g = int(phase) + np.arange(int(n), dtype=np.int64)
+    return (g % M == M - 1).astype(np.uint8)
 
 
 def linear_map(n: int, M: int) -> np.ndarray:

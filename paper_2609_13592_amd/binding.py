@@ -20,6 +20,7 @@ OK, EINVAL, ENOMEM, EAGAIN, ENODEV, EHIP = 0, -22, -12, -11, -19, -5
 KV_LPP, KV_ALL_HBM, KV_ALL_HOST, KV_BUDGET = 0, 1, 2, 3
 KV_LOCAL, KV_SHH = 0, 1
 TIER_HBM, TIER_HOST = 0, 1
+PLACE_MPP, PLACE_MPP_GLOBAL, PLACE_LINEAR, PLACE_RANDOM = 0, 1, 2, 3
 DTYPE_F32, DTYPE_BF16 = 0, 1
 SCHED_ADDRESS, SCHED_CAP = 0, 1
 PAGE_BYTES = 2 * 1024 * 1024
@@ -70,6 +71,8 @@ _SIGS = {
     "boost_modulus_from_alpha": (_i32, [_dbl, C.POINTER(_u32)]),
     "boost_superpage_pages": (_i32, [_u64, C.POINTER(_u32)]),
     "boost_plan_mpp": (_i32, [_u64, _u32, _u64, _vp, _u64, C.POINTER(_u64)]),
+    "boost_plan_contrast": (_i32, [_i32, _u64, _u32, _u64, _vp, _vp, _u64,
+                                   C.POINTER(_u64)]),
     "boost_modulus_from_budget": (_i32, [_vp, _vp, C.c_size_t, _u64, _u32,
                                          C.POINTER(_u32)]),
     "boost_place_weights": (_i32, [_vp, _vp, _u64, _u32, _u64, C.POINTER(_vp)]),
@@ -236,6 +239,19 @@ def boost_plan_mpp(nbytes: int, M: int, footprint: int = 0) -> np.ndarray:
     _check(load().boost_plan_mpp(nbytes, M, footprint, _ptr(out), out.size,
                                  C.byref(n)))
     return out
+
+
+def boost_plan_contrast(kind: int, nbytes: int, M: int, phase: int = 0,
+                        uniforms=None) -> np.ndarray:
+    n = -(-int(nbytes) // PAGE_BYTES)
+    u = None if uniforms is None else np.ascontiguousarray(uniforms, dtype=np.float64)
+    if u is not None and u.size < n:
+        raise ValueError(f"{n} uniforms needed, {u.size} given")
+    out = np.zeros(max(n, 1), dtype=np.uint8)
+    got = _u64()
+    _check(load().boost_plan_contrast(kind, nbytes, M, phase, _ptr(u), _ptr(out),
+                                      out.size, C.byref(got)))
+    return out[:got.value]
 
 
 def boost_modulus_from_budget(sizes, budget: int, M_alpha: int, footprints=None) -> int:

@@ -1,7 +1,9 @@
 // Placement engine (CPU only): modulus from the bandwidth ratio, modulo page
 // placement over superpages with per-tensor restart, modulus under an HBM
 // budget.  Follows §3.1 (modulo placement, per-tensor allocation), §3.2 and
-// §4.4 (superpages of lcm(CTA footprint, page); ceil rule).
+// §4.4 (superpages of lcm(CTA footprint, page); ceil rule).  Contrast
+// placements for the comparisons of §2.6 and §5.7: modulo placement without
+// the per-tensor restart, a linear split, and random (BAPP-R) placement.
 #include <cmath>
 #include <cstring>
 #include <numeric>
@@ -86,6 +88,45 @@ int boost_plan_mpp(uint64_t bytes, uint32_t M, uint64_t footprint_bytes,
   if (rc) return rc;
   *n_pages = t.size();
   if (tier_out) std::memcpy(tier_out, t.data(), std::min<uint64_t>(tier_cap, t.size()));
+  return BOOST_OK;
+}
+
+int boost_plan_contrast(int kind, uint64_t bytes, uint32_t M, uint64_t phase,
+                        const double* uniforms, uint8_t* tier_out, uint64_t tier_cap,
+                        uint64_t* n_pages) {
+  if (!n_pages) return fail(BOOST_EINVAL, "null n_pages");
+  if (bytes == 0) return fail(BOOST_EINVAL, "tensor of 0 bytes");
+  if (M < 2) return fail(BOOST_EINVAL, "modulus M=%u < 2", M);
+  const uint64_t n = pages_of(bytes);
+  std::vector<uint8_t> t(n, BOOST_TIER_HBM);
+  switch (kind) {
+    case BOOST_PLACE_MPP: {
+      int rc = mpp_tiers(bytes, M, 0, t);
+      if (rc) return rc;
+      break;
+    }
+    case BOOST_PLACE_MPP_GLOBAL:
+      // the modulo pattern runs on over the pages of earlier tensors: the
+      // page with global index phase + i is on host iff that index is the
+      // last of its group of M
+      for (uint64_t i = 0; i < n; ++i)
+        if ((phase + i) % M == M - 1) t[i] = BOOST_TIER_HOST;
+      break;
+    case BOOST_PLACE_LINEAR:
+      // the first pages in HBM, the last floor(n / M) on host
+      for (uint64_t i = n - n / M; i < n; ++i) t[i] = BOOST_TIER_HOST;
+      break;
+    case BOOST_PLACE_RANDOM:
+      if (!uniforms) return fail(BOOST_EINVAL, "random placement needs n uniforms");
+      // each page on host with probability 1/M, decided by the caller's draw
+      for (uint64_t i = 0; i < n; ++i)
+        if (uniforms[i] * M < 1.0) t[i] = BOOST_TIER_HOST;
+      break;
+    default:
+      return fail(BOOST_EINVAL, "placement kind %d", kind);
+  }
+  *n_pages = n;
+  if (tier_out) std::memcpy(tier_out, t.data(), std::min<uint64_t>(tier_cap, n));
   return BOOST_OK;
 }
 

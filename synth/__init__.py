@@ -33,6 +33,11 @@ def round_bf16(a: np.ndarray) -> np.ndarray:
     return r
 
 
+def uniforms(seed: int, n: int) -> np.ndarray:
+    """n draws uniform on [0, 1) (float64) from ``default_rng(seed)``."""
+    return np.random.default_rng(seed).random(int(n))
+
+
 def normal_bf16(rng: np.random.Generator, shape, sigma: float) -> np.ndarray:
     f = rng.standard_normal(shape, dtype=np.float32)
     if sigma != 1.0:
@@ -131,3 +136,18 @@ def churn_trace(seed: int, n_events: int, batch: int, lo: int, hi: int):
     victims = rng.integers(0, batch, size=n_events)
     lengths = rng.integers(lo, hi, size=n_events, endpoint=True)
     return [(int(v), int(l)) for v, l in zip(victims, lengths)]
+
+
+def poisson_arrivals(seed: int, steps: int, rate: float, prompt_lo: int, prompt_hi: int,
+                     out_lo: int, out_hi: int):
+    """Requests arriving over `steps` decode steps: the number arriving at each
+    step is Poisson(rate); each request has a prompt length and an output
+    length, uniform integers in the closed ranges.  Returns a list of
+    (arrival step, prompt length, output length) in arrival order."""
+    rng = np.random.default_rng(seed)
+    counts = rng.poisson(rate, size=steps)
+    n = int(counts.sum())
+    prompts = rng.integers(prompt_lo, prompt_hi, size=n, endpoint=True)
+    outs = rng.integers(out_lo, out_hi, size=n, endpoint=True)
+    steps_of = np.repeat(np.arange(steps), counts)
+    return [(int(s), int(p), int(o)) for s, p, o in zip(steps_of, prompts, outs)]

@@ -106,3 +106,40 @@ def test_budget_modulus_70b_chain():
     per_layer = [(64 + 16) * 128 * d * 2, d * 64 * 128 * 2, 2 * f * d * 2, d * f * 2]
     sizes = per_layer * 80 + [v * d * 2] * 2
     assert bd.boost_modulus_from_budget(sizes, 120 * 10 ** 9, 10 ** 6) == 6
+
+
+@given(st.integers(1, 300 * opl.PAGE), st.integers(2, 200), st.integers(0, 10 ** 6),
+       st.integers(0, 2 ** 31))
+@settings(max_examples=300, deadline=None)
+def test_plan_contrast_matches_oracle(nbytes, M, phase, seed):
+    import synth
+    n = opl.n_pages(nbytes)
+    u = synth.uniforms(seed, n)
+    assert np.array_equal(bd.boost_plan_contrast(bd.PLACE_MPP, nbytes, M),
+                          opl.mpp_tier_map(nbytes, M))
+    assert np.array_equal(bd.boost_plan_contrast(bd.PLACE_MPP_GLOBAL, nbytes, M, phase),
+                          opl.mpp_global_map(n, M, phase))
+    assert np.array_equal(bd.boost_plan_contrast(bd.PLACE_LINEAR, nbytes, M),
+                          opl.linear_map(n, M))
+    assert np.array_equal(bd.boost_plan_contrast(bd.PLACE_RANDOM, nbytes, M, 0, u),
+                          opl.bapp_r_from_uniforms(u, M))
+
+
+def test_plan_contrast_random_boundary_draws():
+    """Draws exactly at k / M decide the same way on both sides."""
+    M = 12
+    u = np.array([0.0, 1 / M, np.nextafter(1 / M, 0), np.nextafter(1 / M, 1), 0.5,
+                  np.nextafter(1.0, 0)])
+    got = bd.boost_plan_contrast(bd.PLACE_RANDOM, u.size * opl.PAGE, M, 0, u)
+    assert np.array_equal(got, opl.bapp_r_from_uniforms(u, M))
+
+
+def test_plan_contrast_bad_arguments():
+    for args in ((9, opl.PAGE, 4), (bd.PLACE_MPP, 0, 4), (bd.PLACE_LINEAR, opl.PAGE, 1)):
+        with pytest.raises(bd.BoostError) as e:
+            bd.boost_plan_contrast(*args)
+        assert e.value.code == bd.EINVAL
+    with pytest.raises(bd.BoostError):
+        bd.boost_plan_contrast(bd.PLACE_RANDOM, opl.PAGE, 4)
+    with pytest.raises(ValueError):
+        bd.boost_plan_contrast(bd.PLACE_RANDOM, 3 * opl.PAGE, 4, 0, np.zeros(2))

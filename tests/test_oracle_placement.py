@@ -185,3 +185,64 @@ def test_budget_modulus_70b_chain():
     assert M == 6 and host == 11054
     assert (sum(pages) - host) * pl.PAGE <= 120 * 10 ** 9
     assert (sum(pages) - sum(n // 7 for n in pages)) * pl.PAGE > 120 * 10 ** 9
+
+
+# ------------------------------------------------------------ contrast maps
+def test_global_modulo_at_phase_zero_is_mpp():
+    """Special case: at phase 0 the pattern that runs across tensors is the
+    per-tensor modulo map (§3.1) of that tensor."""
+    for n in range(1, 70):
+        for M in (2, 3, 11, 16, 127):
+            assert np.array_equal(pl.mpp_global_map(n, M, 0),
+                                  pl.mpp_tier_map(n * pl.PAGE, M))
+
+
+def test_global_modulo_chain_is_one_big_tensor():
+    """Without the per-tensor restart, the maps of consecutive tensors placed
+    at cumulative phases are the modulo map of their concatenation."""
+    rng = np.random.default_rng(3)
+    for M in (5, 12, 127):
+        sizes = [int(s) for s in rng.integers(1, 300, size=20)]
+        phases = np.concatenate([[0], np.cumsum(sizes)[:-1]])
+        cat = np.concatenate([pl.mpp_global_map(n, M, p) for n, p in zip(sizes, phases)])
+        assert np.array_equal(cat, pl.mpp_tier_map(sum(sizes) * pl.PAGE, M))
+
+
+@pytest.mark.parametrize("M", [2, 7, 12, 127])
+def test_global_modulo_host_count_closed_form(M):
+    for phase in range(0, 3 * M):
+        for n in range(1, 3 * M):
+            got = int(pl.mpp_global_map(n, M, phase).sum())
+            assert got == (phase + n) // M - phase // M
+
+
+def test_global_modulo_breaks_per_kernel_share():
+    """§2.6: an interleave that ignores kernel boundaries can give a small
+    tensor a host page, a host share far above 1/M for that kernel; modulo
+    placement restarted per tensor (§3.1) never exceeds 1/M."""
+    M, n = 127, 16        # a 16-page tensor at the measured modulus
+    shares = [pl.mpp_global_map(n, M, p).mean() for p in range(M)]
+    assert max(shares) == 1 / 16 and sum(s > 0 for s in shares) == n
+    assert pl.mpp_tier_map(n * pl.PAGE, M).sum() == 0
+
+
+def test_bapp_r_from_uniforms_grid():
+    """Draws on the grid i / N put exactly ceil(N / M) pages on host: the
+    first ones, where i * M < N."""
+    for N in (10, 64, 127, 1000):
+        for M in (2, 3, 11, 127):
+            u = np.arange(N) / N
+            t = pl.bapp_r_from_uniforms(u, M)
+            assert t.sum() == -(-N // M)
+            assert t[:-(-N // M)].all()
+
+
+def test_bapp_r_from_uniforms_share():
+    """Random draws: the host share is binomial around 1/M (§2.6)."""
+    import synth
+    M, n = 12, 400
+    fr = np.array([pl.bapp_r_from_uniforms(synth.uniforms(s, n), M).mean()
+                   for s in range(1000)])
+    p = 1 / M
+    assert abs(fr.mean() - p) < 0.003
+    assert abs(fr.std() - math.sqrt(p * (1 - p) / n)) < 0.1 * math.sqrt(p * (1 - p) / n)
