@@ -636,10 +636,24 @@ __global__ __launch_bounds__(256) void split_reduce(GemvParams P) {
 #ifndef BOOST_GEMV_UN_BIG
 #define BOOST_GEMV_UN_BIG 1
 #endif
-template <int B>
+// Batch 1 with a row split over four wavefronts (rows longer than 12K
+// columns): each wavefront's x slice differs from its neighbours', so x misses
+// the L1 cache (counters: as many L2 requests for x as for the weights) and
+// would be fetched from L2 once per row; two rows per wavefront reuse one x
+// slice from registers (8B down projection 22.2 -> 21.2 us, 70B 44.0 ->
+// 42.1 us; with a row over two wavefronts it did not pay).
+#ifndef BOOST_GEMV_RW1_LONG
+#define BOOST_GEMV_RW1_LONG 2
+#endif
+#ifndef BOOST_GEMV_UN1_LONG
+#define BOOST_GEMV_UN1_LONG 4
+#endif
+template <int B, int KS>
 struct Shape {
-  static constexpr int RW = B == 1 ? 1 : (B == 2 ? 2 : (B <= 4 ? 4 : BOOST_GEMV_RW_BIG));
-  static constexpr int UN = B == 1 ? BOOST_GEMV_UN1 : (B <= 4 ? 2 : BOOST_GEMV_UN_BIG);
+  static constexpr int RW = B == 1 ? (KS > 2 ? BOOST_GEMV_RW1_LONG : 1)
+                                   : (B == 2 ? 2 : (B <= 4 ? 4 : BOOST_GEMV_RW_BIG));
+  static constexpr int UN = B == 1 ? (KS > 2 ? BOOST_GEMV_UN1_LONG : BOOST_GEMV_UN1)
+                                   : (B <= 4 ? 2 : BOOST_GEMV_UN_BIG);
 };
 
 // Wavefronts per row (split-K inside the workgroup) for a row of K columns:
@@ -693,7 +707,7 @@ int launch_fixup(GemvParams& P, int n_pages, bool need_fixup, hipStream_t s) {
 
 template <int B, int KS>
 int launch(GemvParams& P, int n_pages, bool need_fixup, const boost_ctx* ctx, hipStream_t s) {
-  constexpr int RW = Shape<B>::RW, UN = Shape<B>::UN;
+  constexpr int RW = Shape<B, KS>::RW, UN = Shape<B, KS>::UN;
   const int64_t grid = plan_grid(P, n_pages, RW * (kWaves / KS), ctx);
   if (grid < 0) return bst::fail(BOOST_EINVAL, "grid too large");
   hipLaunchKernelGGL((gemv_kernel<B, RW, UN, KS>), dim3(static_cast<unsigned>(grid)),
