@@ -121,6 +121,32 @@ def test_window_invariant_brute_force(M):
                 assert all(v == P // M for v in full)
 
 
+@pytest.mark.parametrize("M", range(2, 9))
+def test_mpp_minimises_window_discrepancy_brute_force(M):
+    """Optimality of the modulo rule (§3.1, Insight-1): among ALL tier maps
+    of n <= 16 pages with the same number of host pages, none has a smaller
+    largest window discrepancy max |host(window) - len(window) / M| than the
+    modulo map, and the modulo map's is below one page."""
+    for n in range(M, 17):
+        t = pl.mpp_tier_map(n * pl.PAGE, M).astype(np.int64)
+        h = int(t.sum())
+        assert h == n // M
+
+        def discrepancy(maps):  # maps [C, n] of 0/1 -> [C]
+            ps = np.concatenate([np.zeros((maps.shape[0], 1), np.int64),
+                                 np.cumsum(maps, axis=1)], axis=1)
+            i, j = np.triu_indices(n + 1, k=1)
+            cnt = ps[:, j] - ps[:, i]
+            return np.abs(cnt - (j - i) / M).max(axis=1)
+
+        d_mpp = discrepancy(t[None, :])[0]
+        assert d_mpp < 1.0
+        combos = np.array(list(itertools.combinations(range(n), h)), np.int64)
+        maps = np.zeros((len(combos), n), np.int64)
+        np.put_along_axis(maps, combos, 1, axis=1)
+        assert discrepancy(maps).min() >= d_mpp - 1e-12
+
+
 def test_random_placement_has_window_variance():
     """Contrast (§2.6): a random placement with the same share spreads far
     more than one page across windows, MPP never does."""
