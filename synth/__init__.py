@@ -130,6 +130,24 @@ def attention_inputs(batch: int, hq: int, hkv: int, head_dim: int,
     return lengths, q, ks, vs
 
 
+def attention_kv_torch(lengths, hkv: int, head_dim: int, kv_seed: int, device):
+    """K and V of every request, all requests' tokens concatenated in logical
+    order ([sum L_b, Hkv, D] bf16 each), drawn on a device with torch's seeded
+    generator (used where gigabytes are needed; a different stream from
+    ``attention_inputs``).  Request b's rows start at offsets[b]."""
+    import torch
+    lengths = np.asarray(lengths, dtype=np.int64)
+    total = int(lengths.sum())
+    g = torch.Generator(device=device)
+    g.manual_seed(kv_seed)
+    k = torch.randn((total, hkv, head_dim), generator=g, device=device,
+                    dtype=torch.float32).to(torch.bfloat16)
+    v = torch.randn((total, hkv, head_dim), generator=g, device=device,
+                    dtype=torch.float32).to(torch.bfloat16)
+    offsets = np.concatenate([[0], np.cumsum(lengths)[:-1]]).astype(np.int64)
+    return k, v, offsets
+
+
 def churn_trace(seed: int, n_events: int, batch: int, lo: int, hi: int):
     """Replace events for KV-pool warm-up: (victim slot, new length) pairs."""
     rng = np.random.default_rng(seed)

@@ -169,3 +169,58 @@ def test_config3_full_size_sampled(gpu_ctx):
     exp = np.array([ref[p] for p in pairs])
     assert og.rel_err(got, exp) <= TOL
     assert np.max(np.abs(got - exp)) < 1e-4
+
+
+def test_batch256_long_contexts_full_size_sampled(gpu_ctx):
+    """The largest configuration: batch 256, 32/8 heads, contexts U[1024,
+    8192] (up to 512 blocks, several partitions per request), K/V drawn on
+    the device (seeded torch generator) and written through the allocator's
+    blocks; an LPP pool at modulus 126 and an all-HBM pool agree bitwise, and
+    sampled (request, head) pairs meet the bar against the oracle (their K/V
+    copied back from the generator's output, not from the pool)."""
+    import torch
+    B, Hq, H, D = 256, 32, 8, 128
+    lengths = synth.context_lengths(3, B, 1024, 8192)
+    rng = np.random.default_rng(4)
+    q = synth.normal_bf16(rng, (B, Hq, D), 1.0)
+    k, v, offs = synth.attention_kv_torch(lengths, H, D, kv_seed=5, device="cuda")
+    need = [(int(L) + 15) // 16 for L in lengths]
+    mb = max(need)
+    outs = []
+    for mode, M in ((bd.KV_LPP, 126), (bd.KV_ALL_HBM, 0)):
+        pool = new_pool(gpu_ctx, H, Hq, sum(need), M, mode, max_batch=B, max_blocks=mb)
+        try:
+            tables = np.full((B, mb), -1, dtype=np.int32)
+            for b in range(B):
+                got = bd.boost_kv_alloc(pool, b, need[b])
+                assert got != bd.EAGAIN
+                tables[b, :need[b]] = got
+            if mode == bd.KV_LPP:
+                assert bd.boost_kv_stats(pool)["shh_requests"] > 0
+            slots = np.concatenate([tables[b, np.arange(L) // 16] * 16 + np.arange(L) % 16
+                                    for b, L in enumerate(lengths)]).astype(np.int32)
+            s = torch.from_numpy(slots).cuda()
+            bd.boost_kv_write(gpu_ctx, pool, 0, s, k.view(torch.int16), v.view(torch.int16),
+                              int(s.numel()), stream())
+            sync()
+            outs.append(run_attn(gpu_ctx, pool, 0, q, tables, lengths))
+        finally:
+            bd.boost_kv_pool_destroy(pool)
+    assert np.array_equal(outs[0].view(np.uint32), outs[1].view(np.uint32))
+    # sampled pairs: the longest request, the last one and seeded draws
+    bl = int(np.argmax(lengths))
+    reqs = sorted({bl, B - 1, *[int(x) for x in rng.integers(0, B, 6)]})
+    pairs = [(b, int(h)) for b in reqs for h in rng.integers(0, Hq, 4)] + [(bl, Hq - 1)]
+    ks, vs = {}, {}
+    for b in reqs:
+        a, L = int(offs[b]), int(lengths[b])
+        ks[b] = k[a:a + L].view(torch.int16).cpu().numpy().view(np.uint16)
+        vs[b] = v[a:a + L].view(torch.int16).cpu().numpy().view(np.uint16)
+    got, exp = [], []
+    for b, h in pairs:
+        r = oa.decode_attention(q[b:b + 1], [ks[b]], [vs[b]], heads=[(0, h)])
+        exp.append(r[(0, h)])
+        got.append(outs[0][b, h])
+    got, exp = np.array(got), np.array(exp)
+    assert og.rel_err(got, exp) <= TOL
+    assert np.max(np.abs(got - exp)) < 1e-4
