@@ -36,17 +36,19 @@ constexpr int kLanesTok = kD / 8;  // lanes per token row (16)
 #define BOOST_ATTN_UNROLL 4
 #endif
 #ifndef BOOST_ATTN_ITEMS
-#define BOOST_ATTN_ITEMS 2048
+#define BOOST_ATTN_ITEMS 4096
 #endif
 #ifndef BOOST_ATTN_UNROLL8
 #define BOOST_ATTN_UNROLL8 BOOST_ATTN_UNROLL
 #endif
-// Partitions of at least this many blocks (the longest contexts at large
-// batch) are dispatched partition-major: batch 256 at contexts U[1024, 8192]
-// 970 -> 870 us; at 129-block partitions (batch 64, same contexts) and 64
-// (config 3) it changed the time by -2..+4 %, so they keep request order
+// Partitions of at least this many blocks are dispatched partition-major.
+// Measured with 4096 items: batch 256 at contexts U[1024, 8192] (256-block
+// partitions) 970 -> 870 us; batch 64 at the same contexts (65) 257-270 ->
+// 250-252 us; batch 64 at U[512, 4096] (32) -2 %; batch 8 at 2048 tokens
+// (16-block partitions) is 3 % faster in request order, which it keeps.
+// (With request order throughout, 4096 items were slower than 2048.)
 #ifndef BOOST_ATTN_PART_MAJOR_MIN
-#define BOOST_ATTN_PART_MAJOR_MIN 256
+#define BOOST_ATTN_PART_MAJOR_MIN 32
 #endif
 constexpr int kMaxPartBlocks = 256;         // blocks per partition, at most
 // A work item of fewer than 16 blocks spends as long on its start (q loads)
