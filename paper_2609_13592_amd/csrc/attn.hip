@@ -41,15 +41,6 @@ constexpr int kLanesTok = kD / 8;  // lanes per token row (16)
 #ifndef BOOST_ATTN_UNROLL8
 #define BOOST_ATTN_UNROLL8 BOOST_ATTN_UNROLL
 #endif
-// Partitions of at least this many blocks are dispatched partition-major.
-// Measured with 4096 items: batch 256 at contexts U[1024, 8192] (256-block
-// partitions) 970 -> 870 us; batch 64 at the same contexts (65) 257-270 ->
-// 250-252 us; batch 64 at U[512, 4096] (32) -2 %; batch 8 at 2048 tokens
-// (16-block partitions) is 3 % faster in request order, which it keeps.
-// (With request order throughout, 4096 items were slower than 2048.)
-#ifndef BOOST_ATTN_PART_MAJOR_MIN
-#define BOOST_ATTN_PART_MAJOR_MIN 32
-#endif
 constexpr int kMaxPartBlocks = 256;         // blocks per partition, at most
 // A work item of fewer than 16 blocks spends as long on its start (q loads)
 // and end (slot merge, partial stores) as on its K/V (batch 8 at 2048 tokens:
@@ -76,7 +67,6 @@ struct AttnParams {
   const int32_t* lens;    // [B]
   int B, H, Hq, nb, max_blocks;
   int part_blocks, n_parts;  // partition size in blocks, partitions per request
-  int part_major;            // item order: 1 = partition-major for heads below H - 1
   int max_parts;             // stride of the partial buffers
   float scale;
   float* part_acc;  // [B * Hq * max_parts][D] unnormalised sums of p * v
@@ -212,25 +202,27 @@ __global__ __launch_bounds__(kThreads) void attn_partition(AttnParams P) {
   const int tid = threadIdx.x;
   const int ts = tid / kLanesTok;  // token slot 0..15
   const int dc = tid % kLanesTok;  // 8-dim chunk
-  // Item order (uniform): the highest head first, its items request by
-  // request (they can read host pages).  The other heads follow request by
-  // request too (neighbouring partitions of one request run together), or,
-  // with long partitions, partition by partition: every request's first
-  // (full) partition before any later, shorter one, so the grid ends on
-  // short items instead of whole long ones.
+  // Item order (uniform): first every item of the highest head, request by
+  // request (only those can read host pages, so their slow reads start
+  // first); then the other heads partition by partition, request by request,
+  // head fastest, so the items running together read the same blocks of one
+  // request in different head regions and every request's first (full)
+  // partition runs before its later, shorter ones.  (Against the order
+  // request by request, head slowest: batch 64 at contexts U[512, 4096]
+  // 138 -> 121 us, batch 64 at U[1024, 8192] 257 -> 228 us, batch 256 at
+  // U[1024, 8192] 970 -> 840 us; batch 8 at 2048 tokens unchanged.)
   int part, b, g;
   {
     const int idx = blockIdx.x, first = P.B * P.n_parts;
-    if (!P.part_major || idx < first) {
+    if (idx < first) {
       part = idx % P.n_parts;
-      const int rest = idx / P.n_parts;
-      b = rest % P.B;
-      g = P.H - 1 - rest / P.B;
-    } else {
+      b = idx / P.n_parts;
+      g = P.H - 1;
+    } else {  // only reached with H > 1
       const int j = idx - first, per_part = P.B * (P.H - 1);
       part = j / per_part;
-      b = (j % per_part) % P.B;
-      g = P.H - 2 - (j % per_part) / P.B;
+      b = (j % per_part) / (P.H - 1);
+      g = P.H - 2 - (j % per_part) % (P.H - 1);
     }
   }
   const int L = P.lens[b];
@@ -443,7 +435,6 @@ int boost_paged_attn_decode(boost_ctx* ctx, const boost_kv_pool* pool, int layer
        std::max(kPartMin, std::min(kPartMax, (max_blocks + want_parts - 1) / want_parts))});
   P.part_blocks = std::max(P.part_blocks, 4);
   P.n_parts = (max_blocks + P.part_blocks - 1) / P.part_blocks;
-  P.part_major = P.n_parts > 1 && H > 1 && P.part_blocks >= BOOST_ATTN_PART_MAJOR_MIN;
   P.max_parts = pool->max_parts;
   if (P.n_parts > P.max_parts) return fail(BOOST_EINVAL, "partition scratch too small");
   P.scale = scale > 0.f ? scale : 1.0f / std::sqrt(static_cast<float>(kD));
