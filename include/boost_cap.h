@@ -380,6 +380,13 @@ int boost_embed_gather(boost_ctx *ctx, const boost_tensor *E, int V, int d,
 int boost_rmsnorm(boost_ctx *ctx, const float *x, const void *w, int B, int d,
                   float eps, void *out, void *stream);
 
+/* x[b, i] += r[b, i] (fp32, in place), then out = the RMSNorm of the new x
+ * exactly as boost_rmsnorm computes it: the same bits as boost_residual_add
+ * followed by boost_rmsnorm, in one launch (the step's residual add and the
+ * next norm).  r fp32 [B, d], 16-byte aligned (EINVAL otherwise). */
+int boost_add_rmsnorm(boost_ctx *ctx, float *x, const float *r, const void *w, int B,
+                      int d, float eps, void *out, void *stream);
+
 /* Split the fused qkv output fp32 [B, (Hq + 2H) D] (query heads, then key
  * heads, then value heads) into bf16 q [B, Hq, D], k [B, H, D], v [B, H, D],
  * rotating query and key heads by RoPE at positions[b]: element i pairs with

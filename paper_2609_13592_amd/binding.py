@@ -83,6 +83,7 @@ _SIGS = {
     "boost_gemv_set_schedule": (_i32, [_vp, _i32, _i32]),
     "boost_embed_gather": (_i32, [_vp, _vp, _i32, _i32, _vp, _i32, _vp, _vp]),
     "boost_rmsnorm": (_i32, [_vp, _vp, _vp, _i32, _i32, C.c_float, _vp, _vp]),
+    "boost_add_rmsnorm": (_i32, [_vp, _vp, _vp, _vp, _i32, _i32, C.c_float, _vp, _vp]),
     "boost_rope_qkv": (_i32, [_vp, _vp, _vp, _i32, _i32, _i32, _i32, _dbl, _vp, _vp,
                               _vp, _vp]),
     "boost_kv_append": (_i32, [_vp, _vp, _i32, _vp, _i32, _vp, _vp, _vp, _i32, _vp]),
@@ -396,6 +397,11 @@ def boost_embed_gather(ctx: int, E: int, V: int, d: int, tokens, B: int, out, st
 def boost_rmsnorm(ctx: int, x, w, B: int, d: int, eps: float, out, stream=None):
     _check(load().boost_rmsnorm(ctx, _ptr(x), _ptr(w), B, d, eps, _ptr(out),
                                 _stream(stream)))
+
+
+def boost_add_rmsnorm(ctx: int, x, r, w, B: int, d: int, eps: float, out, stream=None):
+    _check(load().boost_add_rmsnorm(ctx, _ptr(x), _ptr(r), _ptr(w), B, d, eps, _ptr(out),
+                                    _stream(stream)))
 
 
 def boost_rope_qkv(ctx: int, qkv, positions, B: int, Hq: int, H: int, D: int,

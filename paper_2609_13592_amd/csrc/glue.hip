@@ -45,14 +45,25 @@ __global__ __launch_bounds__(256) void embed_gather_kernel(const char* const* __
 }
 
 // One workgroup per row: sum of squares in a fixed order, then
-// y = bf16(x * (1 / sqrt(mean + eps)) * w).
-__global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ x,
+// y = bf16(x * (1 / sqrt(mean + eps)) * w).  With ADD the row first takes
+// the residual r (x += r in fp32, stored back), the same additions the
+// separate residual add makes, so the fused call gives the same bits.
+template <bool ADD>
+__global__ __launch_bounds__(256) void rmsnorm_kernel(float* __restrict__ x,
+                                                      const float* __restrict__ r,
                                                       const uint16_t* __restrict__ w, int d,
                                                       float eps, uint16_t* __restrict__ y) {
   __shared__ float part[4];
-  const float* row = x + static_cast<int64_t>(blockIdx.x) * d;
+  float* row = x + static_cast<int64_t>(blockIdx.x) * d;
   float s = 0.f;
-  for (int i = threadIdx.x; i < d; i += 256) s = fmaf(row[i], row[i], s);
+  for (int i = threadIdx.x; i < d; i += 256) {
+    float v = row[i];
+    if constexpr (ADD) {
+      v += r[static_cast<int64_t>(blockIdx.x) * d + i];
+      row[i] = v;  // read back below by this same lane
+    }
+    s = fmaf(v, v, s);
+  }
 #pragma unroll
   for (int m = 32; m >= 1; m >>= 1) s += __shfl_xor(s, m, 64);
   if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = s;
@@ -69,18 +80,36 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ 
 // them in registers for the second pass (the plain loop above is a chain of
 // dependent round trips: 20 us for a batch of 8 rows of 8192).
 constexpr int kNormVec = 8;
-__global__ __launch_bounds__(256) void rmsnorm_vec_kernel(const float* __restrict__ x,
+template <bool ADD>
+__global__ __launch_bounds__(256) void rmsnorm_vec_kernel(float* __restrict__ x,
+                                                          const float* __restrict__ r,
                                                           const uint16_t* __restrict__ w,
                                                           int d, float eps,
                                                           uint16_t* __restrict__ y) {
   __shared__ float part[4];
   const int n4 = d / 4;
-  const float4* row = reinterpret_cast<const float4*>(x + static_cast<int64_t>(blockIdx.x) * d);
+  float4* row = reinterpret_cast<float4*>(x + static_cast<int64_t>(blockIdx.x) * d);
   float4 v[kNormVec];
 #pragma unroll
   for (int u = 0; u < kNormVec; ++u) {
     const int i = threadIdx.x + u * 256;
     v[u] = i < n4 ? row[i] : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+  if constexpr (ADD) {
+    const float4* res =
+        reinterpret_cast<const float4*>(r + static_cast<int64_t>(blockIdx.x) * d);
+#pragma unroll
+    for (int u = 0; u < kNormVec; ++u) {
+      const int i = threadIdx.x + u * 256;
+      if (i < n4) {
+        const float4 a = res[i];
+        v[u].x += a.x;
+        v[u].y += a.y;
+        v[u].z += a.z;
+        v[u].w += a.w;
+        row[i] = v[u];
+      }
+    }
   }
   float s = 0.f;
 #pragma unroll
@@ -269,24 +298,50 @@ int boost_embed_gather(boost_ctx* ctx, const boost_tensor* E, int V, int d,
   return BOOST_OK;
 }
 
-int boost_rmsnorm(boost_ctx* ctx, const float* x, const void* w, int B, int d, float eps,
-                  void* out, void* stream) {
+}  // extern "C"
+
+namespace {
+// x (+= r when r is given), then the norm; the row layout decides the
+// kernel, never r, so the fused and the separate calls take the same one
+int launch_rmsnorm(boost_ctx* ctx, float* x, const float* r, const void* w, int B, int d,
+                   float eps, void* out, void* stream) {
   if (!ctx || !x || !w || !out) return fail(BOOST_EINVAL, "null argument");
   if (ctx->device < 0) return fail(BOOST_ENODEV, "plan-only context");
   if (B < 1 || d < 1 || !(eps >= 0.f)) return fail(BOOST_EINVAL, "B=%d d=%d eps=%g", B, d, eps);
   const bool vec = d % 4 == 0 && d <= 4 * 256 * kNormVec &&
                    (reinterpret_cast<uintptr_t>(x) & 15) == 0 &&
+                   (reinterpret_cast<uintptr_t>(r) & 15) == 0 &&
                    (reinterpret_cast<uintptr_t>(w) & 7) == 0 &&
                    (reinterpret_cast<uintptr_t>(out) & 7) == 0;
-  if (vec)
-    hipLaunchKernelGGL(rmsnorm_vec_kernel, dim3(B), dim3(256), 0,
-                       static_cast<hipStream_t>(stream), x, static_cast<const uint16_t*>(w), d,
-                       eps, static_cast<uint16_t*>(out));
+  auto s = static_cast<hipStream_t>(stream);
+  auto wp = static_cast<const uint16_t*>(w);
+  auto op = static_cast<uint16_t*>(out);
+  if (vec && r)
+    hipLaunchKernelGGL(rmsnorm_vec_kernel<true>, dim3(B), dim3(256), 0, s, x, r, wp, d, eps, op);
+  else if (vec)
+    hipLaunchKernelGGL(rmsnorm_vec_kernel<false>, dim3(B), dim3(256), 0, s, x, r, wp, d, eps, op);
+  else if (r)
+    hipLaunchKernelGGL(rmsnorm_kernel<true>, dim3(B), dim3(256), 0, s, x, r, wp, d, eps, op);
   else
-    hipLaunchKernelGGL(rmsnorm_kernel, dim3(B), dim3(256), 0, static_cast<hipStream_t>(stream),
-                       x, static_cast<const uint16_t*>(w), d, eps, static_cast<uint16_t*>(out));
+    hipLaunchKernelGGL(rmsnorm_kernel<false>, dim3(B), dim3(256), 0, s, x, r, wp, d, eps, op);
   BOOST_HIP(hipGetLastError());
   return BOOST_OK;
+}
+}  // namespace
+
+extern "C" {
+
+int boost_rmsnorm(boost_ctx* ctx, const float* x, const void* w, int B, int d, float eps,
+                  void* out, void* stream) {
+  // the kernel without the residual never writes x
+  return launch_rmsnorm(ctx, const_cast<float*>(x), nullptr, w, B, d, eps, out, stream);
+}
+
+int boost_add_rmsnorm(boost_ctx* ctx, float* x, const float* r, const void* w, int B, int d,
+                      float eps, void* out, void* stream) {
+  if (!r) return fail(BOOST_EINVAL, "null argument");
+  if (reinterpret_cast<uintptr_t>(r) & 15) return fail(BOOST_EINVAL, "r must be 16-byte aligned");
+  return launch_rmsnorm(ctx, x, r, w, B, d, eps, out, stream);
 }
 
 int boost_rope_qkv(boost_ctx* ctx, const float* qkv, const int32_t* positions, int B, int Hq,

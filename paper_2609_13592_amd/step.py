@@ -8,6 +8,10 @@ This module only sequences C-ABI calls and owns the activation buffers
   paged_attn_decode -> gemv(o) -> residual_add -> rmsnorm -> gemv(gate_up) ->
   silu_mul -> gemv(down) -> residual_add] -> rmsnorm -> gemv(lm_head) -> argmax
 
+where every "residual_add -> rmsnorm" pair is one add_rmsnorm launch (the
+down projection's residual is added by the next layer's first norm, or by
+the final norm).
+
 Weights are [out, in] bf16 matrices placed page by page (each tensor on its
 own, so modulo placement restarts per tensor); norm weights are small bf16
 vectors kept in plain device memory.
@@ -78,10 +82,16 @@ class DecodeModel:
         F32, BF16 = bd.DTYPE_F32, bd.DTYPE_BF16
         bd.boost_embed_gather(c, self.mat["embed"], D.vocab, D.d, tokens, B, self.x, s)
         qkv_n = (D.hq + 2 * D.hkv) * D.hd
+        # a residual add waits in tmp until the next norm takes it (one launch)
+        pending = False
         for l in range(D.layers):
             if hooks is not None:
                 hooks.before_layer(l)
-            bd.boost_rmsnorm(c, self.x, self.norms[f"norm1.{l}"], B, D.d, EPS, self.h, s)
+            if pending:
+                bd.boost_add_rmsnorm(c, self.x, self.tmp, self.norms[f"norm1.{l}"], B, D.d,
+                                     EPS, self.h, s)
+            else:
+                bd.boost_rmsnorm(c, self.x, self.norms[f"norm1.{l}"], B, D.d, EPS, self.h, s)
             bd.boost_decode_gemv(c, self.mat[f"qkv.{l}"], qkv_n, D.d, self.h, B, self.qkv, F32, s)
             bd.boost_rope_qkv(c, self.qkv, positions, B, D.hq, D.hkv, D.hd, THETA,
                               self.q, self.k, self.v, s)
@@ -90,8 +100,8 @@ class DecodeModel:
                                        lens, 0.0, self.o, BF16, s)
             bd.boost_decode_gemv(c, self.mat[f"o.{l}"], D.d, D.hq * D.hd, self.o, B,
                                  self.tmp, F32, s)
-            bd.boost_residual_add(c, self.x, self.tmp, B * D.d, s)
-            bd.boost_rmsnorm(c, self.x, self.norms[f"norm2.{l}"], B, D.d, EPS, self.h, s)
+            bd.boost_add_rmsnorm(c, self.x, self.tmp, self.norms[f"norm2.{l}"], B, D.d, EPS,
+                                 self.h, s)
             bd.boost_decode_gemv(c, self.mat[f"gate_up.{l}"], 2 * D.ffn, D.d, self.h, B,
                                  self.gu, F32, s)
             bd.boost_silu_mul(c, self.gu, B, D.ffn, self.act, s)
@@ -99,10 +109,14 @@ class DecodeModel:
                                  self.tmp, F32, s)
             if hooks is not None:
                 hooks.after_layer(l)
-            bd.boost_residual_add(c, self.x, self.tmp, B * D.d, s)
+            pending = True
         if hooks is not None:
             hooks.before_head()
-        bd.boost_rmsnorm(c, self.x, self.norms["norm_f"], B, D.d, EPS, self.h, s)
+        if pending:
+            bd.boost_add_rmsnorm(c, self.x, self.tmp, self.norms["norm_f"], B, D.d, EPS,
+                                 self.h, s)
+        else:
+            bd.boost_rmsnorm(c, self.x, self.norms["norm_f"], B, D.d, EPS, self.h, s)
         bd.boost_decode_gemv(c, self.mat["lm_head"], D.vocab, D.d, self.h, B, self.logits,
                              F32, s)
         bd.boost_argmax(c, self.logits, B, D.vocab, self.ids, s)

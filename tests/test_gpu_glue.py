@@ -142,3 +142,30 @@ def test_residual_and_argmax(gpu_ctx):
     sync()
     assert ids.cpu().numpy().tolist() == ods.argmax_lowest(s.astype(np.float64)).tolist()
     assert ids.cpu().numpy()[:3].tolist() == [5, 0, VOCAB - 1]
+
+
+@pytest.mark.parametrize("d", [8192, 4096, 12288, 1026])
+def test_add_rmsnorm_equals_add_then_norm(gpu_ctx, d):
+    """The fused residual add + RMSNorm leaves the same x and writes the same
+    bits as the residual add followed by the norm (vector path and plain
+    loop), and x + r meets the oracle's norm."""
+    import torch
+    rng = np.random.default_rng(100 + d)
+    x = (rng.standard_normal((5, d)) * 2).astype(np.float32)
+    r = (rng.standard_normal((5, d)) * 2).astype(np.float32)
+    w = synth.round_bf16((1 + 0.1 * rng.standard_normal(d)).astype(np.float32))
+    wd = to_dev_u16(w)
+    x1, x2 = dev(x), dev(x)
+    o1 = torch.empty((5, d), dtype=torch.int16, device="cuda")
+    o2 = torch.empty((5, d), dtype=torch.int16, device="cuda")
+    bd.boost_residual_add(gpu_ctx, x1, dev(r), 5 * d, stream())
+    bd.boost_rmsnorm(gpu_ctx, x1, wd, 5, d, 1e-5, o1, stream())
+    bd.boost_add_rmsnorm(gpu_ctx, x2, dev(r), wd, 5, d, 1e-5, o2, stream())
+    sync()
+    assert np.array_equal(x2.cpu().numpy(), x + r)
+    assert np.array_equal(x1.cpu().numpy(), x2.cpu().numpy())
+    assert np.array_equal(host_u16(o1), host_u16(o2))
+    assert_bf16_close(host_u16(o2), ods.to_bf16(ods.rmsnorm((x + r).astype(np.float64), w)))
+    with pytest.raises(bd.BoostError) as e:
+        bd.boost_add_rmsnorm(gpu_ctx, x2, None, wd, 5, d, 1e-5, o2, stream())
+    assert e.value.code == bd.EINVAL
