@@ -903,6 +903,9 @@ inline int k_splits(int K) {
   return ks < BOOST_GEMV_KS_MAX ? ks : BOOST_GEMV_KS_MAX;
 }
 
+#ifndef BOOST_HOST_UNITS_PER_WORKER
+#define BOOST_HOST_UNITS_PER_WORKER 16
+#endif
 // Units per page and grid size for units of rows_wg rows; fills in
 // P.units_per_page, P.host_workers and P.address_order.  Returns -1 if the
 // grid is too large.
@@ -923,8 +926,14 @@ int64_t plan_grid(GemvParams& P, int n_pages, int rows_wg, const boost_ctx* ctx)
     grid = static_cast<int64_t>(n_pages) * P.units_per_page;
   } else {
     const int64_t host_units = static_cast<int64_t>(P.n_host_pages) * P.units_per_page;
+    // default: one host worker per BOOST_HOST_UNITS_PER_WORKER host units,
+    // between n_cu / 16 and n_cu / 8 (a tensor with many host pages keeps
+    // more requests on the link in flight; with few, extra workers only slow
+    // the HBM units beside them)
+    const int64_t h_lo = std::max(1, ctx->n_cu / 16), h_hi = std::max(1, ctx->n_cu / 8);
+    const int64_t h_want = (host_units + BOOST_HOST_UNITS_PER_WORKER - 1) / BOOST_HOST_UNITS_PER_WORKER;
     int h = ctx->gemv_host_workers > 0 ? ctx->gemv_host_workers
-                                       : std::max(1, ctx->n_cu / 16);
+                                       : static_cast<int>(std::min(h_hi, std::max(h_lo, h_want)));
     P.host_workers = static_cast<int>(std::min<int64_t>(h, host_units));
     grid = P.host_workers + static_cast<int64_t>(P.n_hbm_pages) * P.units_per_page;
   }
