@@ -346,17 +346,42 @@ __global__ __launch_bounds__(64) void attn_merge(AttnParams P) {
   const int n_blk = min((L + kT - 1) / kT, P.max_blocks);
   const int np = L <= 0 ? 0 : (n_blk + P.part_blocks - 1) / P.part_blocks;
   const int64_t base = static_cast<int64_t>(bh) * P.max_parts;
+  // the largest partition maximum: one partition per lane, then across the
+  // wavefront (a maximum is exact in any order)
   float M = -INFINITY;
-  for (int p = 0; p < np; ++p) M = fmaxf(M, P.part_ml[(base + p) * 2]);
+  for (int p0 = 0; p0 < np; p0 += 64) {
+    const int p = p0 + lane;
+    M = fmaxf(M, p < np ? P.part_ml[(base + p) * 2] : -INFINITY);
+  }
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) M = fmaxf(M, __shfl_xor(M, m, 64));
+  // weighted sums in partition order; the loads of eight partitions go out
+  // together instead of one round trip per partition
+  constexpr int kMergeBatch = 8;
   float den = 0.f, o0 = 0.f, o1 = 0.f;
-  for (int p = 0; p < np; ++p) {
-    const float mp = P.part_ml[(base + p) * 2];
-    if (mp == -INFINITY) continue;
-    const float w = __builtin_amdgcn_exp2f(mp - M);  // maxima are in the log2 domain
-    den = fmaf(P.part_ml[(base + p) * 2 + 1], w, den);
-    const float2 a = *reinterpret_cast<const float2*>(P.part_acc + (base + p) * kD + lane * 2);
-    o0 = fmaf(a.x, w, o0);
-    o1 = fmaf(a.y, w, o1);
+  for (int p0 = 0; p0 < np; p0 += kMergeBatch) {
+    float mp[kMergeBatch], lp[kMergeBatch];
+    float2 a[kMergeBatch];
+#pragma unroll
+    for (int u = 0; u < kMergeBatch; ++u) {
+      const int p = p0 + u;  // uniform
+      mp[u] = -INFINITY;
+      lp[u] = 0.f;
+      a[u] = make_float2(0.f, 0.f);
+      if (p < np) {
+        mp[u] = P.part_ml[(base + p) * 2];
+        lp[u] = P.part_ml[(base + p) * 2 + 1];
+        a[u] = *reinterpret_cast<const float2*>(P.part_acc + (base + p) * kD + lane * 2);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kMergeBatch; ++u) {
+      if (mp[u] == -INFINITY) continue;  // past np, or an empty partition
+      const float w = __builtin_amdgcn_exp2f(mp[u] - M);  // maxima are in the log2 domain
+      den = fmaf(lp[u], w, den);
+      o0 = fmaf(a[u].x, w, o0);
+      o1 = fmaf(a[u].y, w, o1);
+    }
   }
   const float inv = den > 0.f ? 1.f / den : 0.f;
   const int64_t oi = static_cast<int64_t>(bh) * kD + lane * 2;
