@@ -846,14 +846,32 @@ __global__ __launch_bounds__(256) void split_reduce(GemvParams P) {
   const int64_t r = t % P.N;
   const int64_t e0 = r * P.K;
   const int64_t p0 = e0 / kPageElems, p1 = (e0 + P.K - 1) / kPageElems;
+  // all S loads go out together (a loop over a run-time S would wait for
+  // each in turn), then the sums in slice order
   float v = 0.f;
   if (p0 == p1) {
-    for (int s = 0; s < P.S; ++s) v += P.ws[(static_cast<int64_t>(s) * P.B + b) * P.N + r];
+    float part[kMaxSlices];
+#pragma unroll
+    for (int s = 0; s < kMaxSlices; ++s)
+      part[s] = s < P.S ? P.ws[(static_cast<int64_t>(s) * P.B + b) * P.N + r] : 0.f;
+#pragma unroll
+    for (int s = 0; s < kMaxSlices; ++s)
+      if (s < P.S) v += part[s];
   } else {
     const float* cut = P.ws + static_cast<int64_t>(P.S) * P.B * P.N;
+    float part0[kMaxSlices], part1[kMaxSlices];
+#pragma unroll
+    for (int s = 0; s < kMaxSlices; ++s) {
+      part0[s] = s < P.S ? cut[((p1 * 2 + 0) * P.S + s) * P.B + b] : 0.f;
+      part1[s] = s < P.S ? cut[((p1 * 2 + 1) * P.S + s) * P.B + b] : 0.f;
+    }
     float v1 = 0.f;
-    for (int s = 0; s < P.S; ++s) v += cut[((p1 * 2 + 0) * P.S + s) * P.B + b];
-    for (int s = 0; s < P.S; ++s) v1 += cut[((p1 * 2 + 1) * P.S + s) * P.B + b];
+#pragma unroll
+    for (int s = 0; s < kMaxSlices; ++s)
+      if (s < P.S) {
+        v += part0[s];
+        v1 += part1[s];
+      }
     v += v1;
   }
   store_y(P, b, r, v);
@@ -1031,7 +1049,7 @@ int launch_gemm_shape(GemvParams& P, int n_pages, bool need_fixup, const boost_c
          (units * S < ctx->n_cu * 3 / 4 || P.K / S > 16384))
     S *= 2;
 #ifdef BOOST_GEMM_TUNING
-  if (const char* e = getenv("BOOST_GEMM_S")) S = atoi(e);
+  if (const char* e = getenv("BOOST_GEMM_S")) S = std::max(1, std::min(atoi(e), kMaxSlices));
 #endif
   while (S > 1 && static_cast<uint64_t>(S) * P.B * (P.N + 2ull * (n_pages + 1)) >
                       ctx->gemm_ws_floats)
