@@ -406,6 +406,15 @@ int boost_kv_append(boost_ctx *ctx, const boost_kv_pool *pool, int layer,
                     const int32_t *positions, const void *k, const void *v,
                     int B, void *stream);
 
+/* boost_rope_qkv followed by boost_kv_append in one launch: the query heads
+ * go to q (bf16 [B, Hq, D]) and the rotated key and converted value heads
+ * straight into the token's slot of the pool (H and D are the pool's), with
+ * the same bits and the same skipping rules as the two calls. */
+int boost_rope_kv_append(boost_ctx *ctx, const boost_kv_pool *pool, int layer,
+                         const float *qkv, const int32_t *positions, int B, int Hq,
+                         double theta, const int32_t *block_tables, int max_blocks,
+                         void *q, void *stream);
+
 /* out[b, j] = bf16(silu(gu[b, j]) * gu[b, F + j]) for the fused gate_up
  * output fp32 [B, 2F] (gate rows first). */
 int boost_silu_mul(boost_ctx *ctx, const float *gu, int B, int F, void *out,

@@ -87,6 +87,8 @@ _SIGS = {
     "boost_rope_qkv": (_i32, [_vp, _vp, _vp, _i32, _i32, _i32, _i32, _dbl, _vp, _vp,
                               _vp, _vp]),
     "boost_kv_append": (_i32, [_vp, _vp, _i32, _vp, _i32, _vp, _vp, _vp, _i32, _vp]),
+    "boost_rope_kv_append": (_i32, [_vp, _vp, _i32, _vp, _vp, _i32, _i32, _dbl, _vp, _i32,
+                                    _vp, _vp]),
     "boost_silu_mul": (_i32, [_vp, _vp, _i32, _i32, _vp, _vp]),
     "boost_residual_add": (_i32, [_vp, _vp, _vp, C.c_int64, _vp]),
     "boost_argmax": (_i32, [_vp, _vp, _i32, _i32, _vp, _vp]),
@@ -414,6 +416,13 @@ def boost_kv_append(ctx: int, pool: int, layer: int, block_tables, max_blocks: i
                     positions, k, v, B: int, stream=None):
     _check(load().boost_kv_append(ctx, pool, layer, _ptr(block_tables), max_blocks,
                                   _ptr(positions), _ptr(k), _ptr(v), B, _stream(stream)))
+
+
+def boost_rope_kv_append(ctx: int, pool: int, layer: int, qkv, positions, B: int, Hq: int,
+                         theta: float, block_tables, max_blocks: int, q, stream=None):
+    _check(load().boost_rope_kv_append(ctx, pool, layer, _ptr(qkv), _ptr(positions), B, Hq,
+                                       theta, _ptr(block_tables), max_blocks, _ptr(q),
+                                       _stream(stream)))
 
 
 def boost_silu_mul(ctx: int, gu, B: int, F: int, out, stream=None):

@@ -141,26 +141,52 @@ __global__ __launch_bounds__(256) void rmsnorm_vec_kernel(float* __restrict__ x,
   }
 }
 
+// Where the key and value heads of the new token go when they are written
+// straight into the pool (the fused RoPE + KV append): the layer's K and V
+// page tables, the block tables and the pool geometry.
+struct PoolSlot {
+  const char* const* pt_k;
+  const char* const* pt_v;
+  const int32_t* tables;
+  int max_blocks, T, nb;
+};
+
 // One workgroup per (request, head of the fused qkv output), one lane per
 // rotation pair.  Query and key heads are rotated (half-split pairs, angle in
-// double precision); value heads are converted.
+// double precision); value heads are converted.  With POOL the key and value
+// heads go to the token's slot of the pool (the same bits the KV append
+// copies there), skipped like the append skips a position or block outside
+// the table or the pool.
+template <bool POOL>
 __global__ __launch_bounds__(64) void rope_qkv_kernel(const float* __restrict__ qkv,
                                                       const int32_t* __restrict__ pos,
                                                       int Hq, int H, int D, double log2_theta,
                                                       uint16_t* __restrict__ q,
                                                       uint16_t* __restrict__ k,
-                                                      uint16_t* __restrict__ v) {
+                                                      uint16_t* __restrict__ v, PoolSlot ps) {
   const int heads = Hq + 2 * H;
   const int b = blockIdx.x / heads, h = blockIdx.x % heads;
   const int half = D / 2;
   const float* src = qkv + (static_cast<int64_t>(b) * heads + h) * D;
   uint16_t* dst;
-  if (h < Hq)
+  if (h < Hq) {
     dst = q + (static_cast<int64_t>(b) * Hq + h) * D;
-  else if (h < Hq + H)
+  } else if constexpr (POOL) {
+    const int p = pos[b];  // uniform over the workgroup
+    if (p < 0 || p >= ps.max_blocks * ps.T) return;
+    const int32_t blk = ps.tables[static_cast<int64_t>(b) * ps.max_blocks + p / ps.T];
+    if (blk < 0 || blk >= ps.nb) return;
+    const int g = h < Hq + H ? h - Hq : h - Hq - H;
+    // a head row (D * 2 bytes, dividing the page) never crosses a page
+    const uint64_t byte = ((static_cast<uint64_t>(g) * ps.nb + blk) * ps.T + p % ps.T) * D * 2;
+    const char* const* pt = h < Hq + H ? ps.pt_k : ps.pt_v;
+    dst = reinterpret_cast<uint16_t*>(const_cast<char*>(pt[byte >> 21]) +
+                                      (byte & (bst::kPage - 1)));
+  } else if (h < Hq + H) {
     dst = k + (static_cast<int64_t>(b) * H + (h - Hq)) * D;
-  else
+  } else {
     dst = v + (static_cast<int64_t>(b) * H + (h - Hq - H)) * D;
+  }
   for (int i = threadIdx.x; i < half; i += blockDim.x) {
     const float a = src[i], c = src[i + half];
     if (h >= Hq + H) {
@@ -350,10 +376,33 @@ int boost_rope_qkv(boost_ctx* ctx, const float* qkv, const int32_t* positions, i
   if (ctx->device < 0) return fail(BOOST_ENODEV, "plan-only context");
   if (B < 1 || Hq < 1 || H < 1 || D < 2 || D % 2 || !(theta > 1.0))
     return fail(BOOST_EINVAL, "B=%d Hq=%d H=%d D=%d theta=%g", B, Hq, H, D, theta);
-  hipLaunchKernelGGL(rope_qkv_kernel, dim3(B * (Hq + 2 * H)), dim3(64), 0,
+  hipLaunchKernelGGL(rope_qkv_kernel<false>, dim3(B * (Hq + 2 * H)), dim3(64), 0,
                      static_cast<hipStream_t>(stream), qkv, positions, Hq, H, D, std::log2(theta),
                      static_cast<uint16_t*>(q), static_cast<uint16_t*>(k),
-                     static_cast<uint16_t*>(v));
+                     static_cast<uint16_t*>(v), PoolSlot{});
+  BOOST_HIP(hipGetLastError());
+  return BOOST_OK;
+}
+
+int boost_rope_kv_append(boost_ctx* ctx, const boost_kv_pool* p, int layer, const float* qkv,
+                         const int32_t* positions, int B, int Hq, double theta,
+                         const int32_t* block_tables, int max_blocks, void* q, void* stream) {
+  if (!ctx || !p || !qkv || !positions || !block_tables || !q)
+    return fail(BOOST_EINVAL, "null argument");
+  if (ctx->device < 0 || !p->d_page_table) return fail(BOOST_ENODEV, "plan-only pool");
+  if (layer < 0 || static_cast<uint32_t>(layer) >= p->cfg.layers)
+    return fail(BOOST_EINVAL, "layer %d", layer);
+  const int H = static_cast<int>(p->cfg.kv_heads), D = static_cast<int>(p->cfg.head_dim);
+  if (B < 1 || max_blocks < 1 || Hq < 1 || !(theta > 1.0) || kPage % (2ull * D) != 0)
+    return fail(BOOST_EINVAL, "B=%d max_blocks=%d Hq=%d theta=%g D=%d", B, max_blocks, Hq,
+                theta, D);
+  const uint64_t P = p->geom.pages;
+  const PoolSlot ps{p->d_page_table + 2ull * layer * P, p->d_page_table + (2ull * layer + 1) * P,
+                    block_tables, max_blocks, static_cast<int>(p->cfg.block_tokens),
+                    static_cast<int>(p->geom.nb)};
+  hipLaunchKernelGGL(rope_qkv_kernel<true>, dim3(B * (Hq + 2 * H)), dim3(64), 0,
+                     static_cast<hipStream_t>(stream), qkv, positions, Hq, H, D, std::log2(theta),
+                     static_cast<uint16_t*>(q), nullptr, nullptr, ps);
   BOOST_HIP(hipGetLastError());
   return BOOST_OK;
 }

@@ -10,7 +10,7 @@ This module only sequences C-ABI calls and owns the activation buffers
 
 where every "residual_add -> rmsnorm" pair is one add_rmsnorm launch (the
 down projection's residual is added by the next layer's first norm, or by
-the final norm).
+the final norm) and "rope_qkv -> kv_append" is one rope_kv_append launch.
 
 Weights are [out, in] bf16 matrices placed page by page (each tensor on its
 own, so modulo placement restarts per tensor); norm weights are small bf16
@@ -61,8 +61,6 @@ class DecodeModel:
         self.h = torch.zeros((B, D.d), dtype=b16, device=dev)
         self.qkv = torch.zeros((B, (D.hq + 2 * D.hkv) * D.hd), dtype=f32, device=dev)
         self.q = torch.zeros((B, D.hq, D.hd), dtype=b16, device=dev)
-        self.k = torch.zeros((B, D.hkv, D.hd), dtype=b16, device=dev)
-        self.v = torch.zeros((B, D.hkv, D.hd), dtype=b16, device=dev)
         self.o = torch.zeros((B, D.hq, D.hd), dtype=b16, device=dev)
         self.tmp = torch.zeros((B, D.d), dtype=f32, device=dev)
         self.gu = torch.zeros((B, 2 * D.ffn), dtype=f32, device=dev)
@@ -93,9 +91,8 @@ class DecodeModel:
             else:
                 bd.boost_rmsnorm(c, self.x, self.norms[f"norm1.{l}"], B, D.d, EPS, self.h, s)
             bd.boost_decode_gemv(c, self.mat[f"qkv.{l}"], qkv_n, D.d, self.h, B, self.qkv, F32, s)
-            bd.boost_rope_qkv(c, self.qkv, positions, B, D.hq, D.hkv, D.hd, THETA,
-                              self.q, self.k, self.v, s)
-            bd.boost_kv_append(c, self.pool, l, tables, self.mb, positions, self.k, self.v, B, s)
+            bd.boost_rope_kv_append(c, self.pool, l, self.qkv, positions, B, D.hq, THETA,
+                                    tables, self.mb, self.q, s)
             bd.boost_paged_attn_decode(c, self.pool, l, self.q, B, D.hq, tables, self.mb,
                                        lens, 0.0, self.o, BF16, s)
             bd.boost_decode_gemv(c, self.mat[f"o.{l}"], D.d, D.hq * D.hd, self.o, B,

@@ -169,3 +169,58 @@ def test_add_rmsnorm_equals_add_then_norm(gpu_ctx, d):
     with pytest.raises(bd.BoostError) as e:
         bd.boost_add_rmsnorm(gpu_ctx, x2, None, wd, 5, d, 1e-5, o2, stream())
     assert e.value.code == bd.EINVAL
+
+
+def test_rope_kv_append_equals_pair(gpu_ctx):
+    """The fused RoPE + KV append writes the same q as the RoPE call and the
+    same pool slots as the KV append (two identical all-HBM pools, one filled
+    each way: attention over them agrees bitwise; a one-token context returns
+    the appended value head exactly); a position outside the table is
+    skipped by both."""
+    import torch
+    rng = np.random.default_rng(7)
+    heads = HQ + 2 * HKV
+    G = HQ // HKV
+    mb = 32  # blocks per request in the table (512 positions)
+    pos = np.array([0, 1, 15, 16, 100, 255, 511, mb * 16], dtype=np.int32)  # last: outside
+    qkv = rng.standard_normal((B, heads * HD)).astype(np.float32)
+    pools, outs, qs = [], [], []
+    try:
+        for fused in (False, True):
+            pool = bd.boost_kv_pool_create(gpu_ctx, 2, HKV, HD, B * mb, 0, bd.KV_ALL_HBM,
+                                           q_heads=HQ, max_batch=B, max_blocks_per_seq=mb)
+            pools.append(pool)
+            tables = np.stack([bd.boost_kv_alloc(pool, b, mb) for b in range(B)]).astype(np.int32)
+            td, pd = dev(tables), dev(pos)
+            q = torch.empty((B, HQ, HD), dtype=torch.int16, device="cuda")
+            if fused:
+                bd.boost_rope_kv_append(gpu_ctx, pool, 1, dev(qkv), pd, B, HQ, 500000.0, td,
+                                        mb, q, stream())
+            else:
+                k = torch.empty((B, HKV, HD), dtype=torch.int16, device="cuda")
+                v = torch.empty((B, HKV, HD), dtype=torch.int16, device="cuda")
+                bd.boost_rope_qkv(gpu_ctx, dev(qkv), pd, B, HQ, HKV, HD, 500000.0, q, k, v,
+                                  stream())
+                bd.boost_kv_append(gpu_ctx, pool, 1, td, mb, pd, k, v, B, stream())
+            lens = np.minimum(pos + 1, mb * 16).astype(np.int32)
+            out = torch.empty((B, HQ, HD), dtype=torch.float32, device="cuda")
+            bd.boost_paged_attn_decode(gpu_ctx, pool, 1, q, B, HQ, td, mb, dev(lens), 0.0, out,
+                                       bd.DTYPE_F32, stream())
+            sync()
+            qs.append(host_u16(q))
+            outs.append(out.cpu().numpy())
+        assert np.array_equal(qs[0], qs[1])
+        assert np.array_equal(outs[0].view(np.uint32), outs[1].view(np.uint32))
+        # request 0 has one token: its output is the appended value head itself
+        want_v = bf16_to_f32(ods.to_bf16(qkv[0, (HQ + HKV) * HD:].astype(np.float64)))
+        want_v = want_v.reshape(HKV, HD)
+        for h in range(HQ):
+            assert np.array_equal(outs[1][0, h], want_v[h // G])
+        with pytest.raises(bd.BoostError) as e:
+            bd.boost_rope_kv_append(gpu_ctx, pools[1], 2, dev(qkv), dev(pos), B, HQ, 500000.0,
+                                    dev(np.zeros((B, mb), np.int32)), mb, dev(qs[1]),
+                                    stream())
+        assert e.value.code == bd.EINVAL
+    finally:
+        for p in pools:
+            bd.boost_kv_pool_destroy(p)
