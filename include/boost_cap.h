@@ -213,9 +213,9 @@ int boost_prefetch(boost_ctx *ctx, const boost_tensor *view, void *stream);
  *   BOOST_SCHED_CAP: CTA specialisation (§3.2): `host_workers` persistent
  *     workgroups, dispatched first, stream every host-page unit while all
  *     other workgroups stream HBM-page units, so host and HBM reads overlap in
- *     every wave (§3 "CAP").  host_workers = 0 picks the default: one
- *     worker per 16 host units of the tensor, at least n_cu / 16 and at
- *     most n_cu / 8. */
+ *     every wave (§3 "CAP").  host_workers = 0 picks the default: n_cu / 16
+ *     for the GEMV (B <= 6); for the matrix-core kernels one worker per 16
+ *     host units of the tensor, at least n_cu / 16 and at most n_cu / 8. */
 #define BOOST_SCHED_ADDRESS 0
 #define BOOST_SCHED_CAP 1
 int boost_gemv_set_schedule(boost_ctx *ctx, int schedule, int host_workers);

@@ -927,7 +927,8 @@ inline int k_splits(int K) {
 // Units per page and grid size for units of rows_wg rows; fills in
 // P.units_per_page, P.host_workers and P.address_order.  Returns -1 if the
 // grid is too large.
-int64_t plan_grid(GemvParams& P, int n_pages, int rows_wg, const boost_ctx* ctx) {
+int64_t plan_grid(GemvParams& P, int n_pages, int rows_wg, const boost_ctx* ctx,
+                  bool matrix_core) {
   // units per page: enough for the page that meets the most rows
   const int64_t K = P.K, total = static_cast<int64_t>(P.N) * K;
   int64_t most = 0;
@@ -944,11 +945,14 @@ int64_t plan_grid(GemvParams& P, int n_pages, int rows_wg, const boost_ctx* ctx)
     grid = static_cast<int64_t>(n_pages) * P.units_per_page;
   } else {
     const int64_t host_units = static_cast<int64_t>(P.n_host_pages) * P.units_per_page;
-    // default: one host worker per BOOST_HOST_UNITS_PER_WORKER host units,
-    // between n_cu / 16 and n_cu / 8 (a tensor with many host pages keeps
-    // more requests on the link in flight; with few, extra workers only slow
-    // the HBM units beside them)
-    const int64_t h_lo = std::max(1, ctx->n_cu / 16), h_hi = std::max(1, ctx->n_cu / 8);
+    // default: n_cu / 16 host workers.  The matrix-core kernels, whose
+    // workgroups keep fewer bytes in flight, take one per
+    // BOOST_HOST_UNITS_PER_WORKER host units, up to n_cu / 8 (70B step at
+    // batch 8: 427.6 -> 419.2 ms).  The GEMV's workgroups already keep the
+    // link busy; more of them slowed the HBM units beside them (2 GiB tensor,
+    // 8 host pages: 360 -> 432 us).
+    const int64_t h_lo = std::max(1, ctx->n_cu / 16);
+    const int64_t h_hi = matrix_core ? std::max(1, ctx->n_cu / 8) : h_lo;
     const int64_t h_want = (host_units + BOOST_HOST_UNITS_PER_WORKER - 1) / BOOST_HOST_UNITS_PER_WORKER;
     int h = ctx->gemv_host_workers > 0 ? ctx->gemv_host_workers
                                        : static_cast<int>(std::min(h_hi, std::max(h_lo, h_want)));
@@ -971,7 +975,7 @@ int launch_fixup(GemvParams& P, int n_pages, bool need_fixup, hipStream_t s) {
 template <int B, int KS>
 int launch(GemvParams& P, int n_pages, bool need_fixup, const boost_ctx* ctx, hipStream_t s) {
   constexpr int RW = Shape<B, KS>::RW, UN = Shape<B, KS>::UN;
-  const int64_t grid = plan_grid(P, n_pages, RW * (kWaves / KS), ctx);
+  const int64_t grid = plan_grid(P, n_pages, RW * (kWaves / KS), ctx, false);
   if (grid < 0) return bst::fail(BOOST_EINVAL, "grid too large");
   hipLaunchKernelGGL((gemv_kernel<B, RW, UN, KS>), dim3(static_cast<unsigned>(grid)),
                      dim3(kThreads), 0, s, P);
@@ -996,7 +1000,7 @@ template <int BT, int RT, int UN, bool WL>
 int launch_mfma_shape(GemvParams& P, int n_pages, bool need_fixup, const boost_ctx* ctx,
                       hipStream_t s) {
   P.S = 1;
-  int64_t grid = plan_grid(P, n_pages, 16 * RT, ctx);
+  int64_t grid = plan_grid(P, n_pages, 16 * RT, ctx, true);
   if (grid < 0) return bst::fail(BOOST_EINVAL, "grid too large");
   const int64_t units = static_cast<int64_t>(n_pages) * P.units_per_page;
   int S = 1;
@@ -1037,7 +1041,7 @@ template <int BT, int RT>
 int launch_gemm_shape(GemvParams& P, int n_pages, bool need_fixup, const boost_ctx* ctx,
                       hipStream_t s) {
   P.S = 1;
-  int64_t grid = plan_grid(P, n_pages, 64 * RT, ctx);
+  int64_t grid = plan_grid(P, n_pages, 64 * RT, ctx, true);
   if (grid < 0) return bst::fail(BOOST_EINVAL, "grid too large");
   const int64_t units = static_cast<int64_t>(n_pages) * P.units_per_page;
   // split K over S workgroups until there are about three workgroups per
