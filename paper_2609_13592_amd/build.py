@@ -1,6 +1,13 @@
 """Build libboostcap.so (HIP for gfx950 + host C++) in-tree.
 
 Usage: python -m paper_2609_13592_amd.build   (or build() from Python)
+
+       python -m paper_2609_13592_amd.build --sanitize
+           host-code AddressSanitizer (+ UndefinedBehaviorSanitizer for the
+           plain C++ files) build into _lib_sanitize/, for the CPU tests:
+           BOOST_LIB=<that .so> LD_PRELOAD="<libasan.so> <libubsan.so>"
+           ASAN_OPTIONS=detect_leaks=0 python -m pytest tests -m "not gpu".
+           Device code is built as usual (no GPU sanitizer).
 """
 from __future__ import annotations
 
@@ -35,11 +42,19 @@ def _sources():
     return hip, cpp
 
 
-def _compile(src: str, obj: str, is_hip: bool):
+# host-only sanitizer flags: each -fsanitize= right after -Xarch_host on the
+# hipcc lines, so device code is never built with it
+SAN_HIP = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fno-omit-frame-pointer"]
+SAN_CXX = ["-fsanitize=address,undefined", "-fno-sanitize-recover=undefined",
+           "-fno-omit-frame-pointer"]
+
+
+def _compile(src: str, obj: str, is_hip: bool, sanitize: bool = False):
     if is_hip:
-        cmd = [HIPCC, *HIP_FLAGS, "-x", "hip", "-c", src, "-o", obj]
+        cmd = [HIPCC, *HIP_FLAGS, *(SAN_HIP if sanitize else []), "-x", "hip", "-c", src,
+               "-o", obj]
     else:
-        cmd = ["g++", *CXX_FLAGS, "-c", src, "-o", obj]
+        cmd = ["g++", *CXX_FLAGS, *(SAN_CXX if sanitize else []), "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     # the host pass does not know the packed-fp32 feature: harmless warning
     err = "\n".join(l for l in r.stderr.splitlines()
@@ -49,32 +64,36 @@ def _compile(src: str, obj: str, is_hip: bool):
     return err.strip()
 
 
-def build(verbose: bool = False) -> str:
-    os.makedirs(OUT_DIR, exist_ok=True)
-    obj_dir = os.path.join(OUT_DIR, "obj")
+def build(verbose: bool = False, sanitize: bool = False) -> str:
+    out_dir = os.path.join(HERE, "_lib_sanitize") if sanitize else OUT_DIR
+    lib = os.path.join(out_dir, "libboostcap.so")
+    os.makedirs(out_dir, exist_ok=True)
+    obj_dir = os.path.join(out_dir, "obj")
     os.makedirs(obj_dir, exist_ok=True)
     hip, cpp = _sources()
     jobs = []
     with cf.ThreadPoolExecutor(max_workers=min(8, os.cpu_count() or 4)) as ex:
         for f in hip:
             jobs.append(ex.submit(_compile, os.path.join(CSRC, f),
-                                  os.path.join(obj_dir, f + ".o"), True))
+                                  os.path.join(obj_dir, f + ".o"), True, sanitize))
         for f in cpp:
             jobs.append(ex.submit(_compile, os.path.join(CSRC, f),
-                                  os.path.join(obj_dir, f + ".o"), False))
+                                  os.path.join(obj_dir, f + ".o"), False, sanitize))
         for j in jobs:
             msg = j.result()
             if msg and verbose:
                 print(msg, file=sys.stderr)
     objs = [os.path.join(obj_dir, f + ".o") for f in hip + cpp]
-    tmp = LIB + ".tmp"
+    tmp = lib + ".tmp"
     cmd = [HIPCC, "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp, *objs]
+    if sanitize:
+        cmd += ["-Xarch_host", "-fsanitize=address", "-lubsan"]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed: {' '.join(cmd)}\n{r.stderr}")
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib)
+    return lib
 
 
 if __name__ == "__main__":
-    print(build(verbose=True))
+    print(build(verbose=True, sanitize="--sanitize" in sys.argv[1:]))

@@ -77,8 +77,9 @@ def test_single_layer_parity(gpu_ctx):
 @pytest.mark.parametrize("N,K,B", [(4096, 4096, 1), (300, 14336, 1), (5000, 520, 3),
                                    (1000, 8, 8), (257, 4104, 2), (77, 28672, 5)])
 def test_placement_invariance_and_parity(gpu_ctx, N, K, B):
-    """Bitwise-equal y under all-HBM, alternating, MPP and all-host maps and
-    both schedules; every result within the bar of the oracle."""
+    """Bitwise-equal y under all-HBM, alternating, MPP and all-host maps, both
+    schedules and any number of host workers; every result within the bar
+    of the oracle."""
     w, x = synth.gemv_inputs(11 + N + K + B, N, K, B)
     n = opl.n_pages(w.nbytes)
     maps = {"hbm": np.zeros(n, np.uint8), "host": np.ones(n, np.uint8),
@@ -91,8 +92,11 @@ def test_placement_invariance_and_parity(gpu_ctx, N, K, B):
     for name, tiers in maps.items():
         t = place(gpu_ctx, w, tiers=tiers)
         try:
-            for sched in (bd.SCHED_CAP, bd.SCHED_ADDRESS):
-                bd.boost_gemv_set_schedule(gpu_ctx, sched, 3)
+            # CAP with 3 host workers, with the default count, and with more
+            # workers than host units; address order
+            for sched, hw in ((bd.SCHED_CAP, 3), (bd.SCHED_CAP, 0), (bd.SCHED_CAP, 999),
+                              (bd.SCHED_ADDRESS, 0)):
+                bd.boost_gemv_set_schedule(gpu_ctx, sched, hw)
                 y = run_gemv(gpu_ctx, t, N, K, xd, B)
                 assert og.rel_err(y, r64) <= TOL, (name, sched)
                 assert og.rel_err(y, r32) <= TOL, (name, sched)
@@ -123,8 +127,11 @@ def test_mfma_placement_invariance_and_parity(gpu_ctx, N, K, B):
     for name, tiers in maps.items():
         t = place(gpu_ctx, w, tiers=tiers)
         try:
-            for sched in (bd.SCHED_CAP, bd.SCHED_ADDRESS):
-                bd.boost_gemv_set_schedule(gpu_ctx, sched, 3)
+            # CAP with 3 host workers, with the default count, and with more
+            # workers than host units; address order
+            for sched, hw in ((bd.SCHED_CAP, 3), (bd.SCHED_CAP, 0), (bd.SCHED_CAP, 999),
+                              (bd.SCHED_ADDRESS, 0)):
+                bd.boost_gemv_set_schedule(gpu_ctx, sched, hw)
                 y = run_gemv(gpu_ctx, t, N, K, xd, B)
                 assert og.rel_err(y, r64) <= TOL, (name, sched)
                 assert_f32_bound(y, w, x)
