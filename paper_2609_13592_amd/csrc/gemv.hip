@@ -634,6 +634,9 @@ __global__ __launch_bounds__(kThreads) void mfma_kernel(GemvParams P) {
 // Columns of x (and of W) per LDS chunk: the chunk must be at least one
 // 16-byte load per lane of the workgroup, and one chunk of W per wavefront is
 // what it keeps in flight
+#ifndef BOOST_GEMM_DMA
+#define BOOST_GEMM_DMA 1  // 0: gemm_kernel for every shape
+#endif
 #ifndef BOOST_GEMM_XC_SMALL
 #define BOOST_GEMM_XC_SMALL 128  // batch tiles <= 4
 #endif
@@ -833,6 +836,256 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemvParams P) {
   } else {
     const int u = bid - P.host_workers;
     gemm_unit<BT, RT>(P, P.hbm_pages[u / U], u % U, lds);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Matrix-core GEMM with W and x streamed into LDS by direct-to-LDS loads.
+//
+// Same unit as gemm_unit (64 RT rows of one page, one slice of K, wavefront w
+// owns row tiles w RT .. w RT + RT - 1), but K is walked in stages of 64
+// columns through a ring of dma_stages() stages in LDS, and every byte of a
+// stage, W rows and x rows alike, goes from memory straight into LDS
+// (buffer_load ... lds): no register holds data in flight, so all but one
+// stage of the ring stay in flight per workgroup (gemm_unit keeps one chunk
+// in registers).  One such load instruction moves 1 KiB: lane i writes LDS
+// bytes [16 i, 16 i + 16) of the block at M0, and a lane chooses which global
+// 16 bytes it fetches, so an instruction reads 8 whole 128-byte rows of a
+// stage and lays them out swizzled: row r (0..7) of block b keeps its
+// 16-byte chunk c at position c ^ r ^ (b & 1), so the 16 rows of a fragment
+// read at one chunk (rows 0..7 from an even block, 8..15 from the next) sit
+// at 16 distinct 16-byte positions modulo 256 bytes.  The compiler does not
+// see these loads (inline assembly: it would otherwise wait for all of them
+// before any LDS read); the waits on them are explicit, in issue
+// order: before stage s is read, each wavefront waits until only the later
+// stages' loads are outstanding, then the workgroup barrier makes every
+// wavefront's part of the stage visible and frees the slot read in the
+// previous step, which the next loads overwrite.  Out-of-range lanes (rows
+// past the page, columns outside the page or the slice, batch rows past B)
+// write zeros into LDS, as out-of-range register loads return zeros.
+constexpr int kDmaBlk = 1024;  // 8 rows x 128 bytes
+constexpr int kDmaLds = 160000;  // LDS bytes a ring may take
+// bytes of one stage: W rows, then x rows (stages of 128 columns, one
+// barrier per 128 columns, were 2-7 % slower on the 8B shapes at batch
+// 32..256)
+template <int BT, int RT>
+constexpr int dma_stage_bytes() { return (8 * RT + 2 * BT) * kDmaBlk; }
+// as many stages as fit, up to BOOST_GEMM_DMA_NS (deeper rings, up to 16
+// stages, were no faster on the 8B and 70B shapes)
+#ifndef BOOST_GEMM_DMA_NS
+#define BOOST_GEMM_DMA_NS 4
+#endif
+template <int BT, int RT>
+constexpr int dma_stages() {
+  return kDmaLds / dma_stage_bytes<BT, RT>() >= BOOST_GEMM_DMA_NS ? BOOST_GEMM_DMA_NS
+                                                                  : kDmaLds / dma_stage_bytes<BT, RT>();
+}
+
+// s_waitcnt immediate that waits until at most n vector-memory loads of this
+// wavefront are outstanding (other counters untouched)
+template <int n>
+constexpr int vmcnt_imm() {
+  static_assert(n >= 0 && n < 64, "vmcnt range");
+  return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8);
+}
+
+// 16 bytes per lane from buffer resource r at byte offset off into LDS at
+// lds_block + 16 lane (lds_block uniform over the wavefront).  M0 is set here
+// and declared clobbered; nothing else in these kernels uses M0 (clang warns
+// that a reserved register is clobbered, which is the intent).  One wait
+// state separates the M0 write from the load that reads it, as the compiler
+// leaves between its own M0 writes and direct-to-LDS loads.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void load16_lds(__amdgpu_buffer_rsrc_t r, uint32_t off,
+                                           const char* lds_block) {
+  typedef __attribute__((address_space(3))) const char* lds_ptr;  // LDS byte address
+  const uint32_t la = __builtin_amdgcn_readfirstlane(
+      static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_ptr)lds_block)));
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :
+               : "s"(la), "v"(off), "s"(r)
+               : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+template <int BT, int RT>
+__device__ __forceinline__ void gemm_dma_unit(const GemvParams& P, int page_in, int unit_in,
+                                              char* ring) {
+  static_assert(BT % 2 == 0, "x blocks are spread evenly over the four wavefronts");
+  constexpr int kNs = dma_stages<BT, RT>();
+  constexpr int kSb = dma_stage_bytes<BT, RT>();
+  constexpr int kXq = BT / 2;            // x blocks loaded per wavefront and stage
+  constexpr int kLoads = 2 * RT + kXq;   // load instructions per wavefront and stage
+  static_assert(kNs >= 2, "ring of at least two stages");
+  const int page = __builtin_amdgcn_readfirstlane(page_in);
+  const int unit = __builtin_amdgcn_readfirstlane(unit_in);
+  const int j = unit / P.S, slice = unit % P.S;
+  constexpr int R = 64 * RT;
+  const int64_t K = P.K;
+  const int64_t total = static_cast<int64_t>(P.N) * K;
+  const int64_t pe0 = static_cast<int64_t>(page) * kPageElems;
+  const int64_t pe1 = min(pe0 + kPageElems, total);
+  const int64_t r_lo = pe0 / K;
+  const int64_t r_hi = (pe1 - 1) / K;  // inclusive
+  const int64_t rbase = r_lo + static_cast<int64_t>(j) * R;
+  if (rbase > r_hi) return;  // uniform over the workgroup
+  const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
+  const int lane = threadIdx.x & 63;
+  const int lrow = lane & 15, lgrp = lane >> 4;
+
+  const __amdgpu_buffer_rsrc_t wr =
+      make_rsrc_uniform(P.page_table[page], static_cast<uint32_t>((pe1 - pe0) * 2));
+  const __amdgpu_buffer_rsrc_t xr =
+      make_rsrc_uniform(P.x, static_cast<uint32_t>(static_cast<int64_t>(P.B) * K * 2));
+
+  const int64_t ksl = (K + P.S - 1) / P.S;
+  const int64_t kslice = (ksl + 63) / 64 * 64;
+  const int64_t k_beg = min(K, slice * kslice);
+  const int64_t k_end = min(K, k_beg + kslice);
+  const int nst = static_cast<int>((k_end - k_beg + 63) / 64);
+
+  // loads: lane i of an instruction for block b fetches row i / 8 of the
+  // block and the chunk it stores at position i % 8, i.e. chunk
+  // (i % 8) ^ (i / 8) ^ (b & 1); W blocks 2 T + h (tile T, rows 8 h ..),
+  // x blocks 8 RT + 4 q + wave (an even base: parity of wave)
+  const int brow = lane >> 3;
+  const int c0 = (lane & 7) ^ brow;  // chunk at parity 0; parity 1: c0 ^ 1
+  uint32_t ro[RT][2];
+#pragma unroll
+  for (int a = 0; a < RT; ++a)
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int64_t r = rbase + 16 * (wave * RT + a) + 8 * h + brow;
+      ro[a][h] = r > r_hi ? kOOB
+                          : static_cast<uint32_t>((r * K - pe0) * 2) + 16 * (c0 ^ h);
+    }
+  const int cx = c0 ^ (wave & 1);
+  uint32_t xo[kXq];
+#pragma unroll
+  for (int q = 0; q < kXq; ++q) {
+    const int b = 8 * (wave + 4 * q) + brow;
+    xo[q] = b < P.B ? static_cast<uint32_t>(static_cast<int64_t>(b) * K * 2) + 16 * cx : kOOB;
+  }
+  auto issue = [&](int s, int slot) {  // stage s into ring slot `slot`
+    const int64_t kb = 64 * static_cast<int64_t>(s);
+    // a chunk at or past k_end (a multiple of 8) reads zeros
+    const int64_t kc0 = k_beg + kb + 8 * c0, kc1 = k_beg + kb + 8 * (c0 ^ 1);
+    const uint32_t oob0 = kc0 < k_end ? 0u : kOOB, oob1 = kc1 < k_end ? 0u : kOOB;
+    const uint32_t oobx = (wave & 1) ? oob1 : oob0;
+    const uint32_t kb2 = static_cast<uint32_t>((k_beg + kb) * 2);
+    const char* st = ring + slot * kSb;
+#pragma unroll
+    for (int a = 0; a < RT; ++a)
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+        load16_lds(wr, (ro[a][h] + kb2) | (h ? oob1 : oob0),
+                   st + (2 * (wave * RT + a) + h) * kDmaBlk);
+#pragma unroll
+    for (int q = 0; q < kXq; ++q)
+      load16_lds(xr, (xo[q] + kb2) | oobx, st + (8 * RT + wave + 4 * q) * kDmaBlk);
+  };
+
+  // fragment reads: lane l takes row l % 16 of a tile (block 2 tile + h,
+  // h = l % 16 / 8, block row l % 8) and 8 columns at chunk 4 sub + l / 16
+  // of the stage, at position chunk ^ row ^ h
+  const int r8 = lrow & 7, hb = lrow >> 3;
+  const int fo = hb * kDmaBlk + r8 * 128;
+  const int fx0 = ((lgrp ^ r8 ^ hb) << 4), fx1 = fx0 ^ 64;  // position, sub 0 / 1
+  const int wa = 2 * wave * RT * kDmaBlk + fo;
+  const int xa = 8 * RT * kDmaBlk + fo;
+
+  f32x4_t acc[RT][BT];
+#pragma unroll
+  for (int a = 0; a < RT; ++a)
+#pragma unroll
+    for (int t = 0; t < BT; ++t) acc[a][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  constexpr int TG = BT < 4 ? BT : 4;  // x fragments live at once
+  auto mma = [&](const char* st) {
+#pragma unroll
+    for (int sub = 0; sub < 2; ++sub) {  // the stage's two 32-column steps
+      const int fx = sub ? fx1 : fx0;
+      uint4 wf[RT];
+#pragma unroll
+      for (int a = 0; a < RT; ++a)
+        wf[a] = *reinterpret_cast<const uint4*>(st + wa + a * 2 * kDmaBlk + fx);
+#pragma unroll
+      for (int t0 = 0; t0 < BT; t0 += TG) {
+        uint4 xf[TG];
+#pragma unroll
+        for (int u = 0; u < TG; ++u)
+          xf[u] = *reinterpret_cast<const uint4*>(st + xa + (t0 + u) * 2 * kDmaBlk + fx);
+#pragma unroll
+        for (int u = 0; u < TG; ++u)
+#pragma unroll
+          for (int a = 0; a < RT; ++a)
+            acc[a][t0 + u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                as_bf16x8(wf[a]), as_bf16x8(xf[u]), acc[a][t0 + u], 0, 0, 0);
+      }
+    }
+  };
+
+#pragma unroll
+  for (int s = 0; s < kNs - 1; ++s) issue(s, s);  // stages past the slice: zeros
+  int slot = 0, fill = kNs - 1;
+#pragma unroll 1
+  for (int s = 0; s < nst; ++s) {
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm<(kNs - 2) * kLoads>());  // stage s landed
+    __syncthreads();  // ... for every wavefront; slot `fill` is no longer read
+    issue(s + kNs - 1, fill);
+    mma(ring + slot * kSb);
+    slot = slot + 1 == kNs ? 0 : slot + 1;
+    fill = fill + 1 == kNs ? 0 : fill + 1;
+  }
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm<0>());  // the loads issued past the slice
+  __syncthreads();  // LDS is reused by the next unit of a persistent worker
+
+#pragma unroll
+  for (int a = 0; a < RT; ++a)
+#pragma unroll
+    for (int t = 0; t < BT; ++t) {
+      const int b = 16 * t + lrow;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int64_t r = rbase + 16 * (wave * RT + a) + 4 * lgrp + e;
+        if (b >= P.B || r > r_hi) continue;
+        const float v = acc[a][t][e];
+        const int64_t e0 = r * K;
+        const int side = e0 < pe0 ? 1 : (e0 + K > pe1 ? 0 : -1);  // cut row: its part's side
+        if (P.S == 1) {
+          if (side == 1)
+            P.partial[(static_cast<int64_t>(page) * 2 + 1) * bst::kMaxGemvBatch + b] = v;
+          else if (side == 0)
+            P.partial[(static_cast<int64_t>(page + 1) * 2) * bst::kMaxGemvBatch + b] = v;
+          else
+            store_y(P, b, r, v);
+        } else if (side < 0) {
+          P.ws[(static_cast<int64_t>(slice) * P.B + b) * P.N + r] = v;
+        } else {
+          const int64_t bnd = side ? page : page + 1;
+          P.ws[static_cast<int64_t>(P.S) * P.B * P.N +
+               ((bnd * 2 + side) * P.S + slice) * P.B + b] = v;
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+}
+
+template <int BT, int RT>
+__global__ __launch_bounds__(kThreads) void gemm_dma_kernel(GemvParams P) {
+  __shared__ __attribute__((aligned(16))) char ring[dma_stages<BT, RT>() * dma_stage_bytes<BT, RT>()];
+  const int bid = blockIdx.x;
+  const int U = P.units_per_page;
+  if (P.address_order) {
+    gemm_dma_unit<BT, RT>(P, bid / U, bid % U, ring);
+  } else if (bid < P.host_workers) {
+    const int n_host_units = P.n_host_pages * U;
+    for (int v = bid; v < n_host_units; v += P.host_workers)
+      gemm_dma_unit<BT, RT>(P, P.host_pages[v / U], v % U, ring);
+  } else {
+    const int u = bid - P.host_workers;
+    gemm_dma_unit<BT, RT>(P, P.hbm_pages[u / U], u % U, ring);
   }
 }
 
@@ -1066,8 +1319,18 @@ int launch_gemm_shape(GemvParams& P, int n_pages, bool need_fixup, const boost_c
                            : P.host_workers + static_cast<int64_t>(P.n_hbm_pages) *
                                                   P.units_per_page;
   }
-  hipLaunchKernelGGL((gemm_kernel<BT, RT>), dim3(static_cast<unsigned>(grid)), dim3(kThreads),
-                     0, s, P);
+  // direct-to-LDS streaming up to four batch tiles, and beyond that with
+  // 128-row units; with 64-row units and eight or more batch tiles every
+  // wavefront re-reads the large x tile from LDS for only 16 rows, and the
+  // register-streamed kernel, whose W bypasses LDS, is faster (8B and 70B
+  // shapes at batch 32..256: 0-22 % faster where chosen, 8-21 % slower on
+  // the 70B shapes at batch >= 128 with 64-row units)
+  if (BOOST_GEMM_DMA && (BT <= 4 || RT == 2))
+    hipLaunchKernelGGL((gemm_dma_kernel<BT, RT>), dim3(static_cast<unsigned>(grid)),
+                       dim3(kThreads), 0, s, P);
+  else
+    hipLaunchKernelGGL((gemm_kernel<BT, RT>), dim3(static_cast<unsigned>(grid)), dim3(kThreads),
+                       0, s, P);
   BOOST_HIP(hipGetLastError());
   if (S == 1) return launch_fixup(P, n_pages, need_fixup, s);
   const int64_t lanes = static_cast<int64_t>(P.B) * P.N;

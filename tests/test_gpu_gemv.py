@@ -109,13 +109,17 @@ def test_placement_invariance_and_parity(gpu_ctx, N, K, B):
         assert np.array_equal(y.view(np.uint32), outs[0].view(np.uint32))
 
 
-@pytest.mark.parametrize("N,K,B", [(300, 14336, 7), (5000, 520, 16), (257, 4104, 33),
-                                   (77, 28672, 64), (1000, 8, 100), (600, 4096, 128),
-                                   (130, 14336, 256), (40, 56, 200)])
+@pytest.mark.parametrize("N,K,B", [(300, 14336, 7), (5000, 520, 16), (257, 4104, 20),
+                                   (257, 4104, 33), (77, 28672, 64), (1000, 8, 100),
+                                   (600, 4096, 128), (300, 14336, 128), (130, 14336, 256),
+                                   (40, 56, 200)])
 def test_mfma_placement_invariance_and_parity(gpu_ctx, N, K, B):
     """Batches from 7 up run on the matrix cores: bitwise-equal y under every
     map and schedule, every result within the bar of the oracle (ragged
-    batch tiles, rows cut by page boundaries, pages of both tiers)."""
+    batch tiles, rows cut by page boundaries, pages of both tiers).  Both
+    GEMM kernels appear: direct-to-LDS streaming (B = 20, 33, 64, and
+    128-row units at B = 128 and 256 with K = 14336) and register streaming
+    (64-row units at B = 100, 128, 200)."""
     w, x = synth.gemv_inputs(17 + N + K + B, N, K, B)
     n = opl.n_pages(w.nbytes)
     maps = {"hbm": np.zeros(n, np.uint8), "host": np.ones(n, np.uint8),
