@@ -615,240 +615,21 @@ __global__ __launch_bounds__(kThreads) void mfma_kernel(GemvParams P) {
 }
 
 // ---------------------------------------------------------------------------
-// Matrix-core GEMM for larger batches, x shared through LDS.
+// Matrix-core GEMM for larger batches: W and x streamed into LDS by
+// direct-to-LDS loads.
 //
-// The unit is 64 RT rows of one page and one slice of K; the four wavefronts
-// split the rows (wavefront w owns row tiles w RT .. w RT + RT - 1, 16 rows
-// each) and all take every batch tile.  Per chunk of kXc columns the
-// workgroup copies x[0 .. 16 BT)[chunk] into LDS once (rows padded by 16
-// bytes so the fragment reads are free of bank conflicts), and every
-// wavefront reads its B fragments (lane l: batch row 16 t + l % 16, columns
-// 8 (l / 16) .. + 8 of each 32-column step) from there, so x crosses the
-// L2 -> CU path once per workgroup instead of once per wavefront and row
-// tile.  A fragments of W (lane l: row l % 16 of the tile, the same column
-// mapping) stream from the page straight into registers, one chunk ahead,
-// with the next chunk of x staged in registers meanwhile.  Each wavefront
-// ends with the full sums of its rows over the slice, so there is no
-// cross-wavefront reduction; rows cut by a page boundary and split-K slices
-// go through the same partial buffers as the other matrix-core path.
-// Columns of x (and of W) per LDS chunk: the chunk must be at least one
-// 16-byte load per lane of the workgroup, and one chunk of W per wavefront is
-// what it keeps in flight
-#ifndef BOOST_GEMM_DMA
-#define BOOST_GEMM_DMA 1  // 0: gemm_kernel for every shape
-#endif
-#ifndef BOOST_GEMM_XC_SMALL
-#define BOOST_GEMM_XC_SMALL 128  // batch tiles <= 4
-#endif
-#ifndef BOOST_GEMM_XC_MID
-#define BOOST_GEMM_XC_MID 64  // 8 batch tiles
-#endif
-#ifndef BOOST_GEMM_XC_BIG
-#define BOOST_GEMM_XC_BIG 64  // 16 batch tiles
-#endif
-template <int BT>
-constexpr int gemm_xc() {
-  return BT <= 4 ? BOOST_GEMM_XC_SMALL : (BT <= 8 ? BOOST_GEMM_XC_MID : BOOST_GEMM_XC_BIG);
-}
-template <int BT>
-constexpr int gemm_row_bytes() { return gemm_xc<BT>() * 2 + 16; }  // padded LDS row
-template <int BT>
-constexpr int gemm_lds_bytes() { return 2 * 16 * BT * gemm_row_bytes<BT>(); }
-
-template <int BT, int RT>
-__device__ __forceinline__ void gemm_unit(const GemvParams& P, int page_in, int unit_in,
-                                          char* lds) {
-  // uniform over the workgroup (the page id may come from a vector load the
-  // compiler cannot prove uniform; all that derives from it must stay scalar)
-  const int page = __builtin_amdgcn_readfirstlane(page_in);
-  const int unit = __builtin_amdgcn_readfirstlane(unit_in);
-  const int j = unit / P.S, slice = unit % P.S;
-  constexpr int R = 64 * RT;       // rows of a unit
-  constexpr int XB = 16 * BT;      // batch rows held in LDS (B padded to tiles)
-  constexpr int XC = gemm_xc<BT>();
-  constexpr int RB = gemm_row_bytes<BT>();
-  constexpr int NST = XC / 32;     // 32-column steps per chunk
-  constexpr int kXLoads = XB * XC * 2 / (kThreads * 16);  // 16-byte x loads per lane and chunk
-  static_assert(kXLoads >= 1 && XB * XC * 2 % (kThreads * 16) == 0, "x chunk shape");
-  const int64_t K = P.K;
-  const int64_t total = static_cast<int64_t>(P.N) * K;
-  const int64_t pe0 = static_cast<int64_t>(page) * kPageElems;
-  const int64_t pe1 = min(pe0 + kPageElems, total);
-  const int64_t r_lo = pe0 / K;
-  const int64_t r_hi = (pe1 - 1) / K;  // inclusive
-  const int64_t rbase = r_lo + static_cast<int64_t>(j) * R;
-  if (rbase > r_hi) return;  // uniform over the workgroup
-  const int wave = threadIdx.x >> 6;
-  const int lane = threadIdx.x & 63;
-  const int lrow = lane & 15, lgrp = lane >> 4;
-
-  const __amdgpu_buffer_rsrc_t wr =
-      make_rsrc_uniform(P.page_table[page], static_cast<uint32_t>((pe1 - pe0) * 2));
-  const __amdgpu_buffer_rsrc_t xr =
-      make_rsrc_uniform(P.x, static_cast<uint32_t>(static_cast<int64_t>(P.B) * K * 2));
-
-  // this unit's K slice, whole chunks (the last one may run past K: zeros)
-  const int64_t ksl = (K + P.S - 1) / P.S;
-  const int64_t kslice = (ksl + XC - 1) / XC * XC;
-  const int64_t k_beg = min(K, slice * kslice);
-  const int64_t k_end = min(K, k_beg + kslice);
-
-  // byte offset of column 0 of this lane's row in each of its row tiles
-  // (wrapped for a row begun on the previous page: its columns before the
-  // page read as zero; rows past the page read zero)
-  uint32_t ro[RT];
-#pragma unroll
-  for (int a = 0; a < RT; ++a) {
-    const int64_t r = rbase + 16 * (wave * RT + a) + lrow;
-    ro[a] = r > r_hi ? kOOB : static_cast<uint32_t>((r * K - pe0) * 2);
-  }
-  // x staging: load i of a lane covers batch row (tid + 256 i) / (XC / 8)
-  // and columns 8 ((tid + 256 i) % (XC / 8)) .. + 8 of the chunk
-  uint32_t xo[kXLoads];
-  int xl[kXLoads];
-#pragma unroll
-  for (int i = 0; i < kXLoads; ++i) {
-    const int e = threadIdx.x + kThreads * i;
-    const int b = e / (XC / 8), c = e % (XC / 8);
-    xo[i] = b < P.B ? static_cast<uint32_t>((static_cast<int64_t>(b) * K + 8 * c) * 2) : kOOB;
-    xl[i] = b * RB + 16 * c;
-  }
-  const int xcol = (static_cast<int>(threadIdx.x) % (XC / 8)) * 8;  // the same for every i
-
-  struct Stage {
-    uint4 w[NST][RT];
-    uint4 x[kXLoads];
-  };
-  auto load_chunk = [&](int64_t kb, Stage& g) {  // past k_end: zeros
-    const uint32_t oobx = kb + xcol < k_end ? 0u : kOOB;
-    const uint32_t kb2 = static_cast<uint32_t>(kb * 2);
-#pragma unroll
-    for (int i = 0; i < kXLoads; ++i) g.x[i] = load16(xr, (xo[i] + kb2) | oobx);
-#pragma unroll
-    for (int st = 0; st < NST; ++st) {
-      const int64_t kc = kb + 32 * st + 8 * lgrp;
-      const uint32_t oob = kc < k_end ? 0u : kOOB;
-      const uint32_t kc2 = static_cast<uint32_t>(kc * 2);
-#pragma unroll
-      for (int a = 0; a < RT; ++a) g.w[st][a] = load16<BOOST_MFMA_W_AUX>(wr, (ro[a] + kc2) | oob);
-    }
-  };
-
-  f32x4_t acc[RT][BT];
-#pragma unroll
-  for (int a = 0; a < RT; ++a)
-#pragma unroll
-    for (int t = 0; t < BT; ++t) acc[a][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-
-  // x of a chunk into LDS buffer xb (its previous readers finished before the
-  // last barrier), barrier, the chunk after next's loads, then the products
-  auto stage_x = [&](const Stage& g, char* xb) {
-#pragma unroll
-    for (int i = 0; i < kXLoads; ++i) *reinterpret_cast<uint4*>(xb + xl[i]) = g.x[i];
-  };
-  // batch tiles in groups of four, so at most four x fragments are live
-  constexpr int TG = BT < 4 ? BT : 4;
-  auto mma = [&](const Stage& g, const char* xb) {
-#pragma unroll
-    for (int st = 0; st < NST; ++st)
-#pragma unroll
-      for (int t0 = 0; t0 < BT; t0 += TG) {
-        uint4 xf[TG];
-#pragma unroll
-        for (int u = 0; u < TG; ++u)
-          xf[u] = *reinterpret_cast<const uint4*>(xb + (16 * (t0 + u) + lrow) * RB +
-                                                  (32 * st + 8 * lgrp) * 2);
-#pragma unroll
-        for (int u = 0; u < TG; ++u)
-#pragma unroll
-          for (int a = 0; a < RT; ++a)
-            acc[a][t0 + u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                as_bf16x8(g.w[st][a]), as_bf16x8(xf[u]), acc[a][t0 + u], 0, 0, 0);
-        __builtin_amdgcn_sched_barrier(0);
-      }
-  };
-  // two register sets in fixed roles, one chunk ahead; a chunk past k_end is
-  // zeros, so both halves always run and the loop has one exit
-  char* const xb0 = lds;
-  char* const xb1 = lds + XB * RB;
-  Stage ga, gb;
-  if (k_beg < k_end) load_chunk(k_beg, ga);
-#pragma unroll 1
-  for (int64_t kb = k_beg; kb < k_end; kb += 2 * XC) {
-    stage_x(ga, xb0);
-    __syncthreads();
-    load_chunk(kb + XC, gb);
-    __builtin_amdgcn_sched_barrier(0);  // keep the next chunk's loads ahead
-    mma(ga, xb0);
-    stage_x(gb, xb1);
-    __syncthreads();
-    load_chunk(kb + 2 * XC, ga);
-    __builtin_amdgcn_sched_barrier(0);
-    mma(gb, xb1);
-  }
-
-  // element (row 16 (wave RT + a) + 4 lgrp + e, batch 16 t + lrow) of the
-  // tiles, one tile at a time (keeps the address arithmetic out of the loop's
-  // registers)
-#pragma unroll
-  for (int a = 0; a < RT; ++a)
-#pragma unroll
-    for (int t = 0; t < BT; ++t) {
-      const int b = 16 * t + lrow;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int64_t r = rbase + 16 * (wave * RT + a) + 4 * lgrp + e;
-        if (b >= P.B || r > r_hi) continue;
-        const float v = acc[a][t][e];
-        const int64_t e0 = r * K;
-        const int side = e0 < pe0 ? 1 : (e0 + K > pe1 ? 0 : -1);  // cut row: its part's side
-        if (P.S == 1) {
-          if (side == 1)
-            P.partial[(static_cast<int64_t>(page) * 2 + 1) * bst::kMaxGemvBatch + b] = v;
-          else if (side == 0)
-            P.partial[(static_cast<int64_t>(page + 1) * 2) * bst::kMaxGemvBatch + b] = v;
-          else
-            store_y(P, b, r, v);
-        } else if (side < 0) {
-          P.ws[(static_cast<int64_t>(slice) * P.B + b) * P.N + r] = v;
-        } else {
-          const int64_t bnd = side ? page : page + 1;
-          P.ws[static_cast<int64_t>(P.S) * P.B * P.N +
-               ((bnd * 2 + side) * P.S + slice) * P.B + b] = v;
-        }
-      }
-      __builtin_amdgcn_sched_barrier(0);
-    }
-  __syncthreads();  // LDS is reused by the next unit of a persistent worker
-}
-
-template <int BT, int RT>
-__global__ __launch_bounds__(kThreads) void gemm_kernel(GemvParams P) {
-  __shared__ __attribute__((aligned(16))) char lds[gemm_lds_bytes<BT>()];
-  const int bid = blockIdx.x;
-  const int U = P.units_per_page;
-  if (P.address_order) {
-    gemm_unit<BT, RT>(P, bid / U, bid % U, lds);
-  } else if (bid < P.host_workers) {
-    const int n_host_units = P.n_host_pages * U;
-    for (int v = bid; v < n_host_units; v += P.host_workers)
-      gemm_unit<BT, RT>(P, P.host_pages[v / U], v % U, lds);
-  } else {
-    const int u = bid - P.host_workers;
-    gemm_unit<BT, RT>(P, P.hbm_pages[u / U], u % U, lds);
-  }
-}
-
-// ---------------------------------------------------------------------------
-// Matrix-core GEMM with W and x streamed into LDS by direct-to-LDS loads.
-//
-// Same unit as gemm_unit (64 RT rows of one page, one slice of K, wavefront w
-// owns row tiles w RT .. w RT + RT - 1), but K is walked in stages of 64
-// columns through a ring of dma_stages() stages in LDS, and every byte of a
-// stage, W rows and x rows alike, goes from memory straight into LDS
-// (buffer_load ... lds): no register holds data in flight, so all but one
-// stage of the ring stay in flight per workgroup (gemm_unit keeps one chunk
-// in registers).  One such load instruction moves 1 KiB: lane i writes LDS
+// The unit is 64 RT rows of one page and one slice of K.  K is walked in
+// stages of 64 columns through a ring of dma_stages() stages in LDS, and
+// every byte of a stage, W rows and x rows alike, goes from memory straight
+// into LDS (buffer_load ... lds): no register holds data in flight, so all
+// but one stage of the ring stay in flight per workgroup, and x crosses the
+// L2 -> CU path once per workgroup.  Each wavefront reads its A fragments
+// (lane l: row l % 16 of a 16-row tile, columns 8 (l / 16) .. + 8 of a
+// 32-column step) and B fragments (the same mapping over batch rows) from
+// LDS and ends with the full sums of its tiles over the slice, so there is
+// no cross-wavefront reduction; rows cut by a page boundary and split-K
+// slices go through the same partial buffers as the other matrix-core path.
+// One such load instruction moves 1 KiB: lane i writes LDS
 // bytes [16 i, 16 i + 16) of the block at M0, and a lane chooses which global
 // 16 bytes it fetches, so an instruction reads 8 whole 128-byte rows of a
 // stage and lays them out swizzled: row r (0..7) of block b keeps its
@@ -879,6 +660,25 @@ template <int BT, int RT>
 constexpr int dma_stages() {
   return kDmaLds / dma_stage_bytes<BT, RT>() >= BOOST_GEMM_DMA_NS ? BOOST_GEMM_DMA_NS
                                                                   : kDmaLds / dma_stage_bytes<BT, RT>();
+}
+
+// Row groups of the 2-D arrangement of the four wavefronts over a unit's
+// 4 RT row tiles and BT batch tiles: the one that reads the fewest fragments
+// per 32-column step (4 RT / WR + BT / (4 / WR)), ties to more row groups
+#ifndef BOOST_GEMM_DMA_WR
+#define BOOST_GEMM_DMA_WR 0  // 0: by fragment count; 1, 2 or 4: fixed
+#endif
+template <int BT, int RT>
+constexpr int dma_wave_rows() {
+  if (BOOST_GEMM_DMA_WR > 0 && BT % (4 / BOOST_GEMM_DMA_WR) == 0) return BOOST_GEMM_DMA_WR;
+  int best = 4, cost = RT + BT;
+  for (int wr : {2, 1}) {
+    const int wb = 4 / wr;
+    if (BT % wb) continue;
+    const int c = 4 * RT / wr + BT / wb;
+    if (c < cost) best = wr, cost = c;
+  }
+  return best;
 }
 
 // s_waitcnt immediate that waits until at most n vector-memory loads of this
@@ -992,26 +792,32 @@ __device__ __forceinline__ void gemm_dma_unit(const GemvParams& P, int page_in, 
   const int r8 = lrow & 7, hb = lrow >> 3;
   const int fo = hb * kDmaBlk + r8 * 128;
   const int fx0 = ((lgrp ^ r8 ^ hb) << 4), fx1 = fx0 ^ 64;  // position, sub 0 / 1
-  const int wa = 2 * wave * RT * kDmaBlk + fo;
-  const int xa = 8 * RT * kDmaBlk + fo;
+  // products: the four wavefronts form a WR x (4 / WR) grid over the unit's
+  // 4 RT row tiles and BT batch tiles; wavefront w takes row tiles
+  // [RW (w / WB), + RW) and batch tiles [BW (w % WB), + BW)
+  constexpr int WR = dma_wave_rows<BT, RT>(), WB = 4 / WR;
+  constexpr int RW = 4 * RT / WR, BW = BT / WB;
+  const int t_row = RW * (wave / WB), t_bat = BW * (wave % WB);
+  const int wa = 2 * t_row * kDmaBlk + fo;
+  const int xa = (8 * RT + 2 * t_bat) * kDmaBlk + fo;
 
-  f32x4_t acc[RT][BT];
+  f32x4_t acc[RW][BW];
 #pragma unroll
-  for (int a = 0; a < RT; ++a)
+  for (int a = 0; a < RW; ++a)
 #pragma unroll
-    for (int t = 0; t < BT; ++t) acc[a][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int t = 0; t < BW; ++t) acc[a][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  constexpr int TG = BT < 4 ? BT : 4;  // x fragments live at once
+  constexpr int TG = BW < 4 ? BW : 4;  // x fragments live at once
   auto mma = [&](const char* st) {
 #pragma unroll
     for (int sub = 0; sub < 2; ++sub) {  // the stage's two 32-column steps
       const int fx = sub ? fx1 : fx0;
-      uint4 wf[RT];
+      uint4 wf[RW];
 #pragma unroll
-      for (int a = 0; a < RT; ++a)
+      for (int a = 0; a < RW; ++a)
         wf[a] = *reinterpret_cast<const uint4*>(st + wa + a * 2 * kDmaBlk + fx);
 #pragma unroll
-      for (int t0 = 0; t0 < BT; t0 += TG) {
+      for (int t0 = 0; t0 < BW; t0 += TG) {
         uint4 xf[TG];
 #pragma unroll
         for (int u = 0; u < TG; ++u)
@@ -1019,7 +825,7 @@ __device__ __forceinline__ void gemm_dma_unit(const GemvParams& P, int page_in, 
 #pragma unroll
         for (int u = 0; u < TG; ++u)
 #pragma unroll
-          for (int a = 0; a < RT; ++a)
+          for (int a = 0; a < RW; ++a)
             acc[a][t0 + u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
                 as_bf16x8(wf[a]), as_bf16x8(xf[u]), acc[a][t0 + u], 0, 0, 0);
       }
@@ -1042,13 +848,13 @@ __device__ __forceinline__ void gemm_dma_unit(const GemvParams& P, int page_in, 
   __syncthreads();  // LDS is reused by the next unit of a persistent worker
 
 #pragma unroll
-  for (int a = 0; a < RT; ++a)
+  for (int a = 0; a < RW; ++a)
 #pragma unroll
-    for (int t = 0; t < BT; ++t) {
-      const int b = 16 * t + lrow;
+    for (int t = 0; t < BW; ++t) {
+      const int b = 16 * (t_bat + t) + lrow;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const int64_t r = rbase + 16 * (wave * RT + a) + 4 * lgrp + e;
+        const int64_t r = rbase + 16 * (t_row + a) + 4 * lgrp + e;
         if (b >= P.B || r > r_hi) continue;
         const float v = acc[a][t][e];
         const int64_t e0 = r * K;
@@ -1288,7 +1094,7 @@ int launch_mfma_shape(GemvParams& P, int n_pages, bool need_fixup, const boost_c
 //            MFMAs) when that still gives about one workgroup per CU, else
 //            two (the smaller matrices need the extra workgroups more);
 //   BT > 8:  two row tiles (four would need 256 accumulators per lane).
-// The LDS-shared-x GEMM: units of 64 RT rows (RT = 2 where a page holds at
+// The direct-to-LDS GEMM: units of 64 RT rows (RT = 2 where a page holds at
 // least 128 rows, else 1), split-K over workgroups as above.
 template <int BT, int RT>
 int launch_gemm_shape(GemvParams& P, int n_pages, bool need_fixup, const boost_ctx* ctx,
@@ -1319,18 +1125,8 @@ int launch_gemm_shape(GemvParams& P, int n_pages, bool need_fixup, const boost_c
                            : P.host_workers + static_cast<int64_t>(P.n_hbm_pages) *
                                                   P.units_per_page;
   }
-  // direct-to-LDS streaming up to four batch tiles, and beyond that with
-  // 128-row units; with 64-row units and eight or more batch tiles every
-  // wavefront re-reads the large x tile from LDS for only 16 rows, and the
-  // register-streamed kernel, whose W bypasses LDS, is faster (8B and 70B
-  // shapes at batch 32..256: 0-22 % faster where chosen, 8-21 % slower on
-  // the 70B shapes at batch >= 128 with 64-row units)
-  if (BOOST_GEMM_DMA && (BT <= 4 || RT == 2))
-    hipLaunchKernelGGL((gemm_dma_kernel<BT, RT>), dim3(static_cast<unsigned>(grid)),
-                       dim3(kThreads), 0, s, P);
-  else
-    hipLaunchKernelGGL((gemm_kernel<BT, RT>), dim3(static_cast<unsigned>(grid)), dim3(kThreads),
-                       0, s, P);
+  hipLaunchKernelGGL((gemm_dma_kernel<BT, RT>), dim3(static_cast<unsigned>(grid)), dim3(kThreads),
+                     0, s, P);
   BOOST_HIP(hipGetLastError());
   if (S == 1) return launch_fixup(P, n_pages, need_fixup, s);
   const int64_t lanes = static_cast<int64_t>(P.B) * P.N;
@@ -1358,7 +1154,7 @@ int launch_gemm(GemvParams& P, int n_pages, bool need_fixup, const boost_ctx* ct
   return launch_gemm_shape<BT, 1>(P, n_pages, need_fixup, ctx, s);
 }
 
-// Smallest batch-tile count that takes the LDS-shared-x GEMM
+// Smallest batch-tile count that takes the direct-to-LDS GEMM
 #ifndef BOOST_GEMM_MIN_BT
 #define BOOST_GEMM_MIN_BT 2
 #endif
