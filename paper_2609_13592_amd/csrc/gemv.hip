@@ -665,12 +665,8 @@ constexpr int dma_stages() {
 // Row groups of the 2-D arrangement of the four wavefronts over a unit's
 // 4 RT row tiles and BT batch tiles: the one that reads the fewest fragments
 // per 32-column step (4 RT / WR + BT / (4 / WR)), ties to more row groups
-#ifndef BOOST_GEMM_DMA_WR
-#define BOOST_GEMM_DMA_WR 0  // 0: by fragment count; 1, 2 or 4: fixed
-#endif
 template <int BT, int RT>
 constexpr int dma_wave_rows() {
-  if (BOOST_GEMM_DMA_WR > 0 && BT % (4 / BOOST_GEMM_DMA_WR) == 0) return BOOST_GEMM_DMA_WR;
   int best = 4, cost = RT + BT;
   for (int wr : {2, 1}) {
     const int wb = 4 / wr;
@@ -709,17 +705,24 @@ __device__ __forceinline__ void load16_lds(__amdgpu_buffer_rsrc_t r, uint32_t of
 }
 #pragma clang diagnostic pop
 
-template <int BT, int RT>
+// HOST: the unit is one 16-row tile of a unit (sub-unit unit_in % (4 RT) of
+// unit unit_in / (4 RT)), so a page read over the host link, whose loads wait
+// far longer than HBM's, spreads over 4 RT times more workgroups; every
+// output still sums the same columns in the same order, so the results do
+// not depend on which pages are on the host.
+template <int BT, int RT, bool HOST = false>
 __device__ __forceinline__ void gemm_dma_unit(const GemvParams& P, int page_in, int unit_in,
                                               char* ring) {
   static_assert(BT % 2 == 0, "x blocks are spread evenly over the four wavefronts");
   constexpr int kNs = dma_stages<BT, RT>();
   constexpr int kSb = dma_stage_bytes<BT, RT>();
-  constexpr int kXq = BT / 2;            // x blocks loaded per wavefront and stage
-  constexpr int kLoads = 2 * RT + kXq;   // load instructions per wavefront and stage
+  constexpr int kXq = BT / 2;              // x blocks loaded per wavefront and stage
+  constexpr int kWq = HOST ? 1 : 2 * RT;   // W blocks loaded per wavefront and stage
+  constexpr int kLoads = kWq + kXq;        // load instructions per wavefront and stage
   static_assert(kNs >= 2, "ring of at least two stages");
   const int page = __builtin_amdgcn_readfirstlane(page_in);
-  const int unit = __builtin_amdgcn_readfirstlane(unit_in);
+  const int sub = __builtin_amdgcn_readfirstlane(unit_in);
+  const int unit = HOST ? sub / (4 * RT) : sub;
   const int j = unit / P.S, slice = unit % P.S;
   constexpr int R = 64 * RT;
   const int64_t K = P.K;
@@ -728,7 +731,8 @@ __device__ __forceinline__ void gemm_dma_unit(const GemvParams& P, int page_in, 
   const int64_t pe1 = min(pe0 + kPageElems, total);
   const int64_t r_lo = pe0 / K;
   const int64_t r_hi = (pe1 - 1) / K;  // inclusive
-  const int64_t rbase = r_lo + static_cast<int64_t>(j) * R;
+  const int64_t rbase =
+      r_lo + static_cast<int64_t>(j) * R + (HOST ? 16 * (sub % (4 * RT)) : 0);
   if (rbase > r_hi) return;  // uniform over the workgroup
   const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
   const int lane = threadIdx.x & 63;
@@ -748,18 +752,25 @@ __device__ __forceinline__ void gemm_dma_unit(const GemvParams& P, int page_in, 
   // loads: lane i of an instruction for block b fetches row i / 8 of the
   // block and the chunk it stores at position i % 8, i.e. chunk
   // (i % 8) ^ (i / 8) ^ (b & 1); W blocks 2 T + h (tile T, rows 8 h ..),
-  // x blocks 8 RT + 4 q + wave (an even base: parity of wave)
+  // x blocks 8 RT + 4 q + wave (an even base: parity of wave).  A host
+  // sub-unit has one tile: wavefronts 0 and 1 load its blocks 0 and 1, and
+  // 2 and 3 issue an out-of-range load into the unused block 2, so every
+  // wavefront issues the same number of loads per stage.
   const int brow = lane >> 3;
   const int c0 = (lane & 7) ^ brow;  // chunk at parity 0; parity 1: c0 ^ 1
-  uint32_t ro[RT][2];
+  uint32_t ro[kWq];
+  int wblk[kWq], wpar[kWq];
 #pragma unroll
-  for (int a = 0; a < RT; ++a)
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int64_t r = rbase + 16 * (wave * RT + a) + 8 * h + brow;
-      ro[a][h] = r > r_hi ? kOOB
-                          : static_cast<uint32_t>((r * K - pe0) * 2) + 16 * (c0 ^ h);
-    }
+  for (int i = 0; i < kWq; ++i) {
+    const int h = HOST ? (wave & 1) : (i & 1);
+    const int blk = HOST ? min(wave, 2) : 2 * (wave * RT + i / 2) + h;
+    const int64_t r = rbase + 8 * blk + brow;  // block blk holds rows 8 blk ..
+    const bool live = !HOST || wave < 2;
+    ro[i] = (!live || r > r_hi) ? kOOB
+                                : static_cast<uint32_t>((r * K - pe0) * 2) + 16 * (c0 ^ h);
+    wblk[i] = blk;
+    wpar[i] = h;
+  }
   const int cx = c0 ^ (wave & 1);
   uint32_t xo[kXq];
 #pragma unroll
@@ -776,11 +787,8 @@ __device__ __forceinline__ void gemm_dma_unit(const GemvParams& P, int page_in, 
     const uint32_t kb2 = static_cast<uint32_t>((k_beg + kb) * 2);
     const char* st = ring + slot * kSb;
 #pragma unroll
-    for (int a = 0; a < RT; ++a)
-#pragma unroll
-      for (int h = 0; h < 2; ++h)
-        load16_lds(wr, (ro[a][h] + kb2) | (h ? oob1 : oob0),
-                   st + (2 * (wave * RT + a) + h) * kDmaBlk);
+    for (int i = 0; i < kWq; ++i)
+      load16_lds(wr, (ro[i] + kb2) | (wpar[i] ? oob1 : oob0), st + wblk[i] * kDmaBlk);
 #pragma unroll
     for (int q = 0; q < kXq; ++q)
       load16_lds(xr, (xo[q] + kb2) | oobx, st + (8 * RT + wave + 4 * q) * kDmaBlk);
@@ -795,9 +803,13 @@ __device__ __forceinline__ void gemm_dma_unit(const GemvParams& P, int page_in, 
   // products: the four wavefronts form a WR x (4 / WR) grid over the unit's
   // 4 RT row tiles and BT batch tiles; wavefront w takes row tiles
   // [RW (w / WB), + RW) and batch tiles [BW (w % WB), + BW)
-  constexpr int WR = dma_wave_rows<BT, RT>(), WB = 4 / WR;
-  constexpr int RW = 4 * RT / WR, BW = BT / WB;
+  // (a host sub-unit: one row tile, the batch tiles over min(4, BT)
+  // wavefronts; with BT = 2 wavefronts 2 and 3 only load)
+  constexpr int WR = HOST ? 1 : dma_wave_rows<BT, RT>();
+  constexpr int WB = HOST ? (BT < 4 ? BT : 4) : 4 / WR;
+  constexpr int RW = (HOST ? 1 : 4 * RT) / WR, BW = BT / WB;
   const int t_row = RW * (wave / WB), t_bat = BW * (wave % WB);
+  const bool computes = !HOST || wave < WB;  // uniform over the wavefront
   const int wa = 2 * t_row * kDmaBlk + fo;
   const int xa = (8 * RT + 2 * t_bat) * kDmaBlk + fo;
 
@@ -840,13 +852,14 @@ __device__ __forceinline__ void gemm_dma_unit(const GemvParams& P, int page_in, 
     __builtin_amdgcn_s_waitcnt(vmcnt_imm<(kNs - 2) * kLoads>());  // stage s landed
     __syncthreads();  // ... for every wavefront; slot `fill` is no longer read
     issue(s + kNs - 1, fill);
-    mma(ring + slot * kSb);
+    if (computes) mma(ring + slot * kSb);
     slot = slot + 1 == kNs ? 0 : slot + 1;
     fill = fill + 1 == kNs ? 0 : fill + 1;
   }
   __builtin_amdgcn_s_waitcnt(vmcnt_imm<0>());  // the loads issued past the slice
   __syncthreads();  // LDS is reused by the next unit of a persistent worker
 
+  if (!computes) return;
 #pragma unroll
   for (int a = 0; a < RW; ++a)
 #pragma unroll
@@ -886,9 +899,10 @@ __global__ __launch_bounds__(kThreads) void gemm_dma_kernel(GemvParams P) {
   if (P.address_order) {
     gemm_dma_unit<BT, RT>(P, bid / U, bid % U, ring);
   } else if (bid < P.host_workers) {
-    const int n_host_units = P.n_host_pages * U;
-    for (int v = bid; v < n_host_units; v += P.host_workers)
-      gemm_dma_unit<BT, RT>(P, P.host_pages[v / U], v % U, ring);
+    const int Uh = U * 4 * RT;  // 16-row sub-units per host page
+    const int n_host_sub = P.n_host_pages * Uh;
+    for (int v = bid; v < n_host_sub; v += P.host_workers)
+      gemm_dma_unit<BT, RT, true>(P, P.host_pages[v / Uh], v % Uh, ring);
   } else {
     const int u = bid - P.host_workers;
     gemm_dma_unit<BT, RT>(P, P.hbm_pages[u / U], u % U, ring);
@@ -983,6 +997,21 @@ inline int k_splits(int K) {
 #ifndef BOOST_HOST_UNITS_PER_WORKER
 #define BOOST_HOST_UNITS_PER_WORKER 16
 #endif
+// Host workers for host_units units on host pages: by default n_cu / 16.
+// The matrix-core kernels, whose workgroups keep fewer bytes in flight, take
+// one per BOOST_HOST_UNITS_PER_WORKER host units, up to n_cu / 8 (70B step at
+// batch 8: 427.6 -> 419.2 ms).  The GEMV's workgroups already keep the link
+// busy; more of them slowed the HBM units beside them (2 GiB tensor, 8 host
+// pages: 360 -> 432 us).  Never more workers than host units.
+int host_worker_count(const boost_ctx* ctx, int64_t host_units, bool matrix_core) {
+  const int64_t h_lo = std::max(1, ctx->n_cu / 16);
+  const int64_t h_hi = matrix_core ? std::max(1, ctx->n_cu / 8) : h_lo;
+  const int64_t h_want = (host_units + BOOST_HOST_UNITS_PER_WORKER - 1) / BOOST_HOST_UNITS_PER_WORKER;
+  const int64_t h = ctx->gemv_host_workers > 0 ? ctx->gemv_host_workers
+                                               : std::min(h_hi, std::max(h_lo, h_want));
+  return static_cast<int>(std::min(h, host_units));
+}
+
 // Units per page and grid size for units of rows_wg rows; fills in
 // P.units_per_page, P.host_workers and P.address_order.  Returns -1 if the
 // grid is too large.
@@ -1004,18 +1033,7 @@ int64_t plan_grid(GemvParams& P, int n_pages, int rows_wg, const boost_ctx* ctx,
     grid = static_cast<int64_t>(n_pages) * P.units_per_page;
   } else {
     const int64_t host_units = static_cast<int64_t>(P.n_host_pages) * P.units_per_page;
-    // default: n_cu / 16 host workers.  The matrix-core kernels, whose
-    // workgroups keep fewer bytes in flight, take one per
-    // BOOST_HOST_UNITS_PER_WORKER host units, up to n_cu / 8 (70B step at
-    // batch 8: 427.6 -> 419.2 ms).  The GEMV's workgroups already keep the
-    // link busy; more of them slowed the HBM units beside them (2 GiB tensor,
-    // 8 host pages: 360 -> 432 us).
-    const int64_t h_lo = std::max(1, ctx->n_cu / 16);
-    const int64_t h_hi = matrix_core ? std::max(1, ctx->n_cu / 8) : h_lo;
-    const int64_t h_want = (host_units + BOOST_HOST_UNITS_PER_WORKER - 1) / BOOST_HOST_UNITS_PER_WORKER;
-    int h = ctx->gemv_host_workers > 0 ? ctx->gemv_host_workers
-                                       : static_cast<int>(std::min(h_hi, std::max(h_lo, h_want)));
-    P.host_workers = static_cast<int>(std::min<int64_t>(h, host_units));
+    P.host_workers = host_worker_count(ctx, host_units, matrix_core);
     grid = P.host_workers + static_cast<int64_t>(P.n_hbm_pages) * P.units_per_page;
   }
   return grid > 0x7fffffff ? -1 : grid;
@@ -1121,10 +1139,16 @@ int launch_gemm_shape(GemvParams& P, int n_pages, bool need_fixup, const boost_c
     P.S = S;
     P.ws = ctx->gemm_ws;
     P.units_per_page *= S;
-    grid = P.address_order ? static_cast<int64_t>(n_pages) * P.units_per_page
-                           : P.host_workers + static_cast<int64_t>(P.n_hbm_pages) *
-                                                  P.units_per_page;
   }
+  if (P.address_order) {
+    grid = static_cast<int64_t>(n_pages) * P.units_per_page;
+  } else {
+    // host pages run as 16-row sub-units (4 RT per unit)
+    const int64_t host_sub = static_cast<int64_t>(P.n_host_pages) * P.units_per_page * 4 * RT;
+    P.host_workers = host_worker_count(ctx, host_sub, true);
+    grid = P.host_workers + static_cast<int64_t>(P.n_hbm_pages) * P.units_per_page;
+  }
+  if (grid > 0x7fffffff) return bst::fail(BOOST_EINVAL, "grid too large");
   hipLaunchKernelGGL((gemm_dma_kernel<BT, RT>), dim3(static_cast<unsigned>(grid)), dim3(kThreads),
                      0, s, P);
   BOOST_HIP(hipGetLastError());
