@@ -215,7 +215,9 @@ int boost_prefetch(boost_ctx *ctx, const boost_tensor *view, void *stream);
  *     other workgroups stream HBM-page units, so host and HBM reads overlap in
  *     every wave (§3 "CAP").  host_workers = 0 picks the default: n_cu / 16
  *     for the GEMV (B <= 6); for the matrix-core kernels one worker per 16
- *     host units of the tensor, at least n_cu / 16 and at most n_cu / 8. */
+ *     host units of the tensor, at least n_cu / 16 and at most n_cu / 8
+ *     (from B = 17 a host unit is one 16-row tile of a work unit, so a host
+ *     page spreads over more workers).  Never more workers than host units. */
 #define BOOST_SCHED_ADDRESS 0
 #define BOOST_SCHED_CAP 1
 int boost_gemv_set_schedule(boost_ctx *ctx, int schedule, int host_workers);
