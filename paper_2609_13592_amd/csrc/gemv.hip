@@ -721,8 +721,8 @@ __device__ __forceinline__ void gemm_dma_unit(const GemvParams& P, int page_in, 
   constexpr int kLoads = kWq + kXq;        // load instructions per wavefront and stage
   static_assert(kNs >= 2, "ring of at least two stages");
   const int page = __builtin_amdgcn_readfirstlane(page_in);
-  const int sub = __builtin_amdgcn_readfirstlane(unit_in);
-  const int unit = HOST ? sub / (4 * RT) : sub;
+  const int uin = __builtin_amdgcn_readfirstlane(unit_in);
+  const int unit = HOST ? uin / (4 * RT) : uin;
   const int j = unit / P.S, slice = unit % P.S;
   constexpr int R = 64 * RT;
   const int64_t K = P.K;
@@ -732,7 +732,7 @@ __device__ __forceinline__ void gemm_dma_unit(const GemvParams& P, int page_in, 
   const int64_t r_lo = pe0 / K;
   const int64_t r_hi = (pe1 - 1) / K;  // inclusive
   const int64_t rbase =
-      r_lo + static_cast<int64_t>(j) * R + (HOST ? 16 * (sub % (4 * RT)) : 0);
+      r_lo + static_cast<int64_t>(j) * R + (HOST ? 16 * (uin % (4 * RT)) : 0);
   if (rbase > r_hi) return;  // uniform over the workgroup
   const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
   const int lane = threadIdx.x & 63;
