@@ -116,10 +116,12 @@ def test_placement_invariance_and_parity(gpu_ctx, N, K, B):
 def test_mfma_placement_invariance_and_parity(gpu_ctx, N, K, B):
     """Batches from 7 up run on the matrix cores: bitwise-equal y under every
     map and schedule, every result within the bar of the oracle (ragged
-    batch tiles, rows cut by page boundaries, pages of both tiers).  Both
-    GEMM kernels appear: direct-to-LDS streaming (B = 20, 33, 64, and
-    128-row units at B = 128 and 256 with K = 14336) and register streaming
-    (64-row units at B = 100, 128, 200)."""
+    batch tiles, rows cut by page boundaries, pages of both tiers).  From
+    B = 17 the GEMM covers 2, 4, 8 and 16 batch tiles with 64-row units
+    (B = 20, 33, 64, 100, 128, 200) and 128-row units (K = 14336 at B = 128
+    and 256), each with its own wavefront grid, and the host pages of the
+    "host", "alt" and "mpp3" maps run as 16-row sub-units: the bitwise
+    comparison across maps checks that they sum in the same order."""
     w, x = synth.gemv_inputs(17 + N + K + B, N, K, B)
     n = opl.n_pages(w.nbytes)
     maps = {"hbm": np.zeros(n, np.uint8), "host": np.ones(n, np.uint8),
