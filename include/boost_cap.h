@@ -354,8 +354,11 @@ int boost_kv_write(boost_ctx *ctx, const boost_kv_pool *pool, int layer,
  * of the heads that can hold host pages are dispatched first.
  * q: device bf16 [B, Hq, D]; block_tables: device int32 [B, max_blocks];
  * ctx_lens: device int32 [B]; out: device [B, Hq, D] fp32 or bf16.
- * scale <= 0 selects 1/sqrt(D).  A block id outside the pool contributes
- * nothing; ctx_lens[b] = 0 gives a zero row.  1 <= B <= max_batch,
+ * scale <= 0 selects 1/sqrt(D).  A block id outside [0, nb_pool) at a
+ * position inside the context is skipped: its 16 tokens are left out of the
+ * softmax (no read, no weight), as if they were not in the context; a row
+ * whose every token is skipped, or ctx_lens[b] = 0, gives a zero row.
+ * 1 <= B <= max_batch,
  * Hq == q_heads of the pool, max_blocks <= max_blocks_per_seq.
  * Errors: EINVAL, ENODEV, EHIP. */
 int boost_paged_attn_decode(boost_ctx *ctx, const boost_kv_pool *pool, int layer,

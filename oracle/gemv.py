@@ -49,7 +49,15 @@ def gemv_f32(w_u16: np.ndarray, x_u16: np.ndarray) -> np.ndarray:
 
 
 def gemv_rows_f64(w_rows_u16: np.ndarray, row_ids, x_u16: np.ndarray):
-    """Sampled outputs: y[:, row_ids] from the given rows of W only."""
+    """Sampled outputs y[:, row_ids] (fp64), from the rows W[row_ids] only.
+
+    ``w_rows_u16[i]`` must be row ``row_ids[i]`` of W, in the same order, so
+    that a tensor too large to bring to the host is checked on the rows that
+    matter (every row cut by a page boundary, plus random ones).  Column i of
+    the result is output row ``row_ids[i]``."""
+    w_rows_u16 = np.asarray(w_rows_u16)
+    if w_rows_u16.ndim != 2 or w_rows_u16.shape[0] != len(row_ids):
+        raise ValueError("one row of W per row id")
     w = bf16_to_f32(w_rows_u16).astype(np.float64)
     x = bf16_to_f32(x_u16).astype(np.float64)
     return x @ w.T

@@ -258,6 +258,8 @@ __global__ __launch_bounds__(kThreads) void attn_partition(AttnParams P) {
 
   const uint32_t lane_off = static_cast<uint32_t>(tid) * 16;
   // address of head-block (g, blk) of K and V: uniform scalar arithmetic
+  // (a block id outside the pool reads nothing and its tokens are masked
+  // out of the softmax, as if the block were not in the context)
   auto fetch = [&](int bi, uint4& kq, uint4& vq) {
     const int32_t blk = row[bi];
     const bool ok = blk >= 0 && blk < P.nb;
@@ -266,21 +268,27 @@ __global__ __launch_bounds__(kThreads) void attn_partition(AttnParams P) {
     const uint64_t off = host ? byte - P.host_from : byte;
     kq = load_block((host ? P.k_host : P.k_hbm) + off, ok, lane_off);
     vq = load_block((host ? P.v_host : P.v_hbm) + off, ok, lane_off);
+    return ok;
   };
-  bool valid[kUnroll];
-#pragma unroll
-  for (int u = 0; u < kUnroll; ++u) valid[u] = true;
   int i = 0;
   for (; i + kUnroll <= nfull; i += kUnroll) {
     uint4 kb[kUnroll], vb[kUnroll];
+    bool valid[kUnroll];
+    bool all_ok = true;  // uniform: block ids are the same for every lane
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) fetch(i + u, kb[u], vb[u]);
-    consume<G, kUnroll, false>(qp, kb, vb, valid, sc2, m, l, acc);
+    for (int u = 0; u < kUnroll; ++u) {
+      valid[u] = fetch(i + u, kb[u], vb[u]);
+      all_ok = all_ok && valid[u];
+    }
+    if (all_ok)
+      consume<G, kUnroll, false>(qp, kb, vb, valid, sc2, m, l, acc);
+    else
+      consume<G, kUnroll, true>(qp, kb, vb, valid, sc2, m, l, acc);
   }
   for (; i < nbp; ++i) {  // remaining blocks, the last one possibly partial
     uint4 kb[1], vb[1];
-    fetch(i, kb[0], vb[0]);
-    const bool v1[1] = {(blk_beg + i) * kT + ts < L};
+    const bool ok = fetch(i, kb[0], vb[0]);
+    const bool v1[1] = {ok && (blk_beg + i) * kT + ts < L};
     consume<G, 1, true>(qp, kb, vb, v1, sc2, m, l, acc);
   }
 

@@ -4,6 +4,7 @@
 // one HBM slab; the device page table maps (layer, K/V, page) to an address.
 #include <algorithm>
 #include <cstring>
+#include <new>
 
 #include "runtime.h"
 
@@ -66,19 +67,28 @@ int boost_kv_pool_create(boost_ctx* ctx, const boost_kv_cfg* cfg, boost_kv_pool*
   if (cfg->block_tokens != 16) return fail(BOOST_EINVAL, "block_tokens must be 16");
   if (cfg->head_dim != 64 && cfg->head_dim != 128)
     return fail(BOOST_EINVAL, "head_dim must be 64 or 128");
+  if (cfg->kv_heads == 0) return fail(BOOST_EINVAL, "0 kv_heads");
   if (cfg->q_heads == 0 || cfg->q_heads % cfg->kv_heads || cfg->q_heads / cfg->kv_heads > 16)
     return fail(BOOST_EINVAL, "q_heads %u must be a multiple of kv_heads %u (ratio <= 16)",
                 cfg->q_heads, cfg->kv_heads);
-  auto* p = new boost_kv_pool();
-  p->ctx = ctx;
-  p->cfg = *cfg;
-  int rc = kv_geometry(cfg->n_blocks, cfg->kv_heads, cfg->head_dim, cfg->block_tokens,
-                       cfg->M, cfg->tier_mode, cfg->layers, cfg->hbm_budget_bytes, p->geom);
-  if (rc) {
+  boost_kv_pool* p = nullptr;
+  try {  // host-side allocator state: per-block host heads and the two free lists
+    if (fault_host_alloc()) throw std::bad_alloc();
+    p = new boost_kv_pool();
+    p->ctx = ctx;
+    p->cfg = *cfg;
+    int rc = kv_geometry(cfg->n_blocks, cfg->kv_heads, cfg->head_dim, cfg->block_tokens,
+                         cfg->M, cfg->tier_mode, cfg->layers, cfg->hbm_budget_bytes, p->geom);
+    if (rc) {
+      delete p;
+      return rc;
+    }
+    p->dsr.init(p->geom);
+  } catch (const std::bad_alloc&) {
     delete p;
-    return rc;
+    return fail(BOOST_ENOMEM, "KV pool: host memory for the allocator state");
   }
-  p->dsr.init(p->geom);
+  int rc = BOOST_OK;
   if (ctx->device < 0) {  // plan-only: allocator bookkeeping only
     *out = p;
     return BOOST_OK;

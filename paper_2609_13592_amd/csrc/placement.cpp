@@ -5,6 +5,7 @@
 // placements for the comparisons of §2.6 and §5.7: modulo placement without
 // the per-tensor restart, a linear split, and random (BAPP-R) placement.
 #include <cmath>
+#include <cstdlib>
 #include <cstring>
 #include <numeric>
 #include <unordered_map>
@@ -28,6 +29,11 @@ int fail(int code, const char* fmt, ...) {
 void clear_error() { g_err.clear(); }
 
 uint64_t pages_of(uint64_t bytes) { return (bytes + kPage - 1) / kPage; }
+
+bool fault_host_alloc() {
+  const char* e = std::getenv("BOOST_FAULT_HOST_ALLOC");
+  return e && std::strtol(e, nullptr, 10) != 0;
+}
 
 static uint64_t superpage(uint64_t footprint) {
   if (footprint == 0) return 1;

@@ -17,6 +17,9 @@ int slab_alloc(boost_ctx* ctx, uint64_t pages, bool host, Slab& s) {
   if (pages == 0) return BOOST_OK;
   const size_t bytes = pages * kPage + kPage;  // room to align to 2 MiB
   if (host) {
+    if (fault_host_alloc())
+      return fail(BOOST_ENOMEM, "host allocation of %llu pages refused (BOOST_FAULT_HOST_ALLOC)",
+                  (unsigned long long)pages);
     unsigned flags = hipHostMallocMapped |
                      (ctx->host_coherent ? hipHostMallocCoherent
                                          : hipHostMallocNonCoherent);

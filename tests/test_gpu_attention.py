@@ -224,3 +224,41 @@ def test_batch256_long_contexts_full_size_sampled(gpu_ctx):
     got, exp = np.array(got), np.array(exp)
     assert og.rel_err(got, exp) <= TOL
     assert np.max(np.abs(got - exp)) < 1e-4
+
+
+def test_block_ids_outside_pool_are_skipped(gpu_ctx):
+    """Block-table entries outside [0, nb_pool) at positions inside the
+    context leave their 16 tokens out of the softmax: the output equals the
+    oracle's attention over the remaining tokens (checked on the CPU), for
+    entries in the unmasked main loop (the first blocks), in the partial
+    last block, for a whole group of blocks, and for a request whose every
+    block is invalid (zero row).  Under LPP and all-HBM pools alike."""
+    H, Hq = 8, 32
+    lengths = np.array([100, 300, 700, 40, 2049])
+    _, q, ks, vs = synth.attention_inputs(len(lengths), Hq, H, 128, 0, 0, seed=14,
+                                          kv_seed=15, lengths=lengths)
+    bad = {0: [0, 6], 1: [5, 18], 2: [1, 2, 3, 4, 43], 3: [0, 1, 2], 4: [7, 64, 128]}
+    keep_k, keep_v = [], []
+    for b, L in enumerate(lengths):
+        tok = np.arange(int(L))
+        keep = ~np.isin(tok // 16, bad[b])
+        keep_k.append(ks[b][keep])
+        keep_v.append(vs[b][keep])
+    ref = oa.decode_attention(q, keep_k, keep_v)
+    outs = []
+    for mode, M in ((bd.KV_LPP, 3), (bd.KV_ALL_HBM, 0)):
+        pool = new_pool(gpu_ctx, H, Hq, 2000, M, mode, max_blocks=160)
+        try:
+            tables = fill_pool(bd, gpu_ctx, pool, 0, lengths, ks, vs)
+            nb = bd.boost_kv_pool_info(pool)["nb_pool"]
+            for b, blks in bad.items():
+                for j, blk in enumerate(blks):
+                    tables[b, blk] = -1 if j % 2 == 0 else nb + 5 * j
+            o = run_attn(gpu_ctx, pool, 0, q, tables, lengths)
+            assert np.all(o[3] == 0)             # every block skipped
+            assert og.rel_err(o, ref) <= TOL
+            assert np.max(np.abs(o - ref)) < 1e-4
+            outs.append(o)
+        finally:
+            bd.boost_kv_pool_destroy(pool)
+    assert np.array_equal(outs[0].view(np.uint32), outs[1].view(np.uint32))

@@ -277,3 +277,42 @@ def test_prefetch_staged_view(gpu_ctx):
     finally:
         bd.boost_tensor_free(v)
         bd.boost_tensor_free(t)
+
+
+@pytest.mark.parametrize("kind", [0, 1, 2, 3, 9])
+def test_full_size_70b_tensor_sampled_batch8(gpu_ctx, kind):
+    """Full-size Llama-3-70B-shaped tensors (fused qkv 10240 x 8192, o
+    8192 x 8192, fused gate_up 57344 x 8192, down 8192 x 28672, lm_head
+    128256 x 8192: 80 to 1002 pages) placed by MPP at M = 6, the modulus of
+    the 120e9-byte HBM weight budget, at batch 8: the matrix-core kernel with
+    weights staged through LDS, one K slice, many host units per CAP worker,
+    and (down) rows cut by page boundaries through split_fixup.  Sampled rows,
+    including every row a page boundary cuts, element by element against the
+    oracle at the stated bar and within the fp32 summation bound."""
+    import torch
+    per_layer, head = synth.chain_shapes(synth.LLAMA70B)
+    shapes = {k: (n, kk) for _, k, n, kk in per_layer}
+    shapes[9] = head[2:]
+    N, K = shapes[kind]
+    B = 8
+    wt = synth.chain_weight_torch(5, kind, N, K, "cuda")
+    w_dev = wt.view(torch.int16)
+    rng = np.random.default_rng(70 + kind)
+    x = synth.normal_bf16(rng, (B, K), 1.0)
+    t = bd.boost_place_weights(gpu_ctx, w_dev, N * K * 2, 6)
+    try:
+        tiers = bd.boost_tensor_tiers(t)
+        assert np.array_equal(tiers, opl.mpp_tier_map(N * K * 2, 6))
+        assert tiers.sum() == len(tiers) // 6
+        y = run_gemv(gpu_ctx, t, N, K, to_dev_u16(x), B)
+        cut = np.arange(0, N * K, opl.PAGE // 2) // K        # row at each page start
+        rows = np.unique(np.concatenate([rng.integers(0, N, 300), [0, N - 1], cut]))
+        w_rows = w_dev[torch.from_numpy(rows).cuda()].cpu().numpy().view(np.uint16)
+        ref = og.gemv_rows_f64(w_rows, rows, x)
+        assert og.rel_err(y[:, rows], ref) <= TOL
+        assert_f32_bound(y, w_rows, x, rows)
+        assert np.all(np.isfinite(y))
+    finally:
+        bd.boost_tensor_free(t)
+        del wt, w_dev
+        torch.cuda.empty_cache()

@@ -90,6 +90,13 @@ def test_bad_configs(plan_ctx):
         make(plan_ctx, 100, 8, 96, 4)                  # head_dim
     with pytest.raises(bd.BoostError):
         bd.boost_kv_pool_create(plan_ctx, 1, 8, 128, 100, 4, q_heads=12)  # Hq % H
+    # zero KV heads, with and without query heads; zero blocks or layers
+    for args, kw in (((1, 0, 128, 100, 4), dict(q_heads=32)), ((1, 0, 128, 100, 4), {}),
+                     ((1, 8, 128, 0, 4), {}), ((0, 8, 128, 100, 4), {}),
+                     ((1, 8, 128, 100, 4), dict(block_tokens=0))):
+        with pytest.raises(bd.BoostError) as e:
+            bd.boost_kv_pool_create(plan_ctx, *args, **kw)
+        assert e.value.code == bd.EINVAL, (args, kw)
     pool = make(plan_ctx, 100, 8, 128, 4)
     with pytest.raises(bd.BoostError):
         bd.boost_kv_block_host_heads(pool, 10 ** 6)

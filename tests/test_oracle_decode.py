@@ -166,3 +166,94 @@ def test_mlp_only_layer_closed_form():
     exp = ods.f64(ods.to_bf16(ods.rmsnorm(x, w["norm_f"]))) @ ods.f64(w["lm_head"]).T
     logits, _, _ = ods.decode_step(w, tokens, kc, vc, lengths, DIMS)
     assert np.allclose(logits, exp, rtol=1e-12, atol=1e-12)
+
+
+SMALL = dict(layers=1, d=8, hq=2, hkv=1, hd=4, ffn=8, vocab=10)
+
+
+def small_model(seed, qkv=None):
+    rng = np.random.default_rng(seed)
+    d, Hq, H, D, F, V = (SMALL[k] for k in ("d", "hq", "hkv", "hd", "ffn", "vocab"))
+    w = {"embed": synth.normal_bf16(rng, (V, d), 1.0),
+         "norm_f": bf(1 + 0.1 * rng.standard_normal(d)),
+         "lm_head": synth.normal_bf16(rng, (V, d), 0.3),
+         "norm1.0": bf(1 + 0.1 * rng.standard_normal(d)),
+         "norm2.0": bf(1 + 0.1 * rng.standard_normal(d)),
+         "qkv.0": synth.normal_bf16(rng, ((Hq + 2 * H) * D, d), 0.5),
+         "o.0": synth.normal_bf16(rng, (d, Hq * D), 0.3),
+         "gate_up.0": synth.normal_bf16(rng, (2 * F, d), 0.3),
+         "down.0": synth.normal_bf16(rng, (d, F), 0.3)}
+    if qkv is not None:
+        w["qkv.0"] = qkv
+    return w
+
+
+def rot4(x, pos, theta=ods.THETA):
+    """Half-split rotation of one D = 4 head written out: element 0 pairs
+    with 2 at angle pos, element 1 with 3 at angle pos * theta^(-1/2)."""
+    a0, a1 = pos, pos / math.sqrt(theta)
+    c0, s0, c1, s1 = math.cos(a0), math.sin(a0), math.cos(a1), math.sin(a1)
+    return np.array([x[0] * c0 - x[2] * s0, x[1] * c1 - x[3] * s1,
+                     x[0] * s0 + x[2] * c0, x[1] * s1 + x[3] * c1])
+
+
+def test_rope_position_is_context_length_minus_one():
+    """Context of two tokens (one cached, one new): the new token sits at
+    position 1.  Its query and key are the qkv rows rotated by exactly that
+    position, and the attention output worked from them by hand matches;
+    rotating by position 2 (or 0) would give other queries and another
+    output."""
+    w = small_model(11)
+    kc = [[synth.normal_bf16(np.random.default_rng(12), (1, 1, 4), 1.0)]]
+    vc = [[synth.normal_bf16(np.random.default_rng(13), (1, 1, 4), 1.0)]]
+    tr = {}
+    ods.decode_step(w, np.array([3]), kc, vc, [2], SMALL, trace=tr)
+    raw = ods.f64(tr["h"]) @ ods.f64(w["qkv.0"]).T                  # [1, 16]
+    q_raw = raw[0, :8].reshape(2, 4)
+    k_raw = raw[0, 8:12]
+    v_raw = raw[0, 12:16]
+    exp_q = np.stack([rot4(q_raw[h], 1.0) for h in range(2)])
+    assert np.array_equal(tr["q"][0], ods.to_bf16(exp_q))
+    assert np.array_equal(tr["k"][0, 0], ods.to_bf16(rot4(k_raw, 1.0)))
+    assert np.array_equal(tr["v"][0, 0], ods.to_bf16(v_raw))
+    for wrong in (0.0, 2.0):
+        bad = np.stack([rot4(q_raw[h], wrong) for h in range(2)])
+        assert not np.array_equal(tr["q"][0], ods.to_bf16(bad))
+    # the attention output of each query head over (cached, new), by hand
+    k0, v0 = ods.f64(kc[0][0][0, 0]), ods.f64(vc[0][0][0, 0])
+    k1, v1 = ods.f64(tr["k"][0, 0]), ods.f64(tr["v"][0, 0])
+
+    def attend(q):
+        s0, s1 = float(q @ k0) / 2.0, float(q @ k1) / 2.0      # 1/sqrt(D), D = 4
+        e0, e1 = math.exp(s0 - max(s0, s1)), math.exp(s1 - max(s0, s1))
+        return (e0 * v0 + e1 * v1) / (e0 + e1)
+
+    got = ods.f64(tr["o"][0])
+    for h in range(2):
+        ref = attend(ods.f64(tr["q"][0, h]))
+        assert np.all(np.abs(got[h] - ref) <= 2.0 ** -8 * np.abs(ref) + 1e-30)
+    # the same by hand with the query rotated to position 2 instead: far off
+    q2 = ods.f64(ods.to_bf16(rot4(q_raw[0], 2.0)))
+    assert np.max(np.abs(attend(q2) - got[0])) > 1e-2
+
+
+def test_qkv_split_query_key_value_rows():
+    """Fused qkv rows are Hq*D query rows, then H*D key rows, then H*D value
+    rows, each head-major.  Row r of the weight is (r + 1) * e_0, so output
+    r is (r + 1) * h[0]: query head 0 gets 1..4, head 1 5..8, the key 9..12
+    and the value 13..16 (times h[0]).  At position 0 RoPE is the identity
+    and one token's attention returns its value."""
+    qkv = np.zeros((16, 8), np.float32)
+    qkv[:, 0] = np.arange(1, 17)
+    w = small_model(21, qkv=bf(qkv))
+    tr = {}
+    _, _, app = ods.decode_step(w, np.array([5]), [[np.zeros((0, 1, 4), np.uint16)]],
+                                [[np.zeros((0, 1, 4), np.uint16)]], [1], SMALL, trace=tr)
+    h0 = float(ods.f64(tr["h"])[0, 0])
+    assert h0 != 0.0
+    ramp = np.arange(1, 17, dtype=np.float64) * h0
+    assert np.array_equal(tr["q"][0], ods.to_bf16(ramp[:8].reshape(2, 4)))
+    assert np.array_equal(tr["k"][0, 0], ods.to_bf16(ramp[8:12]))
+    assert np.array_equal(tr["v"][0, 0], ods.to_bf16(ramp[12:16]))
+    assert np.array_equal(app[0][0], tr["k"]) and np.array_equal(app[0][1], tr["v"])
+    assert np.array_equal(tr["o"][0], np.stack([tr["v"][0, 0]] * 2))

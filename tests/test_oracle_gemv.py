@@ -102,3 +102,41 @@ def test_rel_err_measure():
     y = r.copy()
     y[1] = -2.04
     assert abs(og.rel_err(y, r) - 0.02) < 1e-12
+
+
+def test_rows_hand_worked_shuffled():
+    """Sampled rows in shuffled order: column i is output row row_ids[i].
+    W [5 x 4] and x [2 x 4] are small integers (exact in bf16); the outputs
+    are worked by hand:
+      row 4 = [1, 0, -2, 3]:  x0 = [1, 2, 3, 4] -> 1 - 6 + 12 = 7
+                              x1 = [-1, 0, 2, 1] -> -1 - 4 + 3 = -2
+      row 0 = [2, -1, 0, 1]:  x0 -> 2 - 2 + 4 = 4;   x1 -> -2 + 1 = -1
+      row 2 = [0, 3, 1, -1]:  x0 -> 6 + 3 - 4 = 5;   x1 -> 2 - 1 = 1"""
+    W = bf(np.array([[2, -1, 0, 1], [5, 5, 5, 5], [0, 3, 1, -1], [9, 9, 9, 9],
+                     [1, 0, -2, 3]]))
+    x = bf(np.array([[1, 2, 3, 4], [-1, 0, 2, 1]]))
+    rows = np.array([4, 0, 2])
+    y = og.gemv_rows_f64(W[rows], rows, x)
+    assert y.tolist() == [[7.0, 4.0, 5.0], [-2.0, -1.0, 1.0]]
+    # the same columns of the full product
+    assert og.gemv_f64(W, x)[:, rows].tolist() == y.tolist()
+    with pytest.raises(ValueError):
+        og.gemv_rows_f64(W[rows], rows[:2], x)
+
+
+def test_rows_equal_brute_force_columns():
+    """Random rows (shuffled, repeated) against a plain double loop over the
+    full W: a row shift, a transposed W or a dropped batch row fails."""
+    rng = np.random.default_rng(9)
+    n, k, B = 37, 72, 3
+    w = synth.normal_bf16(rng, (n, k), 0.02)
+    x = synth.normal_bf16(rng, (B, k), 1.0)
+    rows = rng.permutation(n)[:11]
+    rows = np.concatenate([rows, rows[:2]])
+    y = og.gemv_rows_f64(w[rows], rows, x)
+    wf = og.bf16_to_f32(w).astype(np.float64)
+    xf = og.bf16_to_f32(x).astype(np.float64)
+    for b in range(B):
+        for i, r in enumerate(rows):
+            ref = sum(wf[r, c] * xf[b, c] for c in range(k))
+            assert abs(y[b, i] - ref) <= 1e-12 * max(1.0, abs(ref))
