@@ -13,7 +13,8 @@ import os
 import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-# BOOST_LIB may name another build of the same library (e.g. a tuning variant)
+# BOOST_LIB may name another build of the same library: the host-sanitizer
+# build used by the CPU tests (python -m paper_2609_13592_amd.build --sanitize)
 _LIB_PATH = os.environ.get("BOOST_LIB") or os.path.join(HERE, "_lib", "libboostcap.so")
 
 OK, EINVAL, ENOMEM, EAGAIN, ENODEV, EHIP = 0, -22, -12, -11, -19, -5

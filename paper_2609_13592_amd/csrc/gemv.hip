@@ -23,7 +23,6 @@
 // chunk is loaded once per column step and reused for the RW rows.  Partial
 // sums are reduced across the 64 lanes by a fixed xor butterfly.
 #include <algorithm>
-#include <cstdlib>
 
 #include "runtime.h"
 
@@ -1129,9 +1128,6 @@ int launch_gemm_shape(GemvParams& P, int n_pages, bool need_fixup, const boost_c
   while (S < kMaxSlices && P.K / (2 * S) >= 512 &&
          (units * S < ctx->n_cu * 3 / 4 || P.K / S > 16384))
     S *= 2;
-#ifdef BOOST_GEMM_TUNING
-  if (const char* e = getenv("BOOST_GEMM_S")) S = std::max(1, std::min(atoi(e), kMaxSlices));
-#endif
   while (S > 1 && static_cast<uint64_t>(S) * P.B * (P.N + 2ull * (n_pages + 1)) >
                       ctx->gemm_ws_floats)
     S /= 2;
@@ -1163,11 +1159,6 @@ int launch_gemm_shape(GemvParams& P, int n_pages, bool need_fixup, const boost_c
 template <int BT>
 int launch_gemm(GemvParams& P, int n_pages, bool need_fixup, const boost_ctx* ctx,
                 hipStream_t s) {
-#ifdef BOOST_GEMM_TUNING
-  if (const char* e = getenv("BOOST_GEMM_RT"))
-    return atoi(e) == 2 ? launch_gemm_shape<BT, 2>(P, n_pages, need_fixup, ctx, s)
-                        : launch_gemm_shape<BT, 1>(P, n_pages, need_fixup, ctx, s);
-#endif
   // 128-row units where a page fills them and they still give a workgroup
   // per CU, or where a page holds 64..127 rows (one unit per page either
   // way); 64-row units otherwise
