@@ -367,6 +367,27 @@ int boost_paged_attn_decode(boost_ctx *ctx, const boost_kv_pool *pool, int layer
                             const int32_t *ctx_lens, float scale, void *out,
                             int out_dtype, void *stream);
 
+/* Allocation-free variant of boost_paged_attn_decode, for callers that cannot
+ * allocate device memory or use a pool's scratch (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * arguments, kernels and bits, but the partition partials live in a
+ * fixed-size static device array of the library (16.25 MiB per device, held
+ * until the process ends) instead of the pool's scratch.  The call allocates
+ * nothing.  Limit: B * Hq * partitions <= 32768 partial rows, where the
+ * partition count is the one the call picks from max_blocks, B and the KV
+ * heads (batch 64 x 32 query heads at up to 4096 tokens, or batch 256 x 32 at
+ * up to 8192, fit); larger calls fail with BOOST_EINVAL.  Every call on one
+ * GPU shares that GPU's array: calls that overlap on one GPU (on different
+ * streams, or from different pools or threads) race and must be ordered by
+ * the caller.  Nothing in the array needs to start at zero (each call writes
+ * every partial it reads).  Errors: as boost_paged_attn_decode, and EINVAL
+ * beyond the limit. */
+int boost_paged_attn_decode_noalloc(boost_ctx *ctx, const boost_kv_pool *pool,
+                                    int layer, const void *q, int B, int Hq,
+                                    const int32_t *block_tables, int max_blocks,
+                                    const int32_t *ctx_lens, float scale,
+                                    void *out, int out_dtype, void *stream);
+
 /* -------------------------------------------- a6: glue of a full decode step */
 
 /* The paper measures whole decode steps of Llama-style models (§5.1) without

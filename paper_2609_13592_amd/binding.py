@@ -106,6 +106,8 @@ _SIGS = {
     "boost_kv_write": (_i32, [_vp, _vp, _i32, _vp, _vp, _vp, _i32, _vp]),
     "boost_paged_attn_decode": (_i32, [_vp, _vp, _i32, _vp, _i32, _i32, _vp, _i32,
                                        _vp, C.c_float, _vp, _i32, _vp]),
+    "boost_paged_attn_decode_noalloc": (_i32, [_vp, _vp, _i32, _vp, _i32, _i32, _vp, _i32,
+                                               _vp, C.c_float, _vp, _i32, _vp]),
     "boost_decode_gemv": (_i32, [_vp, _vp, _i32, _i32, _vp, _i32, _vp, _i32, _vp]),
 }
 
@@ -389,6 +391,15 @@ def boost_paged_attn_decode(ctx: int, pool: int, layer: int, q, B: int, Hq: int,
                                           _ptr(block_tables), max_blocks,
                                           _ptr(ctx_lens), scale, _ptr(out), out_dtype,
                                           _stream(stream)))
+
+
+def boost_paged_attn_decode_noalloc(ctx: int, pool: int, layer: int, q, B: int, Hq: int,
+                                    block_tables, max_blocks: int, ctx_lens, scale: float,
+                                    out, out_dtype: int = DTYPE_F32, stream=None):
+    _check(load().boost_paged_attn_decode_noalloc(ctx, pool, layer, _ptr(q), B, Hq,
+                                                  _ptr(block_tables), max_blocks,
+                                                  _ptr(ctx_lens), scale, _ptr(out),
+                                                  out_dtype, _stream(stream)))
 
 
 # ---------------------------------------------------------- decode-step glue

@@ -19,6 +19,7 @@
 // partition order.  The arithmetic is independent of the placement.
 #include <algorithm>
 #include <cmath>
+#include <mutex>
 
 #include "runtime.h"
 
@@ -414,16 +415,28 @@ int launch(AttnParams& P, hipStream_t s) {
   return BOOST_OK;
 }
 
-}  // namespace
+// Scratch of the allocation-free entry point: partition partials of up to
+// kStaticRows (request, query head, partition) rows, the sums of p * v
+// ([kStaticRows][D] floats) followed by the running (max, sum) pairs
+// ([kStaticRows][2]).  16.25 MiB, held by every device the library runs on
+// until the process ends.  The host never uses the array's name as an
+// address: boost_init looks up each device's copy once
+// (attn_scratch_setup) and the entry point passes that address.
+constexpr int64_t kStaticRows = 32768;
+__device__ __align__(256) float scratch[kStaticRows * (kD + 2)];
 
-using namespace bst;
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+float* g_scratch_ptr[kMaxDevices] = {};  // per device: address of `scratch`
 
-extern "C" {
-
-int boost_paged_attn_decode(boost_ctx* ctx, const boost_kv_pool* pool, int layer,
-                            const void* q, int B, int Hq, const int32_t* block_tables,
-                            int max_blocks, const int32_t* ctx_lens, float scale,
-                            void* out, int out_dtype, void* stream) {
+// Everything both entry points check and compute, then the two launches;
+// part_acc / part_ml / max_parts name the partial buffers (max_parts = 0:
+// the call's own partition count, with at most cap_rows rows).
+int decode(boost_ctx* ctx, const boost_kv_pool* pool, int layer, const void* q, int B, int Hq,
+           const int32_t* block_tables, int max_blocks, const int32_t* ctx_lens, float scale,
+           void* out, int out_dtype, void* stream, float* part_acc, float* part_ml,
+           int max_parts, int64_t cap_rows) {
+  using bst::fail;
   if (!ctx || !pool || !q || !block_tables || !ctx_lens || !out)
     return fail(BOOST_EINVAL, "null argument");
   if (ctx->device < 0 || !pool->d_page_table) return fail(BOOST_ENODEV, "plan-only pool");
@@ -446,11 +459,11 @@ int boost_paged_attn_decode(boost_ctx* ctx, const boost_kv_pool* pool, int layer
   AttnParams P{};
   const uint64_t pages = pool->geom.pages, hp = pool->geom.host_pages;
   const uint64_t tk = 2ull * layer, tv = 2ull * layer + 1;  // tensor indices
-  P.k_hbm = pool->hbm.base + tk * (pages - hp) * kPage;
-  P.v_hbm = pool->hbm.base + tv * (pages - hp) * kPage;
+  P.k_hbm = pool->hbm.base + tk * (pages - hp) * bst::kPage;
+  P.v_hbm = pool->hbm.base + tv * (pages - hp) * bst::kPage;
   P.k_host = hp ? pool->host[layer].base : P.k_hbm;
-  P.v_host = hp ? pool->host[layer].base + hp * kPage : P.v_hbm;
-  P.host_from = (pages - hp) * kPage;
+  P.v_host = hp ? pool->host[layer].base + hp * bst::kPage : P.v_hbm;
+  P.host_from = (pages - hp) * bst::kPage;
   P.q = static_cast<const uint16_t*>(q);
   P.tables = block_tables;
   P.lens = ctx_lens;
@@ -468,11 +481,15 @@ int boost_paged_attn_decode(boost_ctx* ctx, const boost_kv_pool* pool, int layer
        std::max(kPartMin, std::min(kPartMax, (max_blocks + want_parts - 1) / want_parts))});
   P.part_blocks = std::max(P.part_blocks, 4);
   P.n_parts = (max_blocks + P.part_blocks - 1) / P.part_blocks;
-  P.max_parts = pool->max_parts;
+  P.max_parts = max_parts > 0 ? max_parts : P.n_parts;
   if (P.n_parts > P.max_parts) return fail(BOOST_EINVAL, "partition scratch too small");
+  if (static_cast<int64_t>(B) * Hq * P.max_parts > cap_rows)
+    return fail(BOOST_EINVAL, "%lld partial rows (B=%d x Hq=%d x %d partitions) exceed the "
+                "scratch's %lld", static_cast<long long>(B) * Hq * P.max_parts, B, Hq,
+                P.max_parts, static_cast<long long>(cap_rows));
   P.scale = scale > 0.f ? scale : 1.0f / std::sqrt(static_cast<float>(kD));
-  P.part_acc = pool->d_part_acc;
-  P.part_ml = pool->d_part_ml;
+  P.part_acc = part_acc;
+  P.part_ml = part_ml;
   P.out = out;
   P.out_bf16 = out_dtype == BOOST_DTYPE_BF16;
   auto s = static_cast<hipStream_t>(stream);
@@ -483,6 +500,60 @@ int boost_paged_attn_decode(boost_ctx* ctx, const boost_kv_pool* pool, int layer
     case 8: return launch<8>(P, s);
     default: return fail(BOOST_EINVAL, "Hq/H=%d not in {1, 2, 4, 8}", G);
   }
+}
+
+}  // namespace
+
+namespace bst {
+// Once per device, with that device current: the device address of this
+// device's copy of `scratch`.  Called by boost_init.
+int attn_scratch_setup(int device) {
+  if (device < 0 || device >= kMaxDevices)
+    return fail(BOOST_EINVAL, "device %d beyond the %d the static scratch serves", device,
+                kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[device]) return BOOST_OK;
+  void* ptr = nullptr;
+  const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+  if (e != hipSuccess || !ptr)
+    return fail(BOOST_EHIP, "hipGetSymbolAddress(scratch) on device %d: %s", device,
+                hipGetErrorString(e));
+  g_scratch_ptr[device] = static_cast<float*>(ptr);
+  return BOOST_OK;
+}
+}  // namespace bst
+
+using namespace bst;
+
+extern "C" {
+
+int boost_paged_attn_decode(boost_ctx* ctx, const boost_kv_pool* pool, int layer,
+                            const void* q, int B, int Hq, const int32_t* block_tables,
+                            int max_blocks, const int32_t* ctx_lens, float scale,
+                            void* out, int out_dtype, void* stream) {
+  if (!pool) return fail(BOOST_EINVAL, "null argument");
+  const int64_t rows = static_cast<int64_t>(pool->cfg.max_batch) * pool->cfg.q_heads *
+                       std::max(1, pool->max_parts);
+  return decode(ctx, pool, layer, q, B, Hq, block_tables, max_blocks, ctx_lens, scale, out,
+                out_dtype, stream, pool->d_part_acc, pool->d_part_ml,
+                std::max(1, pool->max_parts), rows);
+}
+
+int boost_paged_attn_decode_noalloc(boost_ctx* ctx, const boost_kv_pool* pool, int layer,
+                                    const void* q, int B, int Hq,
+                                    const int32_t* block_tables, int max_blocks,
+                                    const int32_t* ctx_lens, float scale, void* out,
+                                    int out_dtype, void* stream) {
+  if (!ctx) return fail(BOOST_EINVAL, "null argument");
+  if (ctx->device < 0) return fail(BOOST_ENODEV, "plan-only context");
+  float* base = nullptr;
+  {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (ctx->device < kMaxDevices) base = g_scratch_ptr[ctx->device];
+  }
+  if (!base) return fail(BOOST_EHIP, "static scratch of device %d not set up", ctx->device);
+  return decode(ctx, pool, layer, q, B, Hq, block_tables, max_blocks, ctx_lens, scale, out,
+                out_dtype, stream, base, base + kStaticRows * kD, 0, kStaticRows);
 }
 
 }  // extern "C"

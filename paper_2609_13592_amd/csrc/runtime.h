@@ -38,6 +38,10 @@ struct Slab {
 int slab_alloc(boost_ctx* ctx, uint64_t pages, bool host, Slab& s);
 void slab_free(Slab& s);
 
+// Device address of the attention's static scratch on `device` (the device
+// current), looked up once per device; boost_init calls it.
+int attn_scratch_setup(int device);
+
 }  // namespace bst
 
 struct boost_tensor {

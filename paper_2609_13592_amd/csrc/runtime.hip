@@ -200,6 +200,12 @@ int boost_init(int device, boost_ctx** out) {
       delete c;
       return fail(BOOST_ENOMEM, "GEMM workspace: %s", hipGetErrorString(e));
     }
+    const int rc = attn_scratch_setup(device);
+    if (rc) {
+      (void)hipFree(c->gemm_ws);
+      delete c;
+      return rc;
+    }
   } else if (device != -1) {
     delete c;
     return fail(BOOST_EINVAL, "device %d", device);
