@@ -106,6 +106,32 @@ int boost_calibrate(boost_ctx *ctx, uint64_t hbm_bytes, uint64_t host_bytes,
 int boost_stream_read_gbps(boost_ctx *ctx, const void *src, uint64_t bytes,
                            int grid, int iters, double *gbps);
 
+/* Concurrent two-tier streaming probe (the bound §3 "CAP" measures with a
+ * streaming kernel whose workgroups read the host tier and HBM at once, swept
+ * over the host share).  Allocates an HBM buffer of hbm_bytes and a pinned,
+ * device-mapped host buffer of host_bytes (coherent or not as set by
+ * boost_set_host_coherent), then for each of n_points points launches one
+ * kernel of host_wgs[i] + hbm_wgs[i] workgroups in which the workgroups
+ * 0, s, 2 s, ..., (host_wgs[i] - 1) s (s = host_stride[i], or 1 when
+ * host_stride is NULL; s = 8 puts them on one XCD, which receives every
+ * eighth workgroup) stream host_use[i] bytes of the host buffer and the
+ * others stream hbm_use[i] bytes of the HBM buffer (16-byte non-temporal
+ * loads, contiguous slices), `iters` timed launches after one warm-up.  results[5 i .. 5 i + 4] receive:
+ *   0: GB/s of both tiers' bytes over the launches back to back (events),
+ *   1: microseconds per launch (events),
+ *   2: HBM tier GB/s inside the launch: hbm_use / (last HBM workgroup's end -
+ *      the launch's first workgroup start), from each workgroup's clock,
+ *   3: host tier GB/s inside the launch, the same way (0 when unused),
+ *   4: microseconds from the first workgroup start to the last end.
+ * Synchronises; allocates and frees its buffers (load-time tool).
+ * Errors: EINVAL (null, sizes beyond the buffers, bytes not a multiple of 16,
+ * bytes without workgroups, a slice over 2 GiB, a stride outside [1, 64] or
+ * whose host workgroups fall past the grid), ENODEV, ENOMEM, EHIP. */
+int boost_cap_sweep(boost_ctx *ctx, uint64_t hbm_bytes, uint64_t host_bytes,
+                    int n_points, const uint64_t *hbm_use, const int *hbm_wgs,
+                    const uint64_t *host_use, const int *host_wgs,
+                    const int *host_stride, int iters, double *results);
+
 /* C1: modulus M = K + 1 with K = ceil(1/alpha) (§3.1 modulo placement, §4.4
  * ceil rule keeping the host share at or below alpha).  alpha in (0, 1].
  * Errors: EINVAL. */

@@ -69,6 +69,7 @@ _SIGS = {
     "boost_calibrate": (_i32, [_vp, _u64, _u64, _i32, C.POINTER(_dbl),
                                C.POINTER(_dbl), C.POINTER(_dbl)]),
     "boost_stream_read_gbps": (_i32, [_vp, _vp, _u64, _i32, _i32, C.POINTER(_dbl)]),
+    "boost_cap_sweep": (_i32, [_vp, _u64, _u64, _i32, _vp, _vp, _vp, _vp, _vp, _i32, _vp]),
     "boost_modulus_from_alpha": (_i32, [_dbl, C.POINTER(_u32)]),
     "boost_superpage_pages": (_i32, [_u64, C.POINTER(_u32)]),
     "boost_plan_mpp": (_i32, [_u64, _u32, _u64, _vp, _u64, C.POINTER(_u64)]),
@@ -223,6 +224,23 @@ def boost_stream_read_gbps(ctx: int, src, nbytes: int, grid: int, iters: int) ->
     _check(load().boost_stream_read_gbps(ctx, _ptr(src), nbytes, grid, iters,
                                          C.byref(g)))
     return g.value
+
+
+def boost_cap_sweep(ctx: int, hbm_bytes: int, host_bytes: int, points, iters: int):
+    """points: [(hbm_use, hbm_wgs, host_use, host_wgs[, host_stride])];
+    returns an array [n_points, 5]: combined GB/s, us per launch, HBM GB/s,
+    host GB/s, us of the last launch from first start to last end."""
+    n = len(points)
+    hu = np.ascontiguousarray([p[0] for p in points], dtype=np.uint64)
+    hw = np.ascontiguousarray([p[1] for p in points], dtype=np.int32)
+    ou = np.ascontiguousarray([p[2] for p in points], dtype=np.uint64)
+    ow = np.ascontiguousarray([p[3] for p in points], dtype=np.int32)
+    st = np.ascontiguousarray([p[4] if len(p) > 4 else 1 for p in points], dtype=np.int32)
+    res = np.zeros((n, 5), dtype=np.float64)
+    _check(load().boost_cap_sweep(ctx, hbm_bytes, host_bytes, n, hu.ctypes.data,
+                                  hw.ctypes.data, ou.ctypes.data, ow.ctypes.data,
+                                  st.ctypes.data, iters, res.ctypes.data))
+    return res
 
 
 def boost_modulus_from_alpha(alpha: float) -> int:

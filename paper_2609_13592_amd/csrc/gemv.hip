@@ -50,6 +50,7 @@ struct GemvParams {
   int y_bf16;
   int B;     // batch rows of x and y
   int join;  // 1: a cut row between two pages of one tier is summed by one unit
+  int tail_first;  // 1: the last unit of every page is dispatched before the others
   int S;     // K slices per row group (matrix-core path; 1 = no split)
   float* ws;  // S > 1: [S][B][N] partials, then [(n_pages + 1) * 2][S][B] of cut rows
   float* partial;  // [(n_pages + 1) boundaries][2 sides][kMaxGemvBatch]
@@ -323,20 +324,52 @@ __device__ void gemv_unit(const GemvParams& P, int page, int j, float* lds) {
   }
 }
 
+// Unit `idx` of a list of n pages (list == nullptr: pages 0..n-1) with U units
+// each.  Normally page idx / U, unit idx % U.  With tail_first the first n
+// indices are the last non-empty unit of every page and the rest the other
+// units in page order: the last unit of a page holds the row cut by the page
+// boundary, which it sums over both pages when they are in one tier, so it
+// reads twice as many steps as the others; dispatched first it overlaps
+// them instead of running alone at the end of the launch.
+template <int kRowsWg>
+__device__ __forceinline__ void unit_of(const GemvParams& P, const int32_t* list, int n, int U,
+                                        int idx, int& page, int& j) {
+  if (!P.tail_first) {
+    page = list ? list[idx / U] : idx / U;
+    j = idx % U;
+    return;
+  }
+  const int i = idx < n ? idx : (idx - n) / (U - 1);
+  page = list ? list[i] : i;
+  const int64_t total = static_cast<int64_t>(P.N) * P.K;
+  const int64_t pe0 = static_cast<int64_t>(page) * kPageElems;
+  const int64_t pe1 = min(pe0 + kPageElems, total);
+  const int last = static_cast<int>(((pe1 - 1) / P.K - pe0 / P.K) / kRowsWg);
+  if (idx < n) {
+    j = last;
+  } else {
+    const int k = (idx - n) % (U - 1);
+    j = k < last ? k : k + 1;
+  }
+}
+
 template <int B, int RW, int UN, int KS>
 __global__ __launch_bounds__(kThreads) void gemv_kernel(GemvParams P) {
   __shared__ float lds[2 * kWaves * RW * B];
+  constexpr int kRowsWg = (kWaves / KS) * RW;
   const int bid = blockIdx.x;
   const int U = P.units_per_page;
+  int page, j;
   if (P.address_order) {
-    gemv_unit<B, RW, UN, KS>(P, bid / U, bid % U, lds);
+    unit_of<kRowsWg>(P, nullptr, P.n_pages, U, bid, page, j);
+    gemv_unit<B, RW, UN, KS>(P, page, j, lds);
   } else if (bid < P.host_workers) {
     const int n_host_units = P.n_host_pages * U;
     for (int v = bid; v < n_host_units; v += P.host_workers)
       gemv_unit<B, RW, UN, KS>(P, P.host_pages[v / U], v % U, lds);
   } else {
-    const int u = bid - P.host_workers;
-    gemv_unit<B, RW, UN, KS>(P, P.hbm_pages[u / U], u % U, lds);
+    unit_of<kRowsWg>(P, P.hbm_pages, P.n_hbm_pages, U, bid - P.host_workers, page, j);
+    gemv_unit<B, RW, UN, KS>(P, page, j, lds);
   }
 }
 
@@ -974,9 +1007,12 @@ __global__ __launch_bounds__(256) void split_reduce(GemvParams P) {
 #ifndef BOOST_GEMV_UN1_LONG
 #define BOOST_GEMV_UN1_LONG 4
 #endif
+#ifndef BOOST_GEMV_RW1
+#define BOOST_GEMV_RW1 1
+#endif
 template <int B, int KS>
 struct Shape {
-  static constexpr int RW = B == 1 ? (KS > 2 ? BOOST_GEMV_RW1_LONG : 1)
+  static constexpr int RW = B == 1 ? (KS > 2 ? BOOST_GEMV_RW1_LONG : BOOST_GEMV_RW1)
                                    : (B == 2 ? 2 : (B <= 4 ? 4 : BOOST_GEMV_RW_BIG));
   static constexpr int UN = B == 1 ? (KS > 2 ? BOOST_GEMV_UN1_LONG : BOOST_GEMV_UN1)
                                    : (B <= 4 ? 2 : BOOST_GEMV_UN_BIG);
@@ -988,8 +1024,14 @@ struct Shape {
 #ifndef BOOST_GEMV_KS_MAX
 #define BOOST_GEMV_KS_MAX 4
 #endif
+#ifndef BOOST_GEMV_KS2_ABOVE
+#define BOOST_GEMV_KS2_ABOVE 6144
+#endif
+#ifndef BOOST_GEMV_KS4_ABOVE
+#define BOOST_GEMV_KS4_ABOVE 12288
+#endif
 inline int k_splits(int K) {
-  const int ks = K <= 6144 ? 1 : (K <= 12288 ? 2 : 4);
+  const int ks = K <= BOOST_GEMV_KS2_ABOVE ? 1 : (K <= BOOST_GEMV_KS4_ABOVE ? 2 : 4);
   return ks < BOOST_GEMV_KS_MAX ? ks : BOOST_GEMV_KS_MAX;
 }
 
@@ -1048,11 +1090,16 @@ int launch_fixup(GemvParams& P, int n_pages, bool need_fixup, hipStream_t s) {
   return BOOST_OK;
 }
 
+#ifndef BOOST_GEMV_TAIL_FIRST
+#define BOOST_GEMV_TAIL_FIRST 1
+#endif
 template <int B, int KS>
 int launch(GemvParams& P, int n_pages, bool need_fixup, const boost_ctx* ctx, hipStream_t s) {
   constexpr int RW = Shape<B, KS>::RW, UN = Shape<B, KS>::UN;
   const int64_t grid = plan_grid(P, n_pages, RW * (kWaves / KS), ctx, false);
   if (grid < 0) return bst::fail(BOOST_EINVAL, "grid too large");
+  // rows cut by page boundaries: their units go first (see unit_of)
+  P.tail_first = kPageElems % P.K != 0 && P.units_per_page >= 2 ? BOOST_GEMV_TAIL_FIRST : 0;
   hipLaunchKernelGGL((gemv_kernel<B, RW, UN, KS>), dim3(static_cast<unsigned>(grid)),
                      dim3(kThreads), 0, s, P);
   BOOST_HIP(hipGetLastError());
