@@ -48,6 +48,11 @@ def parse():
                    help="replay each step as a captured HIP graph")
     p.add_argument("--pmc-ref", action="store_true",
                    help="also run a plain 1 GiB device copy (counter scale reference)")
+    p.add_argument("--cap-quick", action="store_true",
+                   help="cap_probe: only a handful of points, for counter runs")
+    p.add_argument("--summarize-pmc", default="",
+                   help="summarise the rocprofv3 counter CSVs under this directory "
+                        "(per kernel and grid) as JSON on stdout, then exit")
     p.add_argument("--workload", default="chain8b",
                    choices=("chain8b", "llama70b", "throughput8b", "host_share_sweep",
                             "cap_probe", "batch_sweep", "placements", "dsr_churn"),
@@ -301,6 +306,33 @@ def counter_traffic(kernel: str, source: str):
     if hashlib.sha256(src).hexdigest() != data["source_sha256"]:
         return None
     return int(data["traffic_bytes_per_launch"])
+
+
+def summarize_pmc(directory: str):
+    """Per-kernel sums of rocprofv3 counter CSVs (every `*counter_collection.csv`
+    under `directory`): for each (kernel name, grid size) the number of
+    dispatches and, per counter, the mean value per dispatch."""
+    import csv
+    import glob
+    acc = {}
+    for path in sorted(glob.glob(os.path.join(directory, "**", "*counter_collection.csv"),
+                                 recursive=True)):
+        with open(path, newline="") as fh:
+            for row in csv.DictReader(fh):
+                name = row.get("Kernel_Name", "?").replace("(anonymous namespace)::", "")
+                name = name[5:] if name.startswith("void ") else name
+                name = name.split("(")[0].strip()
+                key = f"{name} grid={row.get('Grid_Size', '?')}"
+                ent = acc.setdefault(key, {"dispatches": set(), "sums": {}})
+                ent["dispatches"].add(row.get("Dispatch_Id"))
+                c = row.get("Counter_Name", "?")
+                ent["sums"][c] = ent["sums"].get(c, 0.0) + float(row.get("Counter_Value", 0) or 0)
+    out = {}
+    for key, ent in sorted(acc.items()):
+        n = len(ent["dispatches"])
+        out[key] = {"dispatches": n,
+                    "per_dispatch": {c: round(v / n, 1) for c, v in sorted(ent["sums"].items())}}
+    return out
 
 
 # ----------------------------------------------------------- CPU baseline
@@ -779,27 +811,49 @@ def cap_probe(args, bd, ctx, torch, bw_hbm, bw_host, alpha, M_alpha):
     """The streaming-probe bound of concurrent access (§3 "CAP": the paper
     sweeps the host share of a streaming kernel whose workgroups read host
     memory and HBM at once, and §6.1 notes the compute units must be able to
-    saturate both tiers together).  Three sweeps of one kernel
-    (`boost_cap_sweep`):
+    saturate both tiers together).  Sweeps of one kernel (`boost_cap_sweep`):
       * HBM alone, 2 GiB, over the number of workgroups (how many compute
         units it takes to saturate HBM);
-      * host alone, 256 MiB, over the number of workgroups (how many the host
-        link needs);
-      * both at once: 2 GiB in total with a share f on host, f from 0 to
-        1/16, read by h host workgroups beside the HBM workgroups, against
-        the same 2 GiB from HBM alone, with coherent and non-coherent host
-        pages.
-    Each point gives the combined rate and each tier's rate inside the launch
-    (workgroup clocks).  The measured-optimal host share is the best point
-    of the concurrent sweep; its modulus (1/f) is what the placement should
-    use when it beats all-HBM, and "no host page" otherwise."""
+      * host alone, 256 MiB, over workgroups x loads in flight per lane x
+        cache policy (what the host link needs);
+      * both at once: 2 GiB in total with a share f on host, read by h host
+        workgroups beside 8192 HBM workgroups of 256 KiB (more than fit at
+        once, so the dispatcher balances them over the compute units),
+        against the same 2 GiB from HBM alone; and the one-wave layouts (2048
+        HBM workgroups with static slices), coherent and non-coherent pages;
+      * the host share moved by the copy engine instead (host -> HBM copy on a
+        second stream beside the HBM-only launch).
+    Each point gives the combined rate, each tier's rate inside the launch
+    (workgroup clocks) and the HBM bandwidth lost per GB/s of host bandwidth
+    gained.  The measured-optimal host share is the best point of the
+    concurrent sweeps; its modulus (1/f) is what the placement should use when
+    it beats all-HBM, and "no host page" otherwise."""
     T = 2 << 30
     HOST = 256 << 20
+    iters = 15
     n_cu = bd.boost_ctx_info(ctx)[1]
-    hbm_wgs = n_cu * 8
-    iters = 5
+    if args.cap_quick:
+        # distinct grids per point, so a counter run can tell the launches apart
+        hb = int(T / M_alpha) // 16 * 16
+        pts = {"hbm_only": dict(hbm_bytes=T, hbm_wgs=8192),
+               "host_only_8wg": dict(host_bytes=HOST, host_wgs=8),
+               "alpha_share_spread_8wg": dict(hbm_bytes=T - hb, hbm_wgs=8192, host_bytes=hb,
+                                              host_wgs=8),
+               "hbm_only_queue": dict(hbm_bytes=T, hbm_wgs=n_cu * 8 - 16, hbm_chunk_kib=256),
+               "alpha_share_queue_one_xcd_8wg": dict(hbm_bytes=T - hb, hbm_wgs=n_cu * 8 - 8,
+                                                     host_bytes=hb, host_wgs=8, host_stride=8,
+                                                     hbm_chunk_kib=256)}
+        res = bd.boost_cap_sweep(ctx, T, HOST, list(pts.values()), 3)
+        return {"metric": "CAP probe points for counter runs", "unit": "us",
+                "points": {k: {"grid": v.get("hbm_wgs", 0) + v.get("host_wgs", 0),
+                               "hbm_bytes": v.get("hbm_bytes", 0),
+                               "host_bytes": v.get("host_bytes", 0),
+                               "us": round(float(r[1]), 2),
+                               "hbm_in_launch_gbps": round(float(r[2]), 1),
+                               "host_in_launch_gbps": round(float(r[3]), 2)}
+                           for (k, v), r in zip(pts.items(), res)}}
 
-    def run(points, coherent):
+    def run(points, coherent=1):
         bd.boost_set_host_coherent(ctx, coherent)
         try:
             return bd.boost_cap_sweep(ctx, T, HOST, points, iters)
@@ -810,54 +864,130 @@ def cap_probe(args, bd, ctx, torch, bw_hbm, bw_host, alpha, M_alpha):
         return int(x) // 16 * 16
 
     out = {}
-    grids = [16, 32, 64, 128, 192, 256, 384, 512, 1024, 2048, 4096]
-    res = run([(T, g, 0, 0) for g in grids], 1)
+    # how the HBM stream is handed to the workgroups, all-HBM: static slices
+    # (one per workgroup, 8192 or 2048 of them), persistent workers with
+    # 256 KiB chunks dealt round robin, from a queue, and from a queue after a
+    # first chunk of their own (the claim of the next chunk overlapping the
+    # current one)
+    n_slots = bd.boost_ctx_info(ctx)[1] * 8
+    modes = {"static_8192": dict(hbm_bytes=T, hbm_wgs=8192),
+             "static_one_wave": dict(hbm_bytes=T, hbm_wgs=n_slots),
+             "persistent_round_robin_256k": dict(hbm_bytes=T, hbm_wgs=n_slots,
+                                                 hbm_chunk_kib=256, chunk_static=1),
+             "persistent_queue_256k": dict(hbm_bytes=T, hbm_wgs=n_slots, hbm_chunk_kib=256),
+             "persistent_queue_first_own_256k": dict(hbm_bytes=T, hbm_wgs=n_slots,
+                                                     hbm_chunk_kib=256, chunk_static=2),
+             "persistent_queue_first_own_64k": dict(hbm_bytes=T, hbm_wgs=n_slots,
+                                                    hbm_chunk_kib=64, chunk_static=2)}
+    res = run(list(modes.values()))
+    out["hbm_stream_modes"] = {k: {"us": round(float(r[1]), 2),
+                                   "in_launch_gbps": round(float(r[2]), 1),
+                                   "last_end_by_xcd_us": [round(float(v), 1) for v in r[8:16]]}
+                               for k, r in zip(modes, res)}
+    grids = [64, 128, 256, 512, 1024, 2048, 4096, 8192]
+    res = run([dict(hbm_bytes=T, hbm_wgs=g) for g in grids])
     out["hbm_by_workgroups"] = [{"workgroups": g, "gbps": round(float(r[0]), 1),
                                  "in_launch_gbps": round(float(r[2]), 1)}
                                 for g, r in zip(grids, res)]
-    hw = [1, 2, 4, 8, 16, 32, 64, 128, 256]
-    for tag, coh in (("host_by_workgroups", 1), ("host_by_workgroups_noncoherent", 0)):
-        res = run([(0, 0, HOST, h) for h in hw], coh)
-        out[tag] = [{"workgroups": h, "gbps": round(float(r[0]), 2),
-                     "in_launch_gbps": round(float(r[3]), 2)} for h, r in zip(hw, res)]
-    shares = [0.0, 1 / 1024, 1 / 512, 1 / 256, 1 / M_alpha, 1 / 64, 1 / 16]
-    hosts = [4, 8, 16, 32]
-    # layouts of the concurrent launch: the HBM grid filling every workgroup
-    # slot (8 per CU, so each host workgroup delays one HBM workgroup), half
-    # of the slots (no HBM workgroup waits), and half with the host
-    # workgroups on one XCD (every eighth workgroup)
-    layouts = {"concurrent": (hbm_wgs, 1, 1),
-               "concurrent_noncoherent": (hbm_wgs, 1, 0),
-               "concurrent_half_grid": (hbm_wgs // 2, 1, 1),
-               "concurrent_half_grid_one_xcd": (hbm_wgs // 2, 8, 1)}
-    for tag, (g_hbm, stride, coh) in layouts.items():
+    host_pts = [(h, d, 0) for d in (1, 2, 4, 8) for h in (1, 2, 4, 8, 16, 32, 64)]
+    host_pts += [(h, 8, pol) for pol in (1, 2) for h in (4, 16)]
+    host_pts += [(h, 8, 0) for h in (128, 256)]
+    res = run([dict(host_bytes=HOST, host_wgs=h, host_depth=d, host_policy=pol)
+               for h, d, pol in host_pts])
+    out["host_by_workgroups"] = [
+        {"workgroups": h, "depth": d, "policy": pol, "gbps": round(float(r[0]), 2),
+         "in_launch_gbps": round(float(r[3]), 2),
+         "bytes_in_flight": h * 256 * 16 * d}
+        for (h, d, pol), r in zip(host_pts, res)]
+
+    shares = [1 / 1024, 1 / 256, 1 / M_alpha, 1 / 64]
+    BAL = 8192                   # HBM workgroups of 256 KiB, balanced by the dispatcher
+    ONE_WAVE = bd.boost_ctx_info(ctx)[1] * 8   # every slot once, static slices
+
+    def with_refs(g_hbm, pts, coherent=1, chunk=0):
+        """Run the points each right after an all-HBM reference launch set (and
+        one more at the end); per point, the mean of the two references
+        around it."""
+        ref = dict(hbm_bytes=T, hbm_wgs=g_hbm, hbm_chunk_kib=chunk)
+        seq = [ref]
+        for q in pts:
+            seq += [q, ref]
+        res = run(seq, coherent)
+        refs = res[0::2]
+        rows = res[1::2]
+        t_ref = [(refs[k][1] + refs[k + 1][1]) / 2 for k in range(len(pts))]
+        h_ref = [(refs[k][2] + refs[k + 1][2]) / 2 for k in range(len(pts))]
+        spread = float(np.std(refs[:, 1]) / np.mean(refs[:, 1]))
+        return rows, t_ref, h_ref, float(np.median(refs[:, 1])), float(np.median(refs[:, 2])), spread
+
+    def sweep(tag, g_hbm, combos, coherent=1, stride=1, chunk=0):
         pts, keys = [], []
         for f in shares:
-            for h in (hosts if f > 0 else [0]):
-                host_use = r16(f * T)
-                pts.append((T - host_use, g_hbm, host_use, h, stride if h else 1))
-                keys.append((f, h))
-        # the all-HBM reference again at the end, so drift shows
-        pts.append((T, g_hbm, 0, 0, 1))
-        res = run(pts, coh)
-        t_ref = float(np.median([res[0][1], res[-1][1]]))
+            hb = r16(f * T)
+            for h, d, pol in combos:
+                # persistent queue workers: the host workgroups take slots of
+                # the one wave
+                g = g_hbm - h if chunk else g_hbm
+                pts.append(dict(hbm_bytes=T - hb, hbm_wgs=g, host_bytes=hb, host_wgs=h,
+                                host_stride=stride, host_depth=d, host_policy=pol,
+                                hbm_chunk_kib=chunk))
+                keys.append((f, h, d, pol))
+        res, t_refs, h_refs, t_med, h_med, spread = with_refs(g_hbm, pts, coherent, chunk)
         rows = []
-        for (f, h), r in zip(keys, res):
-            host_b = r16(f * T)
-            bound_us = max((T - host_b) / (bw_hbm * 1e3), host_b / (bw_host * 1e3))
-            rows.append({"host_share": round(f, 6), "host_workgroups": h,
-                         "us": round(float(r[1]), 2),
+        for key, r, t_ref, h_ref in zip(keys, res, t_refs, h_refs):
+            f, h, d, pol = key
+            hb = r16(f * T)
+            bound_us = max((T - hb) / (bw_hbm * 1e3), hb / (bw_host * 1e3))
+            host_g = float(r[3])
+            rows.append({"host_share": round(f, 6), "host_workgroups": h, "depth": d,
+                         "policy": pol, "us": round(float(r[1]), 2),
+                         "ref_us": round(t_ref, 2),
                          "speedup_vs_hbm_only": round(t_ref / float(r[1]), 4),
                          "gbps": round(float(r[0]), 1),
                          "hbm_in_launch_gbps": round(float(r[2]), 1),
-                         "host_in_launch_gbps": round(float(r[3]), 2),
+                         "ref_hbm_in_launch_gbps": round(h_ref, 1),
+                         "host_in_launch_gbps": round(host_g, 2),
+                         "hbm_median_end_us": round(float(r[5]), 2),
+                         "hbm_last_end_us": round(float(r[7]), 2),
+                         "hbm_last_end_by_xcd_us": [round(float(v), 1) for v in r[8:16]],
+                         "hbm_lost_per_host_gbps": round((h_ref - float(r[2])) / host_g, 2)
+                         if host_g > 0 else None,
                          "bound_us": round(bound_us, 2),
-                         "bound_speedup": round(t_ref / bound_us, 4) if bound_us else None})
-        out[tag] = {"hbm_workgroups": g_hbm, "host_stride": stride, "coherent": bool(coh),
-                    "hbm_only_us": round(t_ref, 2),
-                    "hbm_only_spread": round(abs(res[0][1] - res[-1][1]) / t_ref, 4),
-                    "points": rows}
-    cands = [(tag, r) for tag in layouts for r in out[tag]["points"] if r["host_share"] > 0]
+                         "bound_speedup": round(t_ref / bound_us, 4)})
+        out[tag] = {"hbm_workgroups": g_hbm, "host_stride": stride, "coherent": bool(coherent),
+                    "hbm_chunk_kib": chunk, "hbm_only_us": round(t_med, 2), "hbm_only_in_launch_gbps": round(h_med, 1),
+                    "hbm_only_spread": round(spread, 4), "points": rows}
+
+    combos = [(h, d, 0) for d in (2, 8) for h in (4, 8, 16)]
+    sweep("concurrent_balanced", BAL, combos + [(8, 8, 1), (8, 8, 2)])
+    sweep("concurrent_balanced_one_xcd", BAL, combos, stride=8)
+    # persistent HBM workers fed by a queue of 256 KiB chunks (a slower XCD
+    # takes fewer chunks), host workgroups spread or on one XCD
+    sweep("concurrent_queue", ONE_WAVE, [(h, 8, 0) for h in (4, 8, 16)], chunk=256)
+    sweep("concurrent_queue_one_xcd", ONE_WAVE, combos, stride=8, chunk=256)
+    sweep("concurrent_one_wave", ONE_WAVE, [(8, 8, 0)])
+    sweep("concurrent_one_wave_noncoherent", ONE_WAVE, [(8, 8, 0)], coherent=0)
+    sweep("concurrent_balanced_noncoherent", BAL, [(8, 8, 0)], coherent=0)
+
+    # the host share moved by the copy engine beside the HBM-only launch
+    pts = []
+    for f in shares:
+        hb = r16(f * T)
+        pts.append(dict(hbm_bytes=T - hb, hbm_wgs=BAL, host_bytes=hb, dma=1))
+    res, t_refs, h_refs, t_med, _, spread = with_refs(BAL, pts)
+    out["dma_beside_hbm"] = {
+        "hbm_only_us": round(t_med, 2), "hbm_only_spread": round(spread, 4),
+        "points": [{"host_share": round(f, 6), "kernel_us": round(float(r[1]), 2),
+                    "copy_us": round(float(r[6]), 2), "ref_us": round(t_ref, 2),
+                    "speedup_vs_hbm_only": round(t_ref / max(float(r[1]), float(r[6])), 4),
+                    "hbm_in_launch_gbps": round(float(r[2]), 1),
+                    "copy_gbps": round(float(r[3]), 2),
+                    "hbm_lost_per_host_gbps": round((h_ref - float(r[2])) / float(r[3]), 2)
+                    if r[3] > 0 else None}
+                   for f, r, t_ref, h_ref in zip(shares, res, t_refs, h_refs)]}
+
+    tags = [t for t in out if t.startswith("concurrent")]
+    cands = [(tag, r) for tag in tags for r in out[tag]["points"]]
     tag, best = max(cands, key=lambda c: c[1]["speedup_vs_hbm_only"])
     # a gain must clear the spread of the all-HBM reference of its layout
     noise = out[tag]["hbm_only_spread"]
@@ -872,8 +1002,8 @@ def cap_probe(args, bd, ctx, torch, bw_hbm, bw_host, alpha, M_alpha):
             "value": out["measured_optimum"]["speedup_vs_hbm_only"], "unit": "x",
             "n_gpus": 1, "higher_is_better": True, "dtype": "u8", "data": "synthetic",
             "config": {"workload": "streaming read of 2 GiB split between HBM and pinned "
-                                   "host memory, 16-byte non-temporal loads",
-                       "hbm_workgroups": hbm_wgs, "iters": iters},
+                                   "host memory, 16-byte loads",
+                       "iters": iters},
             "calibration": {"hbm_gbps": round(bw_hbm, 1), "host_gbps": round(bw_host, 2),
                             "alpha": round(alpha, 6), "M_from_alpha": M_alpha},
             "results": out}
@@ -1226,6 +1356,9 @@ def dsr_churn(args, bd, ctx, torch, bw_hbm, bw_host, alpha, M):
 
 def main():
     args = parse()
+    if args.summarize_pmc:
+        print(json.dumps(summarize_pmc(args.summarize_pmc), indent=1))
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); "
               "the library has no multi-GPU path.", file=sys.stderr)

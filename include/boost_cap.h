@@ -106,31 +106,64 @@ int boost_calibrate(boost_ctx *ctx, uint64_t hbm_bytes, uint64_t host_bytes,
 int boost_stream_read_gbps(boost_ctx *ctx, const void *src, uint64_t bytes,
                            int grid, int iters, double *gbps);
 
+/* One point of the concurrent two-tier streaming probe. */
+typedef struct boost_cap_point {
+  uint64_t hbm_bytes;   /* bytes read from the HBM buffer */
+  uint64_t host_bytes;  /* bytes read from the host buffer */
+  int32_t hbm_wgs;      /* workgroups that stream the HBM bytes */
+  int32_t host_wgs;     /* workgroups that stream the host bytes (0 for DMA) */
+  int32_t host_stride;  /* host workgroups are 0, s, 2s, ...: 1 spreads them over
+                           the XCDs, 8 puts them on one XCD */
+  int32_t host_depth;   /* 16-byte loads per lane in flight on host: 1, 2, 4, 8 */
+  int32_t host_policy;  /* host-load cache policy: 0 non-temporal (the kernels'),
+                           1 default, 2 system-coherent */
+  int32_t dma;          /* 1: the host bytes move by a host -> HBM copy on a
+                           second stream, started with the HBM-only launch */
+  int32_t hbm_chunk_kib;  /* 0: each HBM workgroup streams one contiguous slice;
+                           > 0 (a multiple of 4): the HBM workgroups are
+                           persistent and take chunks of this many KiB from a
+                           queue (an atomic counter) until none is left */
+  int32_t chunk_static; /* with hbm_chunk_kib > 0: 0 every chunk from the
+                           queue; 1 the chunks dealt to the persistent workers
+                           round robin, no queue; 2 each worker's first chunk
+                           is its own index, the rest from the queue */
+} boost_cap_point;
+
 /* Concurrent two-tier streaming probe (the bound §3 "CAP" measures with a
  * streaming kernel whose workgroups read the host tier and HBM at once, swept
- * over the host share).  Allocates an HBM buffer of hbm_bytes and a pinned,
- * device-mapped host buffer of host_bytes (coherent or not as set by
- * boost_set_host_coherent), then for each of n_points points launches one
- * kernel of host_wgs[i] + hbm_wgs[i] workgroups in which the workgroups
- * 0, s, 2 s, ..., (host_wgs[i] - 1) s (s = host_stride[i], or 1 when
- * host_stride is NULL; s = 8 puts them on one XCD, which receives every
- * eighth workgroup) stream host_use[i] bytes of the host buffer and the
- * others stream hbm_use[i] bytes of the HBM buffer (16-byte non-temporal
- * loads, contiguous slices), `iters` timed launches after one warm-up.  results[5 i .. 5 i + 4] receive:
- *   0: GB/s of both tiers' bytes over the launches back to back (events),
+ * over the host share; §6.1 notes that the compute units must be able to keep
+ * both tiers busy together).  Allocates an HBM buffer of hbm_bytes and a
+ * pinned, device-mapped host buffer of host_bytes (coherent or not as set by
+ * boost_set_host_coherent; plus an HBM staging buffer of host_bytes when a
+ * point uses DMA), then for each of n_points points launches one kernel of
+ * host_wgs + hbm_wgs workgroups, `iters` timed launches after one warm-up.
+ * Static slices start on 1 KiB boundaries (the last ones shorter or empty).
+ * Host workgroups stream host_bytes of the host buffer (contiguous slices,
+ * the point's depth and cache policy), the others hbm_bytes of the HBM buffer
+ * (16-byte non-temporal loads, 8 per lane in flight, contiguous slices).
+ * results[16 i .. 16 i + 15] receive, each the median over the `iters` launches:
+ *   0: GB/s of both tiers' bytes per launch (events; for DMA points over the
+ *      longer of the launch and the copy),
  *   1: microseconds per launch (events),
- *   2: HBM tier GB/s inside the launch: hbm_use / (last HBM workgroup's end -
+ *   2: HBM tier GB/s inside the launch: hbm_bytes / (last HBM workgroup's end -
  *      the launch's first workgroup start), from each workgroup's clock,
- *   3: host tier GB/s inside the launch, the same way (0 when unused),
- *   4: microseconds from the first workgroup start to the last end.
+ *   3: host tier GB/s: inside the launch the same way, or bytes over the
+ *      copy's event time for DMA points (0 when unused),
+ *   4: microseconds from the first workgroup start to the last end,
+ *   5: microseconds from the first start to the median HBM workgroup's end,
+ *   6: microseconds of the copy (DMA points), else 0,
+ *   7: microseconds from the first start to the last HBM workgroup's end,
+ *   8 + x: the same for the HBM workgroups that ran on XCD x (hardware
+ *      register XCC_ID), x = 0..7 (0 when none ran there).
  * Synchronises; allocates and frees its buffers (load-time tool).
  * Errors: EINVAL (null, sizes beyond the buffers, bytes not a multiple of 16,
  * bytes without workgroups, a slice over 2 GiB, a stride outside [1, 64] or
- * whose host workgroups fall past the grid), ENODEV, ENOMEM, EHIP. */
+ * whose host workgroups fall past the grid, a depth or policy out of range, a
+ * DMA point with host workgroups, a chunk size out of range), ENODEV, ENOMEM,
+ * EHIP. */
 int boost_cap_sweep(boost_ctx *ctx, uint64_t hbm_bytes, uint64_t host_bytes,
-                    int n_points, const uint64_t *hbm_use, const int *hbm_wgs,
-                    const uint64_t *host_use, const int *host_wgs,
-                    const int *host_stride, int iters, double *results);
+                    int n_points, const boost_cap_point *points, int iters,
+                    double *results);
 
 /* C1: modulus M = K + 1 with K = ceil(1/alpha) (§3.1 modulo placement, §4.4
  * ceil rule keeping the host share at or below alpha).  alpha in (0, 1].

@@ -69,7 +69,7 @@ _SIGS = {
     "boost_calibrate": (_i32, [_vp, _u64, _u64, _i32, C.POINTER(_dbl),
                                C.POINTER(_dbl), C.POINTER(_dbl)]),
     "boost_stream_read_gbps": (_i32, [_vp, _vp, _u64, _i32, _i32, C.POINTER(_dbl)]),
-    "boost_cap_sweep": (_i32, [_vp, _u64, _u64, _i32, _vp, _vp, _vp, _vp, _vp, _i32, _vp]),
+    "boost_cap_sweep": (_i32, [_vp, _u64, _u64, _i32, _vp, _i32, _vp]),
     "boost_modulus_from_alpha": (_i32, [_dbl, C.POINTER(_u32)]),
     "boost_superpage_pages": (_i32, [_u64, C.POINTER(_u32)]),
     "boost_plan_mpp": (_i32, [_u64, _u32, _u64, _vp, _u64, C.POINTER(_u64)]),
@@ -226,20 +226,27 @@ def boost_stream_read_gbps(ctx: int, src, nbytes: int, grid: int, iters: int) ->
     return g.value
 
 
+CAP_POINT = np.dtype([("hbm_bytes", np.uint64), ("host_bytes", np.uint64),
+                      ("hbm_wgs", np.int32), ("host_wgs", np.int32),
+                      ("host_stride", np.int32), ("host_depth", np.int32),
+                      ("host_policy", np.int32), ("dma", np.int32),
+                      ("hbm_chunk_kib", np.int32), ("chunk_static", np.int32)])
+
+
 def boost_cap_sweep(ctx: int, hbm_bytes: int, host_bytes: int, points, iters: int):
-    """points: [(hbm_use, hbm_wgs, host_use, host_wgs[, host_stride])];
-    returns an array [n_points, 5]: combined GB/s, us per launch, HBM GB/s,
-    host GB/s, us of the last launch from first start to last end."""
+    """points: dicts with the fields of boost_cap_point (missing ones: bytes and
+    workgroups 0, stride 1, depth 8, policy 0, dma 0, chunk 0); returns an array
+    [n_points, 16] laid out as the header states."""
     n = len(points)
-    hu = np.ascontiguousarray([p[0] for p in points], dtype=np.uint64)
-    hw = np.ascontiguousarray([p[1] for p in points], dtype=np.int32)
-    ou = np.ascontiguousarray([p[2] for p in points], dtype=np.uint64)
-    ow = np.ascontiguousarray([p[3] for p in points], dtype=np.int32)
-    st = np.ascontiguousarray([p[4] if len(p) > 4 else 1 for p in points], dtype=np.int32)
-    res = np.zeros((n, 5), dtype=np.float64)
-    _check(load().boost_cap_sweep(ctx, hbm_bytes, host_bytes, n, hu.ctypes.data,
-                                  hw.ctypes.data, ou.ctypes.data, ow.ctypes.data,
-                                  st.ctypes.data, iters, res.ctypes.data))
+    arr = np.zeros(n, dtype=CAP_POINT)
+    for i, p in enumerate(points):
+        arr[i] = (p.get("hbm_bytes", 0), p.get("host_bytes", 0), p.get("hbm_wgs", 0),
+                  p.get("host_wgs", 0), p.get("host_stride", 1), p.get("host_depth", 8),
+                  p.get("host_policy", 0), p.get("dma", 0), p.get("hbm_chunk_kib", 0),
+                  p.get("chunk_static", 0))
+    res = np.zeros((n, 16), dtype=np.float64)
+    _check(load().boost_cap_sweep(ctx, hbm_bytes, host_bytes, n, arr.ctypes.data, iters,
+                                  res.ctypes.data))
     return res
 
 

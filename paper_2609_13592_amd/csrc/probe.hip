@@ -15,17 +15,22 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kUnroll = 8;
 
-// Stream one contiguous slice (part of `parts`) of n_vec 16-byte vectors:
+// Stream one contiguous slice (part of `parts`, each a whole number of 1 KiB
+// blocks; the last ones shorter or empty) of n_vec 16-byte vectors:
 // lanes stride by 256 vectors so a wavefront's 64 lanes cover 1 KiB
-// contiguous per load.  Loads are raw buffer loads with the non-temporal
-// policy, exactly as the decode kernels stream their operands, so alpha is
-// the ratio the kernels can actually reach.  A slice is at most 2 GiB (the
-// 32-bit buffer offset; checked on the host).  Returns the XOR of every word,
-// which the callers store only when it equals a magic value: that keeps the
-// loads alive without a data-dependent store in practice.
+// contiguous per load; DEPTH loads per lane are in flight at a time.  Loads
+// are raw buffer loads with cache policy AUX (2 = non-temporal, exactly as the
+// decode kernels stream their operands, so alpha is the ratio the kernels can
+// actually reach).  A slice is at most 2 GiB (the 32-bit buffer offset;
+// checked on the host).  Returns the XOR of every word, which the callers
+// store only when it equals a magic value: that keeps the loads alive without
+// a data-dependent store in practice.
+template <int DEPTH = kUnroll, int AUX = 2>
 __device__ __forceinline__ uint32_t stream_slice(const char* src, uint64_t n_vec, int part,
                                                  int parts) {
-  const uint64_t per = (n_vec + parts - 1) / parts;
+  // slices start on 1 KiB boundaries (one wavefront load), so no cache line
+  // is shared by two slices
+  const uint64_t per = ((n_vec + parts - 1) / parts + 63) / 64 * 64;
   const uint64_t beg = static_cast<uint64_t>(part) * per;
   const uint64_t end = beg + per < n_vec ? beg + per : n_vec;
   uint32_t acc = 0;
@@ -35,18 +40,18 @@ __device__ __forceinline__ uint32_t stream_slice(const char* src, uint64_t n_vec
       const_cast<char*>(src) + beg * 16, 0, static_cast<int>(span), 0x00020000);
   const uint32_t n = static_cast<uint32_t>(end - beg);
   uint32_t i = threadIdx.x;
-  for (; i + (kUnroll - 1) * kThreads < n; i += kUnroll * kThreads) {
-    uint4 v[kUnroll];
+  for (; i + (DEPTH - 1) * kThreads < n; i += DEPTH * kThreads) {
+    uint4 v[DEPTH];
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      auto t = __builtin_amdgcn_raw_buffer_load_b128(r, (i + u * kThreads) * 16, 0, 2);
+    for (int u = 0; u < DEPTH; ++u) {
+      auto t = __builtin_amdgcn_raw_buffer_load_b128(r, (i + u * kThreads) * 16, 0, AUX);
       v[u] = *reinterpret_cast<uint4*>(&t);
     }
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
+    for (int u = 0; u < DEPTH; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
   }
   for (; i < n; i += kThreads) {
-    auto t = __builtin_amdgcn_raw_buffer_load_b128(r, i * 16, 0, 2);
+    auto t = __builtin_amdgcn_raw_buffer_load_b128(r, i * 16, 0, AUX);
     uint4 v = *reinterpret_cast<uint4*>(&t);
     acc ^= v.x ^ v.y ^ v.z ^ v.w;
   }
@@ -63,18 +68,21 @@ __global__ __launch_bounds__(kThreads) void stream_read(const char* __restrict__
 // Concurrent two-tier stream (the streaming probe behind the CAP bound of §3:
 // a fixed set of workgroups reads the host tier while the others read HBM).
 // The host workgroups are the first host_wgs multiples of host_stride
-// (stride 1: the first host_wgs workgroups; stride 8: workgroups 0, 8, 16,
-// ..., which the dispatcher places on one XCD when it deals workgroups to
-// the 8 XCDs in turn); they split the host buffer into contiguous slices and
-// the others split the HBM buffer; both walk their slice exactly as
+// (stride 1: the first host_wgs workgroups, which the dispatcher deals to the
+// 8 XCDs in turn; stride 8: workgroups 0, 8, 16, ..., all on one XCD); they
+// split the host buffer into contiguous slices with HD loads per lane in
+// flight and cache policy HAUX, and the others split the HBM buffer as
 // stream_read does.  Thread 0 of every workgroup stores the constant-rate
 // clock at its start and after its last load returned, so the host can tell
 // when each tier's workgroups finished inside the one launch.
+template <int HD, int HAUX>
 __global__ __launch_bounds__(kThreads) void cap_stream(const char* __restrict__ hbm,
                                                        uint64_t hbm_vec,
                                                        const char* __restrict__ host,
                                                        uint64_t host_vec, int host_wgs,
-                                                       int host_stride,
+                                                       int host_stride, uint32_t chunk_vec,
+                                                       int chunk_static,
+                                                       uint32_t* __restrict__ queue,
                                                        uint64_t* __restrict__ clocks,
                                                        uint32_t* __restrict__ sink) {
   const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
@@ -83,16 +91,89 @@ __global__ __launch_bounds__(kThreads) void cap_stream(const char* __restrict__ 
   // the host workgroups before it
   const bool is_host = bid % host_stride == 0 && bid / host_stride < host_wgs;
   const int hosts_before = min(host_wgs, (bid + host_stride - 1) / host_stride);
-  const uint32_t acc = is_host
-                           ? stream_slice(host, host_vec, bid / host_stride, host_wgs)
-                           : stream_slice(hbm, hbm_vec, bid - hosts_before,
-                                          static_cast<int>(gridDim.x) - host_wgs);
+  uint32_t acc = 0;
+  if (is_host) {
+    acc = stream_slice<HD, HAUX>(host, host_vec, bid / host_stride, host_wgs);
+  } else if (chunk_vec == 0) {
+    acc = stream_slice(hbm, hbm_vec, bid - hosts_before, static_cast<int>(gridDim.x) - host_wgs);
+  } else if (chunk_static == 1) {
+    // persistent HBM workers, chunks dealt round robin (no queue)
+    const uint64_t n_chunks = (hbm_vec + chunk_vec - 1) / chunk_vec;
+    const uint64_t workers = static_cast<uint64_t>(gridDim.x) - host_wgs;
+    for (uint64_t c = bid - hosts_before; c < n_chunks; c += workers) {
+      const uint64_t beg = c * chunk_vec;
+      const uint64_t len = hbm_vec - beg < chunk_vec ? hbm_vec - beg : chunk_vec;
+      acc ^= stream_slice(hbm + beg * 16, len, 0, 1);
+    }
+  } else if (chunk_static == 2) {
+    // persistent HBM workers: the first chunk is the worker's own index, the
+    // rest come from a queue whose counter counts past the worker count; the
+    // next chunk is claimed while the current one streams, so the counter's
+    // latency hides behind the loads and the workers never start together
+    __shared__ uint32_t s_next;
+    const uint64_t n_chunks = (hbm_vec + chunk_vec - 1) / chunk_vec;
+    const uint64_t workers = static_cast<uint64_t>(gridDim.x) - host_wgs;
+    uint64_t c = bid - hosts_before;
+    while (c < n_chunks) {
+      uint32_t nxt = 0;
+      if (threadIdx.x == 0)
+        nxt = __hip_atomic_fetch_add(queue, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const uint64_t beg = c * chunk_vec;
+      const uint64_t len = hbm_vec - beg < chunk_vec ? hbm_vec - beg : chunk_vec;
+      acc ^= stream_slice(hbm + beg * 16, len, 0, 1);
+      if (threadIdx.x == 0) s_next = nxt;
+      __syncthreads();
+      c = workers + s_next;
+      __syncthreads();
+    }
+  } else {
+    // persistent HBM workers: chunks of chunk_vec vectors from a queue, so
+    // workers on a slower XCD simply take fewer chunks
+    __shared__ uint32_t s_chunk;
+    const uint64_t n_chunks = (hbm_vec + chunk_vec - 1) / chunk_vec;
+    for (;;) {
+      if (threadIdx.x == 0)
+        s_chunk = __hip_atomic_fetch_add(queue, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __syncthreads();
+      const uint64_t c = s_chunk;
+      __syncthreads();
+      if (c >= n_chunks) break;
+      const uint64_t beg = c * chunk_vec;
+      const uint64_t len = hbm_vec - beg < chunk_vec ? hbm_vec - beg : chunk_vec;
+      acc ^= stream_slice(hbm + beg * 16, len, 0, 1);
+    }
+  }
   __syncthreads();  // every wavefront's loads returned (their values were used)
   if (threadIdx.x == 0) {
-    clocks[2 * bid] = t0;
-    clocks[2 * bid + 1] = __builtin_amdgcn_s_memrealtime();
+    clocks[3 * bid] = t0;
+    clocks[3 * bid + 1] = __builtin_amdgcn_s_memrealtime();
+    // the XCD this workgroup ran on (hardware register XCC_ID, bits 3:0)
+    clocks[3 * bid + 2] = __builtin_amdgcn_s_getreg((3 << 11) | 20) & 0xf;
   }
   if (acc == 0x9e3779b9u) sink[bid] = acc;
+}
+
+typedef void (*CapKernel)(const char*, uint64_t, const char*, uint64_t, int, int, uint32_t,
+                          int, uint32_t*, uint64_t*, uint32_t*);
+
+// Host-load variants: depth 1, 2, 4, 8 loads per lane in flight, times the
+// cache policy (0: non-temporal, as the kernels load; 1: default; 2:
+// system-coherent, sc0 | sc1).
+template <int HD>
+CapKernel cap_kernel_for_policy(int policy) {
+  switch (policy) {
+    case 0: return cap_stream<HD, 2>;
+    case 1: return cap_stream<HD, 0>;
+    default: return cap_stream<HD, 17>;
+  }
+}
+CapKernel cap_kernel(int depth, int policy) {
+  switch (depth) {
+    case 1: return cap_kernel_for_policy<1>(policy);
+    case 2: return cap_kernel_for_policy<2>(policy);
+    case 4: return cap_kernel_for_policy<4>(policy);
+    default: return cap_kernel_for_policy<8>(policy);
+  }
 }
 
 int measure(const void* src, uint64_t bytes, int grid, int iters, uint32_t* sink,
@@ -101,7 +182,7 @@ int measure(const void* src, uint64_t bytes, int grid, int iters, uint32_t* sink
   BOOST_HIP(hipEventCreate(&a));
   BOOST_HIP(hipEventCreate(&b));
   const uint64_t n_vec = bytes / 16;
-  if ((n_vec + grid - 1) / grid * 16 >= (1ull << 31))
+  if (((n_vec + grid - 1) / grid + 63) / 64 * 64 * 16 >= (1ull << 31))
     return bst::fail(BOOST_EINVAL, "slice per workgroup exceeds 2 GiB; raise the grid");
   hipLaunchKernelGGL(stream_read, dim3(grid), dim3(kThreads), 0, 0,
                      static_cast<const char*>(src), n_vec, sink);
@@ -146,98 +227,180 @@ int boost_stream_read_gbps(boost_ctx* ctx, const void* src, uint64_t bytes, int 
 }
 
 int boost_cap_sweep(boost_ctx* ctx, uint64_t hbm_bytes, uint64_t host_bytes, int n_points,
-                    const uint64_t* hbm_use, const int* hbm_wgs, const uint64_t* host_use,
-                    const int* host_wgs, const int* host_stride, int iters,
-                    double* results) {
-  if (!ctx || !hbm_use || !hbm_wgs || !host_use || !host_wgs || !results)
-    return fail(BOOST_EINVAL, "null argument");
+                    const boost_cap_point* pts, int iters, double* results) {
+  if (!ctx || !pts || !results) return fail(BOOST_EINVAL, "null argument");
   if (ctx->device < 0) return fail(BOOST_ENODEV, "plan-only context");
   if (n_points < 1 || iters < 1) return fail(BOOST_EINVAL, "n_points=%d iters=%d", n_points, iters);
   hbm_bytes &= ~4095ull;
   host_bytes &= ~4095ull;
   int max_grid = 1;
-  auto stride = [&](int i) { return host_stride ? host_stride[i] : 1; };
+  bool any_dma = false;
   for (int i = 0; i < n_points; ++i) {
-    if (stride(i) < 1 || stride(i) > 64 ||
-        (host_wgs[i] > 0 && static_cast<int64_t>(host_wgs[i] - 1) * stride(i) >=
-                                static_cast<int64_t>(host_wgs[i]) + hbm_wgs[i]))
+    const boost_cap_point& p = pts[i];
+    if (p.host_stride < 1 || p.host_stride > 64 ||
+        (p.host_wgs > 0 && static_cast<int64_t>(p.host_wgs - 1) * p.host_stride >=
+                               static_cast<int64_t>(p.host_wgs) + p.hbm_wgs))
       return fail(BOOST_EINVAL, "point %d: host stride %d does not fit the grid", i,
-                  stride(i));
-    if (hbm_use[i] > hbm_bytes || host_use[i] > host_bytes || (hbm_use[i] | host_use[i]) % 16 ||
-        hbm_wgs[i] < 0 || host_wgs[i] < 0 || hbm_wgs[i] + host_wgs[i] < 1 ||
-        (hbm_use[i] && !hbm_wgs[i]) || (host_use[i] && !host_wgs[i]) ||
-        hbm_wgs[i] > (1 << 20) || host_wgs[i] > (1 << 20))
+                  p.host_stride);
+    if (p.host_depth != 1 && p.host_depth != 2 && p.host_depth != 4 && p.host_depth != 8)
+      return fail(BOOST_EINVAL, "point %d: host depth %d (1, 2, 4 or 8)", i, p.host_depth);
+    if (p.host_policy < 0 || p.host_policy > 2 || p.dma < 0 || p.dma > 1)
+      return fail(BOOST_EINVAL, "point %d: policy %d dma %d", i, p.host_policy, p.dma);
+    if (p.hbm_chunk_kib < 0 || p.hbm_chunk_kib > (1 << 20) || p.hbm_chunk_kib % 4 ||
+        p.chunk_static < 0 || p.chunk_static > 2)
+      return fail(BOOST_EINVAL, "point %d: HBM chunk %d KiB", i, p.hbm_chunk_kib);
+    if (p.dma && p.host_wgs)
+      return fail(BOOST_EINVAL, "point %d: DMA points read the host bytes by copy, not "
+                  "by workgroups", i);
+    if (p.hbm_bytes > hbm_bytes || p.host_bytes > host_bytes ||
+        (p.hbm_bytes | p.host_bytes) % 16 || p.hbm_wgs < 0 || p.host_wgs < 0 ||
+        p.hbm_wgs + p.host_wgs < 1 || (p.hbm_bytes && !p.hbm_wgs) ||
+        (p.host_bytes && !p.host_wgs && !p.dma) || p.hbm_wgs > (1 << 20) ||
+        p.host_wgs > (1 << 20))
       return fail(BOOST_EINVAL, "point %d: bytes %llu / %llu on %d / %d workgroups", i,
-                  (unsigned long long)hbm_use[i], (unsigned long long)host_use[i], hbm_wgs[i],
-                  host_wgs[i]);
-    if (hbm_wgs[i] && (hbm_use[i] / 16 + hbm_wgs[i] - 1) / hbm_wgs[i] * 16 >= (1ull << 31))
+                  (unsigned long long)p.hbm_bytes, (unsigned long long)p.host_bytes,
+                  p.hbm_wgs, p.host_wgs);
+    if (p.hbm_wgs && ((p.hbm_bytes / 16 + p.hbm_wgs - 1) / p.hbm_wgs + 63) / 64 * 64 * 16 >=
+                         (1ull << 31))
       return fail(BOOST_EINVAL, "point %d: HBM slice exceeds 2 GiB", i);
-    if (host_wgs[i] && (host_use[i] / 16 + host_wgs[i] - 1) / host_wgs[i] * 16 >= (1ull << 31))
+    if (p.host_wgs && ((p.host_bytes / 16 + p.host_wgs - 1) / p.host_wgs + 63) / 64 * 64 * 16 >=
+                          (1ull << 31))
       return fail(BOOST_EINVAL, "point %d: host slice exceeds 2 GiB", i);
-    max_grid = std::max(max_grid, hbm_wgs[i] + host_wgs[i]);
+    max_grid = std::max(max_grid, p.hbm_wgs + p.host_wgs);
+    any_dma = any_dma || p.dma;
   }
   BOOST_HIP(hipSetDevice(ctx->device));
-  Slab dev, host;
+  Slab dev, host, stage;
   int rc = slab_alloc(ctx, std::max<uint64_t>(1, (hbm_bytes + kPage - 1) / kPage), false, dev);
   if (!rc) rc = slab_alloc(ctx, std::max<uint64_t>(1, (host_bytes + kPage - 1) / kPage), true, host);
+  if (!rc && any_dma)
+    rc = slab_alloc(ctx, std::max<uint64_t>(1, (host_bytes + kPage - 1) / kPage), false, stage);
   uint32_t* sink = nullptr;
+  uint32_t* queue = nullptr;
   uint64_t* clocks = nullptr;
-  hipEvent_t ea = nullptr, eb = nullptr;
+  hipEvent_t ea = nullptr, eb = nullptr, ca = nullptr, cb = nullptr;
+  hipStream_t copy_stream = nullptr;
   if (!rc && (hipMalloc(&sink, static_cast<size_t>(max_grid) * 4) != hipSuccess ||
-              hipMalloc(&clocks, static_cast<size_t>(max_grid) * 16) != hipSuccess))
+              hipMalloc(&queue, 256) != hipSuccess ||
+              hipMalloc(&clocks, static_cast<size_t>(max_grid) * 24) != hipSuccess))
     rc = fail(BOOST_ENOMEM, "probe scratch allocation failed");
   if (!rc && hbm_bytes && hipMemset(dev.base, 0x5a, hbm_bytes) != hipSuccess)
     rc = fail(BOOST_EHIP, "memset failed");
   if (!rc && host_bytes) std::memset(host.host_base, 0x5a, host_bytes);
-  if (!rc && (hipEventCreate(&ea) != hipSuccess || hipEventCreate(&eb) != hipSuccess))
+  if (!rc && (hipEventCreate(&ea) != hipSuccess || hipEventCreate(&eb) != hipSuccess ||
+              hipEventCreate(&ca) != hipSuccess || hipEventCreate(&cb) != hipSuccess))
     rc = fail(BOOST_EHIP, "event creation failed");
-  std::vector<uint64_t> clk;
+  // the copy engine's stream (default priority), for the DMA points
+  if (!rc && any_dma && hipStreamCreateWithFlags(&copy_stream, hipStreamNonBlocking) != hipSuccess)
+    rc = fail(BOOST_EHIP, "stream creation failed");
+  std::vector<uint64_t> clk, ends;
   for (int i = 0; i < n_points && !rc; ++i) {
-    const int grid = hbm_wgs[i] + host_wgs[i];
+    const boost_cap_point& p = pts[i];
+    const int grid = p.hbm_wgs + p.host_wgs;
+    const CapKernel kern = cap_kernel(p.host_depth, p.host_policy);
+    const uint32_t chunk_vec = static_cast<uint32_t>(p.hbm_chunk_kib) * 64u;  // 16 B vectors
+    // the queue starts empty for every launch (plain stream order, no graph),
+    // cleared before the launch's first event
+    auto reset = [&]() { return hipMemsetAsync(queue, 0, 4, 0); };
     auto launch = [&]() {
-      hipLaunchKernelGGL(cap_stream, dim3(grid), dim3(kThreads), 0, 0,
-                         static_cast<const char*>(dev.base), hbm_use[i] / 16,
-                         static_cast<const char*>(host.base), host_use[i] / 16, host_wgs[i],
-                         stride(i), clocks, sink);
+      hipLaunchKernelGGL(kern, dim3(grid), dim3(kThreads), 0, 0,
+                         static_cast<const char*>(dev.base), p.hbm_bytes / 16,
+                         static_cast<const char*>(host.base), p.dma ? 0 : p.host_bytes / 16,
+                         p.host_wgs, p.host_stride, chunk_vec, p.chunk_static, queue, clocks,
+                         sink);
     };
-    launch();  // warm-up
-    hipError_t e = hipEventRecord(ea, 0);
-    for (int it = 0; it < iters && e == hipSuccess; ++it) launch();
-    if (e == hipSuccess) e = hipGetLastError();
-    if (e == hipSuccess) e = hipEventRecord(eb, 0);
-    if (e == hipSuccess) e = hipEventSynchronize(eb);
-    float ms = 0;
-    if (e == hipSuccess) e = hipEventElapsedTime(&ms, ea, eb);
-    clk.assign(2 * static_cast<size_t>(grid), 0);
-    if (e == hipSuccess)
-      e = hipMemcpy(clk.data(), clocks, clk.size() * sizeof(uint64_t), hipMemcpyDeviceToHost);
+    // a DMA point: each launch runs beside a host -> HBM copy of the host
+    // bytes on the copy stream, both started together
+    auto copy = [&]() -> hipError_t {
+      return hipMemcpyAsync(stage.base, host.host_base, p.host_bytes, hipMemcpyHostToDevice,
+                            copy_stream);
+    };
+    hipError_t e = reset();
+    if (e == hipSuccess) launch();  // warm-up
+    if (e == hipSuccess && p.dma && p.host_bytes) e = copy();
+    if (e == hipSuccess) e = hipDeviceSynchronize();
+    // per launch: event time, copy time, and from the workgroup clocks the
+    // HBM span, the host span, the median HBM workgroup's end and the whole
+    // span; each result is the median over the launches
+    std::vector<double> t_launch, t_copy, s_hbm, s_host, s_med, s_all, s_xcd[8];
+    for (int it = 0; it < iters && e == hipSuccess; ++it) {
+      float one = 0, one_copy = 0;
+      e = reset();
+      if (e == hipSuccess) e = hipEventRecord(ea, 0);
+      if (e == hipSuccess && p.dma && p.host_bytes) e = hipEventRecord(ca, copy_stream);
+      if (e == hipSuccess && p.dma && p.host_bytes) e = copy();
+      if (e == hipSuccess) launch();
+      if (e == hipSuccess) e = hipGetLastError();
+      if (e == hipSuccess) e = hipEventRecord(eb, 0);
+      if (e == hipSuccess && p.dma && p.host_bytes) e = hipEventRecord(cb, copy_stream);
+      if (e == hipSuccess) e = hipDeviceSynchronize();
+      if (e == hipSuccess) e = hipEventElapsedTime(&one, ea, eb);
+      if (e == hipSuccess && p.dma && p.host_bytes) e = hipEventElapsedTime(&one_copy, ca, cb);
+      clk.assign(3 * static_cast<size_t>(grid), 0);
+      if (e == hipSuccess)
+        e = hipMemcpy(clk.data(), clocks, clk.size() * sizeof(uint64_t), hipMemcpyDeviceToHost);
+      if (e != hipSuccess) break;
+      uint64_t t0 = UINT64_MAX, end_host = 0, end_hbm = 0;
+      ends.clear();
+      uint64_t xcd_end[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+      for (int b = 0; b < grid; ++b) t0 = std::min(t0, clk[3 * b]);
+      for (int b = 0; b < grid; ++b) {
+        const bool is_host = b % p.host_stride == 0 && b / p.host_stride < p.host_wgs;
+        uint64_t& end = is_host ? end_host : end_hbm;
+        end = std::max(end, clk[3 * b + 1]);
+        if (!is_host) {
+          ends.push_back(clk[3 * b + 1]);
+          uint64_t& xe = xcd_end[clk[3 * b + 2] & 7];
+          xe = std::max(xe, clk[3 * b + 1]);
+        }
+      }
+      auto us = [&](uint64_t t) { return t > t0 ? (t - t0) / kRealtimeHz * 1e6 : 0.0; };
+      if (!ends.empty()) {
+        std::nth_element(ends.begin(), ends.begin() + ends.size() / 2, ends.end());
+        s_med.push_back(us(ends[ends.size() / 2]));
+      }
+      for (int x = 0; x < 8; ++x) s_xcd[x].push_back(us(xcd_end[x]));
+      t_launch.push_back(one * 1e3);
+      t_copy.push_back(one_copy * 1e3);
+      s_hbm.push_back(us(end_hbm));
+      s_host.push_back(us(end_host));
+      s_all.push_back(us(std::max(end_hbm, end_host)));
+    }
     if (e != hipSuccess) {
       rc = fail(BOOST_EHIP, "probe point %d: %s", i, hipGetErrorString(e));
       break;
     }
-    // clocks of the last pass: each tier's span from the launch's first start
-    uint64_t t0 = UINT64_MAX, end_host = 0, end_hbm = 0;
-    for (int b = 0; b < grid; ++b) t0 = std::min(t0, clk[2 * b]);
-    for (int b = 0; b < grid; ++b) {
-      const bool is_host = b % stride(i) == 0 && b / stride(i) < host_wgs[i];
-      uint64_t& end = is_host ? end_host : end_hbm;
-      end = std::max(end, clk[2 * b + 1]);
-    }
-    const double total = static_cast<double>(hbm_use[i] + host_use[i]);
-    double* r = results + 5 * static_cast<size_t>(i);
-    r[0] = total * iters / (ms * 1e-3) / 1e9;  // GB/s of both tiers, launches back to back
-    r[1] = static_cast<double>(ms) * 1e3 / iters;  // us per launch
-    r[2] = hbm_use[i] && end_hbm > t0 ? hbm_use[i] / ((end_hbm - t0) / kRealtimeHz) / 1e9 : 0.0;
-    r[3] = host_use[i] && end_host > t0 ? host_use[i] / ((end_host - t0) / kRealtimeHz) / 1e9
-                                        : 0.0;
-    r[4] = (std::max(end_hbm, end_host) - t0) / kRealtimeHz * 1e6;  // us, first start to last end
+    auto median = [](std::vector<double>& v) {
+      if (v.empty()) return 0.0;
+      std::nth_element(v.begin(), v.begin() + v.size() / 2, v.end());
+      return v[v.size() / 2];
+    };
+    const double launch_us = median(t_launch), copy_us = median(t_copy);
+    const double hbm_us = median(s_hbm), host_us = median(s_host);
+    const double total = static_cast<double>(p.hbm_bytes + p.host_bytes);
+    double* r = results + 16 * static_cast<size_t>(i);
+    r[0] = total / (std::max(launch_us, copy_us) * 1e-6) / 1e9;  // GB/s of both tiers
+    r[1] = launch_us;                                           // us per launch
+    r[2] = p.hbm_bytes && hbm_us > 0 ? p.hbm_bytes / (hbm_us * 1e-6) / 1e9 : 0.0;
+    r[3] = p.dma ? (copy_us > 0 ? p.host_bytes / (copy_us * 1e-6) / 1e9 : 0.0)
+                 : (p.host_bytes && host_us > 0 ? p.host_bytes / (host_us * 1e-6) / 1e9 : 0.0);
+    r[4] = median(s_all);  // us, first start to last end
+    r[5] = median(s_med);  // us from the first start to the median HBM workgroup's end
+    r[6] = copy_us;        // us of the copy (DMA points)
+    r[7] = hbm_us;         // us to the last HBM end
+    for (int x = 0; x < 8; ++x) r[8 + x] = median(s_xcd[x]);  // per XCD
   }
   if (ea) (void)hipEventDestroy(ea);
   if (eb) (void)hipEventDestroy(eb);
+  if (ca) (void)hipEventDestroy(ca);
+  if (cb) (void)hipEventDestroy(cb);
+  if (copy_stream) (void)hipStreamDestroy(copy_stream);
   (void)hipFree(sink);
+  (void)hipFree(queue);
   (void)hipFree(clocks);
   slab_free(dev);
   slab_free(host);
+  slab_free(stage);
   return rc;
 }
 

@@ -42,6 +42,17 @@ def test_plan_only_context():
     bd.boost_shutdown(ctx)
 
 
+def test_cap_sweep_needs_a_device():
+    ctx = bd.boost_init(-1)
+    try:
+        with pytest.raises(bd.BoostError) as e:
+            bd.boost_cap_sweep(ctx, 1 << 20, 1 << 20,
+                               [dict(hbm_bytes=1 << 20, hbm_wgs=4)], 1)
+        assert e.value.code == bd.ENODEV
+    finally:
+        bd.boost_shutdown(ctx)
+
+
 def test_bad_arguments():
     for bad in (0.0, -1.0, 1.5):
         with pytest.raises(bd.BoostError) as e:

@@ -48,6 +48,49 @@ def test_calibration(gpu_ctx):
     assert M == opl.modulus_from_alpha(alpha)
 
 
+def test_cap_probe_points(gpu_ctx):
+    """The concurrent streaming probe: every layout variant runs, reports rates
+    inside the physical range, and rejects points outside its contract."""
+    T, H = 256 << 20, 32 << 20
+    pts = [dict(hbm_bytes=T, hbm_wgs=1024),
+           dict(host_bytes=H, host_wgs=8, host_depth=2),
+           dict(hbm_bytes=T - (4 << 20), hbm_wgs=1024, host_bytes=4 << 20, host_wgs=4,
+                host_depth=1, host_policy=2),
+           dict(hbm_bytes=T - (4 << 20), hbm_wgs=1024, host_bytes=4 << 20, host_wgs=4,
+                host_stride=8, host_policy=1),
+           dict(hbm_bytes=T - (4 << 20), hbm_wgs=1024, host_bytes=4 << 20, dma=1),
+           dict(hbm_bytes=T - (4 << 20) - 16, hbm_wgs=1020, host_bytes=4 << 20, host_wgs=4,
+                host_stride=8, hbm_chunk_kib=256),
+           dict(hbm_bytes=T, hbm_wgs=3000, hbm_chunk_kib=64),
+           dict(hbm_bytes=T - 16, hbm_wgs=1000, hbm_chunk_kib=256, chunk_static=1),
+           dict(hbm_bytes=T - 16, hbm_wgs=1000, host_bytes=4 << 20, host_wgs=8,
+                hbm_chunk_kib=256, chunk_static=2)]
+    r = bd.boost_cap_sweep(gpu_ctx, T, H, pts, 2)
+    assert r.shape == (9, 16)
+    assert 500 < r[7, 2] < 9000 and 500 < r[8, 2] < 9000 and 1 < r[8, 3] < 200
+    # queue-fed HBM workers (a ragged last chunk; more workers than slots)
+    assert 500 < r[5, 2] < 9000 and 1 < r[5, 3] < 200
+    assert 500 < r[6, 2] < 9000
+    # every XCD ran HBM workgroups, none ended after the last one
+    assert np.all(r[0, 8:16] > 0) and np.all(r[0, 8:16] <= r[0, 7] + 1e-6)
+    assert 500 < r[0, 2] < 9000 and r[0, 3] == 0
+    assert 1 < r[1, 3] < 200 and r[1, 2] == 0
+    for i in (2, 3):
+        assert 500 < r[i, 2] < 9000 and 1 < r[i, 3] < 200
+        assert 0 < r[i, 5] <= r[i, 7] <= r[i, 4] + 1e-6
+    assert r[4, 6] > 0 and 1 < r[4, 3] < 200
+    for bad in (dict(hbm_bytes=T, hbm_wgs=16, host_depth=3),
+                dict(hbm_bytes=T, hbm_wgs=16, hbm_chunk_kib=6),
+                dict(hbm_bytes=T, hbm_wgs=16, hbm_chunk_kib=64, chunk_static=3),
+                dict(hbm_bytes=T, hbm_wgs=16, host_bytes=H, host_wgs=1, dma=1),
+                dict(hbm_bytes=T + 16, hbm_wgs=16),
+                dict(hbm_bytes=T, hbm_wgs=4, host_bytes=H, host_wgs=2, host_stride=8),
+                dict(host_bytes=H, host_wgs=0)):
+        with pytest.raises(bd.BoostError) as e:
+            bd.boost_cap_sweep(gpu_ctx, T, H, [bad], 1)
+        assert e.value.code == bd.EINVAL
+
+
 def test_single_layer_parity(gpu_ctx):
     """4096 x 4096 bf16 layer, 16 pages, page 15 on host (M = 16)."""
     w, x = synth.single_layer_inputs()
