@@ -44,6 +44,8 @@ def parse():
     p.add_argument("--host-workers", type=int, default=0)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=15.0)
+    p.add_argument("--ab-pairs", type=int, default=200,
+                   help="interleaved tiered / all-HBM step pairs after the timed steps")
     p.add_argument("--graph", action="store_true",
                    help="replay each step as a captured HIP graph")
     p.add_argument("--pmc-ref", action="store_true",
@@ -53,16 +55,26 @@ def parse():
     p.add_argument("--summarize-pmc", default="",
                    help="summarise the rocprofv3 counter CSVs under this directory "
                         "(per kernel and grid) as JSON on stdout, then exit")
+    p.add_argument("--part", default="chain", choices=("chain", "single", "attention"),
+                   help="tier_counters: which part runs its one tiered call")
+    p.add_argument("--tier-profile", default="",
+                   help="directory holding <part>/ (rocprofv3 counter CSVs of a "
+                        "tier_counters run) and <part>.json (its output) for the parts "
+                        "chain, single, attention: write profiles/tier_counters.json "
+                        "and print its table, then exit")
     p.add_argument("--workload", default="chain8b",
                    choices=("chain8b", "llama70b", "throughput8b", "host_share_sweep",
-                            "cap_probe", "batch_sweep", "placements", "dsr_churn"),
+                            "cap_probe", "batch_sweep", "placements", "dsr_churn",
+                            "tier_counters"),
                    help="chain8b: decode weight chain (default); llama70b: full 70B-"
                         "shaped decode step under a 120 GB HBM weight budget; "
                         "throughput8b: 8B-shaped decode at up to 256 requests under a "
                         "40 GB HBM KV budget; host_share_sweep, batch_sweep, "
-                        "placements, dsr_churn: the follow-up experiments (modulus "
-                        "sweep, batch sensitivity, contrast placements, allocator "
-                        "under Poisson arrivals)")
+                        "placements, dsr_churn, cap_probe: the follow-up experiments "
+                        "(modulus sweep, batch sensitivity, contrast placements, "
+                        "allocator under Poisson arrivals, concurrent streaming "
+                        "probe); tier_counters: one tiered call of --part for a "
+                        "counter run")
     p.add_argument("--no-literal", action="store_true",
                    help="throughput8b: skip the 256-request variant (~115 GB of "
                         "pinned host KV)")
@@ -82,6 +94,8 @@ class Chain:
         self.alg_bytes = 0
         self.host_pages = 0
         self.pages = 0
+        self.hbm_weight_bytes = 0
+        self.host_weight_bytes = 0
         rng = np.random.default_rng(7)
         xs = {}
         for K in sorted({k for _, _, _, k in per_layer} | {head[3]}):
@@ -97,6 +111,9 @@ class Chain:
             tiers = bd.boost_tensor_tiers(t)
             self.host_pages += int(tiers.sum())
             self.pages += n
+            a, b = tensor_tier_bytes(bd, t, nbytes)
+            self.hbm_weight_bytes += a
+            self.host_weight_bytes += b
             del w
             y = torch.empty((1, N), dtype=torch.float32, device="cuda")
             self.ops.append((t, h, N, K, xs[K], y))
@@ -178,6 +195,67 @@ def time_steps(torch, fn, steps):
     return np.array([a.elapsed_time(b) for a, b in ev])
 
 
+def ab_pairs(torch, fn_a, fn_b, pairs):
+    """Interleaved A/B: `pairs` pairs of single steps, the order alternating
+    from pair to pair, each step timed by events on the launching stream.
+    Returns the geometric mean of b/a over the pairs (a's speedup over b)
+    with a 95 % interval (t interval on the log ratios) and the medians."""
+    ta, tb = [], []
+    for i in range(pairs):
+        first, second = (fn_a, fn_b) if i % 2 == 0 else (fn_b, fn_a)
+        t1 = time_steps(torch, first, 1)[0]
+        t2 = time_steps(torch, second, 1)[0]
+        ta.append(t1 if i % 2 == 0 else t2)
+        tb.append(t2 if i % 2 == 0 else t1)
+    ta, tb = np.array(ta), np.array(tb)
+    lr = np.log(tb / ta)
+    half = 1.96 * float(np.std(lr, ddof=1)) / np.sqrt(len(lr))
+    m = float(np.mean(lr))
+    return {"pairs": int(pairs), "speedup_geomean": round(float(np.exp(m)), 5),
+            "ci95": [round(float(np.exp(m - half)), 5), round(float(np.exp(m + half)), 5)],
+            "a_ms_median": round(float(np.median(ta)), 4),
+            "b_ms_median": round(float(np.median(tb)), 4),
+            "speedup_of_medians": round(float(np.median(tb) / np.median(ta)), 5)}
+
+
+def tier_counter_entry(part: str):
+    """The committed counter summary of one tiered call of `part` (chain step,
+    single layer, config-3 attention) from profiles/tier_counters.json, or
+    None when the kernel source changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "tier_counters.json")
+    try:
+        ent = json.load(open(path))[part]
+        src = open(os.path.join(ROOT, "paper_2609_13592_amd", "csrc", ent["source"]),
+                   "rb").read()
+    except (OSError, KeyError, ValueError):
+        return None
+    if hashlib.sha256(src).hexdigest() != ent["source_sha256"]:
+        return None
+    return ent
+
+
+def per_tier(part, ms, placement_hbm, placement_host, modulus=None):
+    """Per-tier achieved GB/s of one call taking `ms`.  Bytes: the committed
+    counters (TCC_EA0_RDREQ_DRAM_32B / TCC_EA0_RDREQ_IO_32B) when they were
+    taken on the current kernel source at the same placement; at another
+    modulus the placement's bytes scaled by the counters' ratio to the
+    placement; without current counters the placement's bytes."""
+    ent = tier_counter_entry(part)
+    if ent and (modulus is None or ent["modulus"] == modulus):
+        hbm, host = ent["hbm_bytes"], ent["host_bytes"]
+        src = f"counters (modulus {ent['modulus']})"
+    elif ent:
+        hbm = placement_hbm * ent["hbm_over_placement"]
+        host = placement_host * (ent["host_over_placement"] or 1.0)
+        src = f"placement x counter ratio taken at modulus {ent['modulus']}"
+    else:
+        hbm, host, src = placement_hbm, placement_host, "placement"
+    return {"hbm_bytes": int(hbm), "host_bytes": int(host),
+            "hbm_gbps": round(hbm / (ms * 1e-3) / 1e9, 1),
+            "host_gbps": round(host / (ms * 1e-3) / 1e9, 3), "bytes_from": src}
+
+
 # ------------------------------------------------------------ single layer
 def single_layer_bench(bd, ctx, torch, bw_hbm, bw_host, reps=200):
     """One bf16 layer W[4096 x 4096] (16 pages) with page 15 on host (M = 16),
@@ -215,15 +293,17 @@ def single_layer_bench(bd, ctx, torch, bw_hbm, bw_host, reps=200):
     bound_us = max(15 * bd.PAGE_BYTES / (bw_hbm * 1e9), bd.PAGE_BYTES / (bw_host * 1e9)) * 1e6
     out["placement_bound_us"] = round(bound_us, 2)
     out["pct_of_placement_bound"] = round(100 * bound_us / out["boost"]["us"], 2)
+    out["per_tier"] = per_tier("single", out["boost"]["us"] * 1e-3, 15 * bd.PAGE_BYTES,
+                               bd.PAGE_BYTES)
     out["host_pages"] = [15]
     return out
 
 
 # --------------------------------------------------------------- attention
-def attention_bench(bd, ctx, torch, M, steps, warmup):
-    """Paged-attention decode, batch 64, 32/8 heads, head_dim 128, context
-    lengths U[512, 4096] (seed 0), K/V ~N(0, 1) bf16, blocks from the
-    wave-aware pool (linear placement at modulus M) vs an all-HBM pool."""
+def attention_setup(bd, ctx, torch, M):
+    """Config-3 inputs: batch 64, 32/8 heads, head_dim 128, context lengths
+    U[512, 4096] (seed 0), K/V ~N(0, 1) bf16, blocks from the wave-aware pool
+    (linear placement at modulus M) and from an all-HBM pool."""
     import synth
     B, Hq, H, D = 64, 32, 8, 128
     lengths = synth.context_lengths(0, B, 512, 4096)
@@ -237,7 +317,6 @@ def attention_bench(bd, ctx, torch, M, steps, warmup):
     q = torch.randn((B, Hq, D), generator=g, device="cuda").to(torch.bfloat16)
     lens = torch.from_numpy(lengths.astype(np.int32)).cuda()
     sp = torch.cuda.current_stream().cuda_stream
-    res = {}
     pools = {}
     for name, mode, m in (("boost", bd.KV_LPP, M), ("hbm", bd.KV_ALL_HBM, 0)):
         pool = bd.boost_kv_pool_create(ctx, 1, H, D, sum(need), m, mode, q_heads=Hq,
@@ -259,6 +338,19 @@ def attention_bench(bd, ctx, torch, M, steps, warmup):
         pool, td, _ = pools[name]
         bd.boost_paged_attn_decode(ctx, pool, 0, q, B, Hq, td, mb, lens, 0.0, out,
                                    bd.DTYPE_F32, sp)
+    alg = total * H * D * 2 * 2 + B * Hq * D * 2 + B * Hq * D * 4
+    st = pools["boost"][2]
+    return {"call": call, "pools": pools, "alg": alg, "stats": st, "B": B, "H": H,
+            "D": D, "lengths": lengths}
+
+
+def attention_bench(bd, ctx, torch, M, steps, warmup):
+    """Paged-attention decode on the config-3 inputs (attention_setup): the
+    wave-aware pool against the all-HBM pool, interleaved."""
+    A = attention_setup(bd, ctx, torch, M)
+    call, pools, alg, st = A["call"], A["pools"], A["alg"], A["stats"]
+    H = A["H"]
+    res = {}
     for _ in range(warmup):
         call("boost")
         call("hbm")
@@ -272,14 +364,14 @@ def attention_bench(bd, ctx, torch, M, steps, warmup):
             b_.record()
             torch.cuda.synchronize()
             ms[name].append(a.elapsed_time(b_))
-    alg = total * H * D * 2 * 2 + B * Hq * D * 2 + B * Hq * D * 4
-    st = pools["boost"][2]
     for name in ("boost", "hbm"):
         t = float(np.median(ms[name]))
         res[name] = {"ms": round(t, 4), "gbps": round(alg / (t * 1e-3) / 1e9, 1)}
     res["host_share"] = round(st["used_host_head_blocks"] / (H * st["used_blocks"]), 5)
     res["shh_requests"] = int(st["shh_requests"])
     res["alg_bytes"] = int(alg)
+    host_kv = int(st["used_host_head_blocks"]) * 16 * A["D"] * 2 * 2   # K and V
+    res["per_tier"] = per_tier("attention", res["boost"]["ms"], alg - host_kv, host_kv, M)
     res["speedup_vs_hbm_only"] = round(res["hbm"]["ms"] / res["boost"]["ms"], 4)
     ach = alg / (res["boost"]["ms"] * 1e-3) / 1e9
     res["roofline"] = {"bound": "hbm", "kernel": "attn_partition + attn_merge",
@@ -335,11 +427,82 @@ def summarize_pmc(directory: str):
     return out
 
 
+TIER_KERNELS = {"chain": (("gemv_kernel", "split_fixup"), "gemv.hip"),
+                "single": (("gemv_kernel", "split_fixup"), "gemv.hip"),
+                "attention": (("attn_partition", "attn_merge"), "attn.hip")}
+
+
+def write_tier_profile(directory: str):
+    """Per-tier bytes of the tiered calls of a tier_counters run, summed over
+    the part's kernels, against the placement's bytes; written to
+    profiles/tier_counters.json with the kernel source's hash."""
+    import hashlib
+    prof = {}
+    lines = ["| part | modulus | kernels | DRAM bytes (counter) | host bytes (counter) | "
+             "HBM bytes (placement) | host bytes (placement) | DRAM / placement | "
+             "host / placement |", "|---|---:|---|---:|---:|---:|---:|---:|---:|"]
+    for part, (names, source) in TIER_KERNELS.items():
+        try:
+            meta = json.load(open(os.path.join(directory, part + ".json")))
+        except OSError:
+            continue
+        summ = summarize_pmc(os.path.join(directory, part))
+        dram = io = 0.0
+        used = set()
+        for key, ent in summ.items():
+            if key.split(" grid=")[0].split("<")[0] in names:
+                used.add(key.split(" grid=")[0].split("<")[0])
+                pd = ent["per_dispatch"]
+                dram += pd.get("TCC_EA0_RDREQ_DRAM_32B", 0.0) * 32 * ent["dispatches"]
+                io += pd.get("TCC_EA0_RDREQ_IO_32B", 0.0) * 32 * ent["dispatches"]
+        if part == "attention":
+            host_p = meta["kv_host_bytes_upper"]
+            hbm_p = meta["kv_bytes"] - host_p
+        else:
+            hbm_p, host_p = meta["weight_hbm_bytes"], meta["weight_host_bytes"]
+        sha = hashlib.sha256(open(os.path.join(ROOT, "paper_2609_13592_amd", "csrc", source),
+                                  "rb").read()).hexdigest()
+        prof[part] = {"source": source, "source_sha256": sha, "modulus": meta["modulus"],
+                      "hbm_bytes": int(round(dram)), "host_bytes": int(round(io)),
+                      "placement_hbm_bytes": int(hbm_p), "placement_host_bytes": int(host_p),
+                      "hbm_over_placement": round(dram / hbm_p, 5),
+                      "host_over_placement": round(io / host_p, 5) if host_p else None}
+        lines.append(f"| {part} | {meta['modulus']} | {', '.join(sorted(used))} | {dram:,.0f} | "
+                     f"{io:,.0f} | {hbm_p:,} | {host_p:,} | {dram / hbm_p:.5f} | "
+                     + (f"{io / host_p:.5f} |" if host_p else "- |"))
+    with open(os.path.join(ROOT, "profiles", "tier_counters.json"), "w") as fh:
+        json.dump(prof, fh, indent=1)
+        fh.write("\n")
+    print("\n".join(lines))
+
+
 # ----------------------------------------------------------- CPU baseline
-def cpu_baseline(seconds: float):
+def host_topology():
+    """Logical CPUs and the sockets x cores x threads of the host (lscpu)."""
+    import subprocess
+    topo = {"logical_cpus": os.cpu_count()}
+    try:
+        txt = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        keys = {"Socket(s)": "sockets", "Core(s) per socket": "cores_per_socket",
+                "Thread(s) per core": "threads_per_core", "Model name": "model"}
+        for line in txt.splitlines():
+            k, _, v = line.partition(":")
+            if k.strip() in keys:
+                v = v.strip()
+                topo[keys[k.strip()]] = int(v) if v.isdigit() else v
+    except (OSError, subprocess.SubprocessError):
+        pass
+    try:
+        topo["affinity_cpus"] = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        pass
+    return topo
+
+
+def _oracle_gemv_rate(seconds: float):
     """The oracle GEMV (fp32 accumulation over bf16 weights decoded on the
-    fly) over layer 0 of the same chain, repeated until about `seconds` of
-    CPU work; reported as effective GB/s of algorithmic bytes."""
+    fly) over layer 0 of the chain, repeated until about `seconds` of CPU
+    work: (GB/s of algorithmic bytes, passes, bytes, seconds)."""
     import synth
     from oracle import gemv as og
     per_layer, _ = synth.chain_shapes(synth.LLAMA8B)
@@ -354,16 +517,26 @@ def cpu_baseline(seconds: float):
             spent += time.perf_counter() - t0
             done_bytes += w.nbytes + x.nbytes + w.shape[0] * 4
         passes += 1
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max((i.get("num_threads") or 1) for i in threadpool_info()) or 1
-    except Exception:
-        cores = os.cpu_count() or 1
-    return {"value": round(done_bytes / spent / 1e9, 3), "unit": "GB/s",
-            "cores": int(cores), "kind": "oracle",
+    return done_bytes / spent / 1e9, passes, done_bytes, spent
+
+
+def cpu_baseline(seconds: float):
+    """The oracle on the host cores: the same chain's layer 0 (4 tensors) with
+    every BLAS thread the process gets, then with one thread; reported as
+    effective GB/s of algorithmic bytes."""
+    from threadpoolctl import threadpool_info, threadpool_limits
+    threads = max([(i.get("num_threads") or 1) for i in threadpool_info()] or [1])
+    rate, passes, nbytes, spent = _oracle_gemv_rate(seconds)
+    with threadpool_limits(limits=1):
+        rate1, passes1, nbytes1, spent1 = _oracle_gemv_rate(seconds / 3)
+    return {"value": round(rate, 3), "unit": "GB/s", "cores": int(threads), "kind": "oracle",
             "sample": f"oracle fp32 GEMV over layer 0 of the same chain (4 tensors, "
-                      f"{passes} passes, {done_bytes / 1e9:.2f} GB), "
-                      f"{spent:.1f} s of compute"}
+                      f"{passes} passes, {nbytes / 1e9:.2f} GB), {spent:.1f} s of compute "
+                      f"on {threads} BLAS threads",
+            "single_thread": {"value": round(rate1, 3), "unit": "GB/s", "cores": 1,
+                              "sample": f"{passes1} passes, {nbytes1 / 1e9:.2f} GB, "
+                                        f"{spent1:.1f} s"},
+            "host": host_topology()}
 
 
 # ------------------------------------------------------ 70B full decode step
@@ -1009,6 +1182,61 @@ def cap_probe(args, bd, ctx, torch, bw_hbm, bw_host, alpha, M_alpha):
             "results": out}
 
 
+def tensor_tier_bytes(bd, t, nbytes):
+    """(HBM bytes, host bytes) of a placed tensor, from its tier map."""
+    tiers = bd.boost_tensor_tiers(t)
+    sizes = np.minimum(bd.PAGE_BYTES, nbytes - np.arange(len(tiers)) * bd.PAGE_BYTES)
+    host = int(sizes[tiers == 1].sum())
+    return nbytes - host, host
+
+
+def tier_counters_run(args, bd, ctx, torch, M):
+    """One tiered call of one part of the default bench, for a counter run
+    (rocprofv3 --pmc TCC_EA0_RDREQ_DRAM_32B TCC_EA0_RDREQ_IO_32B): `chain` one
+    step of the 129 GEMVs, `single` the 4096 x 4096 layer with page 15 on
+    host, `attention` the config-3 paged attention on the wave-aware pool.
+    Prints the placement's bytes per tier, which the counters must match."""
+    sp = torch.cuda.current_stream().cuda_stream
+    out = {"part": args.part, "modulus": M}
+    if args.part == "chain":
+        chain = Chain(bd, ctx, torch, args.layers, M)
+        hbm = host = 0
+        for t, h, N, K, x, y in chain.ops:
+            a, b = tensor_tier_bytes(bd, t, N * K * 2)
+            hbm, host = hbm + a, host + b
+        torch.cuda.synchronize()
+        chain.run("boost", sp)
+        torch.cuda.synchronize()
+        out.update(weight_hbm_bytes=hbm, weight_host_bytes=host, launches=len(chain.ops))
+        chain.free()
+    elif args.part == "single":
+        import synth
+        w, x = synth.single_layer_inputs()
+        t = bd.boost_place_weights(ctx, w, w.nbytes, 16)
+        xd = torch.from_numpy(x.view(np.int16)).cuda()
+        y = torch.empty((1, 4096), dtype=torch.float32, device="cuda")
+        a, b = tensor_tier_bytes(bd, t, w.nbytes)
+        torch.cuda.synchronize()
+        bd.boost_decode_gemv(ctx, t, 4096, 4096, xd, 1, y, bd.DTYPE_F32, sp)
+        torch.cuda.synchronize()
+        bd.boost_tensor_free(t)
+        out.update(weight_hbm_bytes=a, weight_host_bytes=b, launches=1)
+    else:
+        A = attention_setup(bd, ctx, torch, M)
+        st = A["stats"]
+        torch.cuda.synchronize()
+        A["call"]("boost")
+        torch.cuda.synchronize()
+        # K and V bytes on host: host head-blocks in use, 16 tokens of D bf16
+        # each, for K and for V (upper bound: a request's last block is
+        # partly empty)
+        host = int(st["used_host_head_blocks"]) * 16 * A["D"] * 2 * 2
+        out.update(kv_bytes=A["alg"], kv_host_bytes_upper=host, launches=1)
+        for pool, _, _ in A["pools"].values():
+            bd.boost_kv_pool_destroy(pool)
+    return out
+
+
 def batch_sweep(args, bd, ctx, torch, bw_hbm, bw_host, alpha, M):
     """Tiered (modulo placement at the measured modulus) vs all-HBM GEMV/GEMM
     time as the batch grows (the batch sensitivity study of §5.10): the
@@ -1359,6 +1587,9 @@ def main():
     if args.summarize_pmc:
         print(json.dumps(summarize_pmc(args.summarize_pmc), indent=1))
         return
+    if args.tier_profile:
+        write_tier_profile(args.tier_profile)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); "
               "the library has no multi-GPU path.", file=sys.stderr)
@@ -1388,6 +1619,11 @@ def main():
            "dsr_churn": lambda: dsr_churn(args, bd, ctx, torch, bw_hbm, bw_host, alpha, M)}
     if args.workload in exp:
         out = exp[args.workload]()
+        bd.boost_shutdown(ctx)
+        print(json.dumps(out), flush=True)
+        return
+    if args.workload == "tier_counters":
+        out = tier_counters_run(args, bd, ctx, torch, M)
         bd.boost_shutdown(ctx)
         print(json.dumps(out), flush=True)
         return
@@ -1453,6 +1689,27 @@ def main():
     bytes_per_launch = chain.alg_bytes / launches
     achieved = bytes_per_launch / (avg_launch_ms * 1e-3) / 1e9
 
+    log("step: A/B pairs")
+    ab = ab_pairs(torch, lambda: step("boost"), lambda: step("hbm"), args.ab_pairs)
+    # the tensors that hold host pages, timed alone (tiered and all-HBM): the
+    # host tier's rate over the launches that read it
+    host_ops = [op for op in chain.ops if tensor_tier_bytes(bd, op[0], op[2] * op[3] * 2)[1]]
+    host_ops_t = None
+    if host_ops:
+        def run_ops(which):
+            for t, h, N, K, x, y in host_ops:
+                bd.boost_decode_gemv(ctx, t if which == "boost" else h, N, K, x, 1, y,
+                                     bd.DTYPE_F32, sp)
+        lh = ab_pairs(torch, lambda: run_ops("boost"), lambda: run_ops("hbm"), 50)
+        hb = sum(tensor_tier_bytes(bd, op[0], op[2] * op[3] * 2)[0] for op in host_ops)
+        hh = sum(tensor_tier_bytes(bd, op[0], op[2] * op[3] * 2)[1] for op in host_ops)
+        host_ops_t = {"tensors": len(host_ops), "ms": lh["a_ms_median"],
+                      "hbm_only_ms": lh["b_ms_median"],
+                      "speedup_vs_hbm_only": lh["speedup_geomean"], "ci95": lh["ci95"],
+                      "hbm_gbps": round(hb / (lh["a_ms_median"] * 1e-3) / 1e9, 1),
+                      "host_gbps": round(hh / (lh["a_ms_median"] * 1e-3) / 1e9, 2),
+                      "host_bytes": int(hh)}
+
     log("step: attention")
     attn = attention_bench(bd, ctx, torch, M, max(10, args.steps), 3)
     log("step: single layer")
@@ -1496,7 +1753,13 @@ def main():
         "pct_combined_roofline": round(100 * eff / (bw_hbm + bw_host), 2),
         "hbm_only": {"ms_per_step": round(ms_hbm, 4), "value": round(eff_hbm, 2),
                      "pct_of_hbm_roofline": round(100 * eff_hbm / bw_hbm, 2)},
-        "speedup_vs_hbm_only": round(ms_hbm / ms, 4),
+        "speedup_vs_hbm_only": ab["speedup_geomean"],
+        "speedup_vs_hbm_only_ci95": ab["ci95"],
+        "ab_pairs": ab,
+        "speedup_vs_hbm_only_timed_region": round(ms_hbm / ms, 4),
+        "per_tier": {"step": per_tier("chain", ms, chain.hbm_weight_bytes,
+                                      chain.host_weight_bytes, M),
+                     "tensors_with_host_pages": host_ops_t},
         "prefetch": {"ms_per_step": round(ms_pre, 4),
                      "value": round(chain.alg_bytes / (ms_pre * 1e-3) / 1e9, 2),
                      "staged_tensors": len(chain.staged),
