@@ -341,7 +341,7 @@ def attention_setup(bd, ctx, torch, M):
     alg = total * H * D * 2 * 2 + B * Hq * D * 2 + B * Hq * D * 4
     st = pools["boost"][2]
     return {"call": call, "pools": pools, "alg": alg, "stats": st, "B": B, "H": H,
-            "D": D, "lengths": lengths}
+            "D": D, "lengths": lengths, "out": out}
 
 
 def attention_bench(bd, ctx, torch, M, steps, warmup):

@@ -195,8 +195,16 @@ __device__ __forceinline__ void consume(const uint32_t (*qp)[4], const uint4* kb
   }
 }
 
+// Waves per SIMD the register allocator targets for G <= 4: three (168
+// registers, no spill) against the two it picks by itself took config 3 from
+// 136 to 126 us; four spill and run at 306 us.  G = 8 keeps the allocator's
+// own choice (a tighter target spills its accumulators).
+#ifndef BOOST_ATTN_WAVES
+#define BOOST_ATTN_WAVES 3
+#endif
 template <int G>
-__global__ __launch_bounds__(kThreads) void attn_partition(AttnParams P) {
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(
+    G == 8 ? 1 : BOOST_ATTN_WAVES))) void attn_partition(AttnParams P) {
   constexpr int kUnroll = G == 8 ? BOOST_ATTN_UNROLL8 : BOOST_ATTN_UNROLL;  // blocks in flight
   __shared__ float s_ml[4][G][2];
   __shared__ float s_acc[4][G][kD];
@@ -233,8 +241,12 @@ __global__ __launch_bounds__(kThreads) void attn_partition(AttnParams P) {
   const int nbp = min(n_blk, blk_beg + P.part_blocks) - blk_beg;
   // leading blocks whose 16 tokens are all inside the context
   const int nfull = max(0, min(nbp, L / kT - blk_beg));
-  const int32_t* row = P.tables + static_cast<int64_t>(b) * P.max_blocks + blk_beg;
   const uint64_t head_off = static_cast<uint64_t>(g) * P.nb * (kT * kD * 2);
+  // the partition's block ids, read once into LDS: a load per block from
+  // memory would put a round trip before every group of K/V loads
+  __shared__ int32_t row[kMaxPartBlocks];
+  if (tid < nbp) row[tid] = P.tables[static_cast<int64_t>(b) * P.max_blocks + blk_beg + tid];
+  __syncthreads();
 
   // q stays in bf16 pairs for the dot2 instruction
   uint32_t qp[G][4];
@@ -286,11 +298,17 @@ __global__ __launch_bounds__(kThreads) void attn_partition(AttnParams P) {
     else
       consume<G, kUnroll, true>(qp, kb, vb, valid, sc2, m, l, acc);
   }
-  for (; i < nbp; ++i) {  // remaining blocks, the last one possibly partial
-    uint4 kb[1], vb[1];
-    const bool ok = fetch(i, kb[0], vb[0]);
-    const bool v1[1] = {ok && (blk_beg + i) * kT + ts < L};
-    consume<G, 1, true>(qp, kb, vb, v1, sc2, m, l, acc);
+  if (i < nbp) {  // the rest (fewer than kUnroll full blocks, then a partial
+                  // one: at most kUnroll blocks), loaded together and masked
+    uint4 kb[kUnroll], vb[kUnroll];
+    bool valid[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const bool ok = i + u < nbp && fetch(i + u, kb[u], vb[u]);
+      if (i + u >= nbp) kb[u] = vb[u] = make_uint4(0, 0, 0, 0);
+      valid[u] = ok && (blk_beg + i + u) * kT + ts < L;
+    }
+    consume<G, kUnroll, true>(qp, kb, vb, valid, sc2, m, l, acc);
   }
 
   // merge the 4 slots of a wavefront (lanes 16 and 32 apart hold the same dims)
