@@ -36,8 +36,10 @@ constexpr int kLanesTok = kD / 8;  // lanes per token row (16)
 #ifndef BOOST_ATTN_UNROLL
 #define BOOST_ATTN_UNROLL 4
 #endif
+// Work items a launch aims for (partition size follows; config 3: 2048
+// items of 64 blocks ran 120 us against 122 us with 4096 of 32)
 #ifndef BOOST_ATTN_ITEMS
-#define BOOST_ATTN_ITEMS 4096
+#define BOOST_ATTN_ITEMS 2048
 #endif
 #ifndef BOOST_ATTN_UNROLL8
 #define BOOST_ATTN_UNROLL8 BOOST_ATTN_UNROLL
@@ -195,12 +197,111 @@ __device__ __forceinline__ void consume(const uint32_t (*qp)[4], const uint4* kb
   }
 }
 
+// Head-distributed softmax for G = 2 and 4.  The G partial dot products of a
+// lane (its 8 dimensions of one token, every query head) are reduced over
+// the token's 16 lanes by a transposing butterfly: exchange with the lane
+// xor 1 (and xor 2 for G = 4) keeping half the heads each time, then add the
+// lanes 4 and 8 apart, so each lane ends with the full score of ONE head
+// (head_of_lane) instead of every lane holding all G.  The running maximum,
+// the exponentials and the running sum are then computed once per head and
+// token instead of 16 times; the probabilities and rescale factors reach the
+// other lanes' accumulators by quad broadcasts.  Same online softmax as
+// consume(), fewer vector instructions per block.
+template <int G>
+__device__ __forceinline__ int head_of_lane(int lane) {
+  const int i = lane & 3;
+  return G == 4 ? 2 * (i & 1) + (i >> 1) : (i & 1);
+}
+// the lane of a quad that holds head j (the map is its own inverse)
+template <int G>
+constexpr int lane_of_head(int j) { return G == 4 ? 2 * (j & 1) + (j >> 1) : j; }
+// value of quad lane k, in every lane of the quad
+template <int K>
+__device__ __forceinline__ float quad_bcast(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), K * 0x55, 0xf, 0xf, true));
+}
+template <int G, int J = 0>
+__device__ __forceinline__ void bcast_heads(float v, float* out) {
+  if constexpr (J < G) {
+    out[J] = quad_bcast<lane_of_head<G>(J)>(v);
+    bcast_heads<G, J + 1>(v, out);
+  }
+}
+
+template <int G>
+__device__ __forceinline__ float score_of_lane_head(const float* d, bool b0, bool b1) {
+  float f;
+  if constexpr (G == 4) {
+    // xor 1: lanes with bit 0 clear keep heads 0, 1; set keep 2, 3
+    const float k0 = b0 ? d[2] : d[0], k1 = b0 ? d[3] : d[1];
+    const float s0 = b0 ? d[0] : d[2], s1 = b0 ? d[1] : d[3];
+    const float e0 = k0 + dpp<0xb1>(s0), e1 = k1 + dpp<0xb1>(s1);
+    // xor 2: bit 1 clear keeps the first of the pair, set the second
+    f = (b1 ? e1 : e0) + dpp<0x4e>(b1 ? e0 : e1);
+  } else {
+    f = (b0 ? d[1] : d[0]) + dpp<0xb1>(b0 ? d[0] : d[1]);
+    f += dpp<0x4e>(f);
+  }
+  f += dpp<0x124>(f);  // row_ror 4: the next quad of the 16-lane row
+  f += dpp<0x128>(f);  // row_ror 8: the other half of the row
+  return f;
+}
+
+template <int G, int U, bool MASKED>
+__device__ __forceinline__ void consume_hd(const uint32_t (*qp)[4], const uint4* kb,
+                                           const uint4* vb, const bool* valid, float sc2,
+                                           bool b0, bool b1, float& mh, float& lh,
+                                           float (*acc)[8]) {
+  float s[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    float d[G];
+#pragma unroll
+    for (int j = 0; j < G; ++j) {
+      float x = dot2(qp[j][0], kb[u].x, 0.f);
+      x = dot2(qp[j][1], kb[u].y, x);
+      x = dot2(qp[j][2], kb[u].z, x);
+      d[j] = dot2(qp[j][3], kb[u].w, x);
+    }
+    const float f = score_of_lane_head<G>(d, b0, b1) * sc2;
+    s[u] = (!MASKED || valid[u]) ? f : -INFINITY;
+  }
+  float mc = mh;
+#pragma unroll
+  for (int u = 0; u < U; ++u) mc = fmaxf(mc, s[u]);
+  // nothing valid yet for this head: keep the state (factor 1)
+  const float c = (MASKED && mc == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f(mh - mc);
+  lh *= c;
+  mh = mc;
+  float cj[G];
+  bcast_heads<G>(c, cj);
+#pragma unroll
+  for (int j = 0; j < G; ++j)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[j][e] *= cj[j];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const float p = (MASKED && s[u] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(s[u] - mh);
+    lh += p;
+    float pj[G], vf[8];
+    bcast_heads<G>(p, pj);
+    unpack8(vb[u], vf);
+#pragma unroll
+    for (int j = 0; j < G; ++j)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[j][e] = fmaf(pj[j], vf[e], acc[j][e]);
+  }
+}
+
 // Waves per SIMD the register allocator targets for G <= 4: three (168
 // registers, no spill) against the two it picks by itself took config 3 from
 // 136 to 126 us; four spill and run at 306 us.  G = 8 keeps the allocator's
 // own choice (a tighter target spills its accumulators).
 #ifndef BOOST_ATTN_WAVES
 #define BOOST_ATTN_WAVES 3
+#endif
+#ifndef BOOST_ATTN_HD
+#define BOOST_ATTN_HD 1
 #endif
 template <int G>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(
@@ -268,6 +369,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[j][e] = 0.f;
   }
+  // head-distributed state (G = 2, 4): this lane's head's maximum and sum
+  constexpr bool kHD = BOOST_ATTN_HD && (G == 2 || G == 4);
+  const bool b0 = tid & 1, b1 = tid & 2;
+  float mh = -INFINITY, lh = 0.f;
 
   const uint32_t lane_off = static_cast<uint32_t>(tid) * 16;
   // address of head-block (g, blk) of K and V: uniform scalar arithmetic
@@ -293,10 +398,17 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(
       valid[u] = fetch(i + u, kb[u], vb[u]);
       all_ok = all_ok && valid[u];
     }
-    if (all_ok)
-      consume<G, kUnroll, false>(qp, kb, vb, valid, sc2, m, l, acc);
-    else
-      consume<G, kUnroll, true>(qp, kb, vb, valid, sc2, m, l, acc);
+    if constexpr (kHD) {
+      if (all_ok)
+        consume_hd<G, kUnroll, false>(qp, kb, vb, valid, sc2, b0, b1, mh, lh, acc);
+      else
+        consume_hd<G, kUnroll, true>(qp, kb, vb, valid, sc2, b0, b1, mh, lh, acc);
+    } else {
+      if (all_ok)
+        consume<G, kUnroll, false>(qp, kb, vb, valid, sc2, m, l, acc);
+      else
+        consume<G, kUnroll, true>(qp, kb, vb, valid, sc2, m, l, acc);
+    }
   }
   if (i < nbp) {  // the rest (fewer than kUnroll full blocks, then a partial
                   // one: at most kUnroll blocks), loaded together and masked
@@ -308,7 +420,14 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(
       if (i + u >= nbp) kb[u] = vb[u] = make_uint4(0, 0, 0, 0);
       valid[u] = ok && (blk_beg + i + u) * kT + ts < L;
     }
-    consume<G, kUnroll, true>(qp, kb, vb, valid, sc2, m, l, acc);
+    if constexpr (kHD)
+      consume_hd<G, kUnroll, true>(qp, kb, vb, valid, sc2, b0, b1, mh, lh, acc);
+    else
+      consume<G, kUnroll, true>(qp, kb, vb, valid, sc2, m, l, acc);
+  }
+  if constexpr (kHD) {  // every head's maximum and sum in every lane again
+    bcast_heads<G>(mh, m);
+    bcast_heads<G>(lh, l);
   }
 
   // merge the 4 slots of a wavefront (lanes 16 and 32 apart hold the same dims)
