@@ -695,15 +695,15 @@ constexpr int dma_stages() {
                                                                   : kDmaLds / dma_stage_bytes<BT, RT>();
 }
 
-// Row groups of the 2-D arrangement of the four wavefronts over a unit's
+// Row groups of the 2-D arrangement of the NW wavefronts over a unit's
 // 4 RT row tiles and BT batch tiles: the one that reads the fewest fragments
-// per 32-column step (4 RT / WR + BT / (4 / WR)), ties to more row groups
-template <int BT, int RT>
+// per 32-column step (4 RT / WR + BT / (NW / WR)), ties to more row groups
+template <int BT, int RT, int NW = 4>
 constexpr int dma_wave_rows() {
-  int best = 4, cost = RT + BT;
-  for (int wr : {2, 1}) {
-    const int wb = 4 / wr;
-    if (BT % wb) continue;
+  int best = -1, cost = 1 << 30;
+  for (int wr = NW; wr >= 1; wr /= 2) {
+    const int wb = NW / wr;
+    if ((4 * RT) % wr || BT % wb) continue;
     const int c = 4 * RT / wr + BT / wb;
     if (c < cost) best = wr, cost = c;
   }
@@ -718,14 +718,15 @@ using bst::vmcnt_imm;
 // far longer than HBM's, spreads over 4 RT times more workgroups; every
 // output still sums the same columns in the same order, so the results do
 // not depend on which pages are on the host.
-template <int BT, int RT, bool HOST = false>
+template <int BT, int RT, bool HOST = false, int NW = 4>
 __device__ __forceinline__ void gemm_dma_unit(const GemvParams& P, int page_in, int unit_in,
                                               char* ring) {
-  static_assert(BT % 2 == 0, "x blocks are spread evenly over the four wavefronts");
+  static_assert((2 * BT) % NW == 0, "x blocks are spread evenly over the wavefronts");
+  static_assert((8 * RT) % NW == 0, "W blocks are spread evenly over the wavefronts");
   constexpr int kNs = dma_stages<BT, RT>();
   constexpr int kSb = dma_stage_bytes<BT, RT>();
-  constexpr int kXq = BT / 2;              // x blocks loaded per wavefront and stage
-  constexpr int kWq = HOST ? 1 : 2 * RT;   // W blocks loaded per wavefront and stage
+  constexpr int kXq = 2 * BT / NW;            // x blocks loaded per wavefront and stage
+  constexpr int kWq = HOST ? 1 : 8 * RT / NW;  // W blocks loaded per wavefront and stage
   constexpr int kLoads = kWq + kXq;        // load instructions per wavefront and stage
   static_assert(kNs >= 2, "ring of at least two stages");
   const int page = __builtin_amdgcn_readfirstlane(page_in);
@@ -760,18 +761,19 @@ __device__ __forceinline__ void gemm_dma_unit(const GemvParams& P, int page_in, 
   // loads: lane i of an instruction for block b fetches row i / 8 of the
   // block and the chunk it stores at position i % 8, i.e. chunk
   // (i % 8) ^ (i / 8) ^ (b & 1); W blocks 2 T + h (tile T, rows 8 h ..),
-  // x blocks 8 RT + 4 q + wave (an even base: parity of wave).  A host
-  // sub-unit has one tile: wavefronts 0 and 1 load its blocks 0 and 1, and
-  // 2 and 3 issue an out-of-range load into the unused block 2, so every
-  // wavefront issues the same number of loads per stage.
+  // wavefront w loading blocks w kWq .. w kWq + kWq - 1; x blocks
+  // 8 RT + NW q + wave (an even base: parity of wave).  A host sub-unit has
+  // one tile: wavefronts 0 and 1 load its blocks 0 and 1, and the others
+  // issue an out-of-range load into the unused block 2, so every wavefront
+  // issues the same number of loads per stage.
   const int brow = lane >> 3;
   const int c0 = (lane & 7) ^ brow;  // chunk at parity 0; parity 1: c0 ^ 1
   uint32_t ro[kWq];
   int wblk[kWq], wpar[kWq];
 #pragma unroll
   for (int i = 0; i < kWq; ++i) {
-    const int h = HOST ? (wave & 1) : (i & 1);
-    const int blk = HOST ? min(wave, 2) : 2 * (wave * RT + i / 2) + h;
+    const int blk = HOST ? min(wave, 2) : wave * kWq + i;
+    const int h = HOST ? (wave & 1) : (blk & 1);
     const int64_t r = rbase + 8 * blk + brow;  // block blk holds rows 8 blk ..
     const bool live = !HOST || wave < 2;
     ro[i] = (!live || r > r_hi) ? kOOB
@@ -783,7 +785,7 @@ __device__ __forceinline__ void gemm_dma_unit(const GemvParams& P, int page_in, 
   uint32_t xo[kXq];
 #pragma unroll
   for (int q = 0; q < kXq; ++q) {
-    const int b = 8 * (wave + 4 * q) + brow;
+    const int b = 8 * (wave + NW * q) + brow;
     xo[q] = b < P.B ? static_cast<uint32_t>(static_cast<int64_t>(b) * K * 2) + 16 * cx : kOOB;
   }
   auto issue = [&](int s, int slot) {  // stage s into ring slot `slot`
@@ -799,7 +801,7 @@ __device__ __forceinline__ void gemm_dma_unit(const GemvParams& P, int page_in, 
       load16_lds(wr, (ro[i] + kb2) | (wpar[i] ? oob1 : oob0), st + wblk[i] * kDmaBlk);
 #pragma unroll
     for (int q = 0; q < kXq; ++q)
-      load16_lds(xr, (xo[q] + kb2) | oobx, st + (8 * RT + wave + 4 * q) * kDmaBlk);
+      load16_lds(xr, (xo[q] + kb2) | oobx, st + (8 * RT + wave + NW * q) * kDmaBlk);
   };
 
   // fragment reads: lane l takes row l % 16 of a tile (block 2 tile + h,
@@ -808,13 +810,14 @@ __device__ __forceinline__ void gemm_dma_unit(const GemvParams& P, int page_in, 
   const int r8 = lrow & 7, hb = lrow >> 3;
   const int fo = hb * kDmaBlk + r8 * 128;
   const int fx0 = ((lgrp ^ r8 ^ hb) << 4), fx1 = fx0 ^ 64;  // position, sub 0 / 1
-  // products: the four wavefronts form a WR x (4 / WR) grid over the unit's
+  // products: the NW wavefronts form a WR x (NW / WR) grid over the unit's
   // 4 RT row tiles and BT batch tiles; wavefront w takes row tiles
   // [RW (w / WB), + RW) and batch tiles [BW (w % WB), + BW)
-  // (a host sub-unit: one row tile, the batch tiles over min(4, BT)
-  // wavefronts; with BT = 2 wavefronts 2 and 3 only load)
-  constexpr int WR = HOST ? 1 : dma_wave_rows<BT, RT>();
-  constexpr int WB = HOST ? (BT < 4 ? BT : 4) : 4 / WR;
+  // (a host sub-unit: one row tile, the batch tiles over min(NW, BT)
+  // wavefronts; the others only load)
+  constexpr int WR = HOST ? 1 : dma_wave_rows<BT, RT, NW>();
+  static_assert(WR > 0, "no wavefront grid fits the unit");
+  constexpr int WB = HOST ? (BT < NW ? BT : NW) : NW / WR;
   constexpr int RW = (HOST ? 1 : 4 * RT) / WR, BW = BT / WB;
   const int t_row = RW * (wave / WB), t_bat = BW * (wave % WB);
   const bool computes = !HOST || wave < WB;  // uniform over the wavefront
@@ -899,23 +902,32 @@ __device__ __forceinline__ void gemm_dma_unit(const GemvParams& P, int page_in, 
     }
 }
 
-template <int BT, int RT>
-__global__ __launch_bounds__(kThreads) void gemm_dma_kernel(GemvParams P) {
+template <int BT, int RT, int NW>
+__global__ __launch_bounds__(64 * NW) void gemm_dma_kernel(GemvParams P) {
   __shared__ __attribute__((aligned(16))) char ring[dma_stages<BT, RT>() * dma_stage_bytes<BT, RT>()];
   const int bid = blockIdx.x;
   const int U = P.units_per_page;
   if (P.address_order) {
-    gemm_dma_unit<BT, RT>(P, bid / U, bid % U, ring);
+    gemm_dma_unit<BT, RT, false, NW>(P, bid / U, bid % U, ring);
   } else if (bid < P.host_workers) {
     const int Uh = U * 4 * RT;  // 16-row sub-units per host page
     const int n_host_sub = P.n_host_pages * Uh;
     for (int v = bid; v < n_host_sub; v += P.host_workers)
-      gemm_dma_unit<BT, RT, true>(P, P.host_pages[v / Uh], v % Uh, ring);
+      gemm_dma_unit<BT, RT, true, NW>(P, P.host_pages[v / Uh], v % Uh, ring);
   } else {
     const int u = bid - P.host_workers;
-    gemm_dma_unit<BT, RT>(P, P.hbm_pages[u / U], u % U, ring);
+    gemm_dma_unit<BT, RT, false, NW>(P, P.hbm_pages[u / U], u % U, ring);
   }
 }
+
+// Wavefronts per workgroup of the direct-to-LDS GEMM: eight (two per SIMD,
+// sharing the one ring of the workgroup) from BOOST_GEMM_NW8_BT batch tiles.
+// At 16 batch tiles (B = 129..256) eight took the 8B matrices 3-12 % faster
+// (B = 256: gate_up 110 -> 102 us, down 92 -> 81 us); at 4 tiles they were
+// -10..+5 %.
+#ifndef BOOST_GEMM_NW8_BT
+#define BOOST_GEMM_NW8_BT 16
+#endif
 
 // y of a split-K call: the S slice partials of every (batch row, row) in
 // slice order; a row cut by a page boundary adds its earlier page's slices,
@@ -1136,6 +1148,10 @@ int launch_mfma_shape(GemvParams& P, int n_pages, bool need_fixup, const boost_c
 //   BT > 8:  two row tiles (four would need 256 accumulators per lane).
 // The direct-to-LDS GEMM: units of 64 RT rows (RT = 2 where a page holds at
 // least 128 rows, else 1), split-K over workgroups as above.
+// Workgroups per four CUs that split-K aims for
+#ifndef BOOST_GEMM_WG_X4
+#define BOOST_GEMM_WG_X4 3
+#endif
 template <int BT, int RT>
 int launch_gemm_shape(GemvParams& P, int n_pages, bool need_fixup, const boost_ctx* ctx,
                       hipStream_t s) {
@@ -1149,7 +1165,7 @@ int launch_gemm_shape(GemvParams& P, int n_pages, bool need_fixup, const boost_c
   // workgroups beat more split-K, whose fp32 partials are extra traffic)
   int S = 1;
   while (S < kMaxSlices && P.K / (2 * S) >= 512 &&
-         (units * S < ctx->n_cu * 3 / 4 || P.K / S > 16384))
+         (units * S < ctx->n_cu * BOOST_GEMM_WG_X4 / 4 || P.K / S > 16384))
     S *= 2;
   while (S > 1 && static_cast<uint64_t>(S) * P.B * (P.N + 2ull * (n_pages + 1)) >
                       ctx->gemm_ws_floats)
@@ -1168,8 +1184,12 @@ int launch_gemm_shape(GemvParams& P, int n_pages, bool need_fixup, const boost_c
     grid = P.host_workers + static_cast<int64_t>(P.n_hbm_pages) * P.units_per_page;
   }
   if (grid > 0x7fffffff) return bst::fail(BOOST_EINVAL, "grid too large");
-  hipLaunchKernelGGL((gemm_dma_kernel<BT, RT>), dim3(static_cast<unsigned>(grid)), dim3(kThreads),
-                     0, s, P);
+  if constexpr (BT >= BOOST_GEMM_NW8_BT && BT % 4 == 0)
+    hipLaunchKernelGGL((gemm_dma_kernel<BT, RT, 8>), dim3(static_cast<unsigned>(grid)),
+                       dim3(8 * 64), 0, s, P);
+  else
+    hipLaunchKernelGGL((gemm_dma_kernel<BT, RT, 4>), dim3(static_cast<unsigned>(grid)),
+                       dim3(kThreads), 0, s, P);
   BOOST_HIP(hipGetLastError());
   if (S == 1) return launch_fixup(P, n_pages, need_fixup, s);
   const int64_t lanes = static_cast<int64_t>(P.B) * P.N;
