@@ -57,6 +57,13 @@ def parse():
                         "(per kernel and grid) as JSON on stdout, then exit")
     p.add_argument("--part", default="chain", choices=("chain", "single", "attention"),
                    help="tier_counters: which part runs its one tiered call")
+    p.add_argument("--summarize-trace", default="",
+                   help="summarise a rocprofv3 --kernel-trace --stats directory as "
+                        "markdown tables (per kernel; per kernel and grid), then exit")
+    p.add_argument("--traffic-profile", default="",
+                   help="FETCH_DIR,WRITE_DIR: rocprofv3 FETCH_SIZE / WRITE_SIZE runs of the "
+                        "default bench with --pmc-ref; write profiles/traffic_counters.json "
+                        "and print its table, then exit")
     p.add_argument("--tier-profile", default="",
                    help="directory holding <part>/ (rocprofv3 counter CSVs of a "
                         "tier_counters run) and <part>.json (its output) for the parts "
@@ -429,6 +436,141 @@ def summarize_pmc(directory: str):
         out[key] = {"dispatches": n,
                     "per_dispatch": {c: round(v / n, 1) for c, v in sorted(ent["sums"].items())}}
     return out
+
+
+def _short_kernel(name: str) -> str:
+    name = name.replace("(anonymous namespace)::", "")
+    name = name[5:] if name.startswith("void ") else name
+    return name.split("(")[0].strip()
+
+
+def summarize_trace(directory: str) -> str:
+    """Markdown tables of a rocprofv3 kernel-trace run: per kernel (calls,
+    average, minimum, maximum, total) and, for this library's kernels, per
+    launch shape (grid size in threads: dispatches, median, mean)."""
+    import csv
+    import glob
+    trace = [r for path in sorted(glob.glob(os.path.join(directory, "**", "*kernel_trace.csv"),
+                                            recursive=True))
+             for r in csv.DictReader(open(path, newline=""))]
+    per, shape = {}, {}
+    for r in trace:
+        k = _short_kernel(r["Kernel_Name"])
+        d = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+        per.setdefault(k, []).append(d)
+        if not (k.startswith("at::") or "rocclr" in k):
+            g = int(r.get("Grid_Size_X") or r.get("Grid_Size") or 0)
+            shape.setdefault((k, g), []).append(d)
+    out = ["| kernel | calls | avg us | min us | max us | total ms |",
+           "|---|---:|---:|---:|---:|---:|"]
+    for k, v in sorted(per.items(), key=lambda kv: -sum(kv[1])):
+        out.append(f"| `{k[:60]}` | {len(v)} | {np.mean(v):.2f} | {min(v):.2f} | "
+                   f"{max(v):.2f} | {sum(v) / 1e3:.2f} |")
+    out += ["", "| kernel | grid (threads) | dispatches | median us | mean us | total ms |",
+            "|---|---:|---:|---:|---:|---:|"]
+    for (k, g), v in sorted(shape.items(), key=lambda kv: -sum(kv[1])):
+        out.append(f"| `{k[:60]}` | {g} | {len(v)} | {np.median(v):.2f} | {np.mean(v):.2f} | "
+                   f"{sum(v) / 1e3:.2f} |")
+    return "\n".join(out)
+
+
+# launch shapes (grid in threads) of one tiered step of the 8B chain at batch 1
+CHAIN_GRIDS = {"qkv": (393216, 32), "o": (262144, 32), "gate_up": (1835008, 32),
+               "down": (530432, 32)}
+
+
+def write_traffic_profile(dirs: str):
+    """HBM traffic per launch from FETCH_SIZE and WRITE_SIZE runs of the default
+    bench (with --pmc-ref), each scaled by what the counter reads for the
+    plain 1 GiB device copy: the GEMV averaged over one tiered chain step
+    (the 128 layer launches by grid, the head's tiered launch as the largest
+    gemv grid not in the layers) and one config-3 attention call (partition
+    and merge kernels).  Written to profiles/traffic_counters.json."""
+    import hashlib
+    fetch_dir, write_dir = dirs.split(",")
+    f, w = summarize_pmc(fetch_dir), summarize_pmc(write_dir)
+
+    def get(summ, name, grid, counter):
+        for key, ent in summ.items():
+            if key.startswith(name) and key.endswith(f"grid={grid}"):
+                return ent["per_dispatch"].get(counter, 0.0), ent["dispatches"]
+        return None, 0
+
+    # scale references: FETCH_SIZE of the calibration's HBM stream with 2048
+    # workgroups (4 GiB read per dispatch), WRITE_SIZE of the 1 GiB fill
+    # that --pmc-ref adds
+    def ref_fetch():
+        for key, ent in f.items():
+            if key.startswith("stream_read") and key.endswith("grid=524288"):
+                return ent["per_dispatch"]["FETCH_SIZE"], 4 << 30
+        raise SystemExit("no 4 GiB calibration stream in the FETCH_SIZE run")
+
+    def ref_write():
+        best = 0.0
+        for key, ent in w.items():
+            if "Fill" in key or "fill" in key:
+                best = max(best, ent["per_dispatch"].get("WRITE_SIZE", 0.0))
+        if best <= 0:
+            raise SystemExit("no fill in the WRITE_SIZE run (run the bench with --pmc-ref)")
+        return best, 1 << 30
+
+    fk_ref, fb_ref = ref_fetch()
+    wk_ref, wb_ref = ref_write()
+    fscale = fb_ref / (fk_ref * 1024)
+    wscale = wb_ref / (wk_ref * 1024)
+    gemv_grids = sorted({int(k.split("grid=")[1]) for k in f if k.startswith("gemv_kernel")})
+    layer_grids = {g for g, _ in CHAIN_GRIDS.values()}
+    # the head's launches: every gemv grid that is neither a layer's nor the
+    # single-layer leg's (tiered and all-HBM legs differ by the host workers)
+    heads = [g for g in gemv_grids if g not in layer_grids and g != 249856]
+    fsum = wsum = 0.0
+    launches = 0
+    rows = []
+    for name, (grid, n) in CHAIN_GRIDS.items():
+        fk, _ = get(f, "gemv_kernel", grid, "FETCH_SIZE")
+        wk, _ = get(w, "gemv_kernel", grid, "WRITE_SIZE")
+        fsum += n * fk * 1024 * fscale
+        wsum += n * wk * 1024 * wscale
+        launches += n
+        rows.append(f"| gemv {name} | {grid} | {n} | {fk:.1f} | {wk:.1f} |")
+    hf = hw = hn = 0.0
+    for g in heads:
+        fk, nd = get(f, "gemv_kernel", g, "FETCH_SIZE")
+        wk, _ = get(w, "gemv_kernel", g, "WRITE_SIZE")
+        hf, hw, hn = hf + fk * nd, hw + wk * nd, hn + nd
+        rows.append(f"| gemv lm_head | {g} | 1 | {fk:.1f} | {wk:.1f} |")
+    fsum += hf / hn * 1024 * fscale
+    wsum += hw / hn * 1024 * wscale
+    launches += 1
+    attn_f = attn_w = 0.0
+    for kname in ("attn_partition", "attn_merge"):
+        for key, ent in f.items():
+            if key.startswith(kname):
+                attn_f += ent["per_dispatch"].get("FETCH_SIZE", 0.0) * 1024 * fscale
+                rows.append(f"| {key} | | {ent['dispatches']} | "
+                            f"{ent['per_dispatch'].get('FETCH_SIZE', 0.0):.1f} | |")
+        for key, ent in w.items():
+            if key.startswith(kname):
+                attn_w += ent["per_dispatch"].get("WRITE_SIZE", 0.0) * 1024 * wscale
+
+    def sha(src):
+        return hashlib.sha256(open(os.path.join(ROOT, "paper_2609_13592_amd", "csrc", src),
+                                   "rb").read()).hexdigest()
+    prof = {"gemv": {"source_sha256": sha("gemv.hip"),
+                     "traffic_bytes_per_launch": int((fsum + wsum) / launches),
+                     "fetch_bytes_per_step": int(fsum), "write_bytes_per_step": int(wsum),
+                     "launches_per_step": launches},
+            "attn_partition": {"source_sha256": sha("attn.hip"),
+                               "traffic_bytes_per_launch": int(attn_f + attn_w),
+                               "fetch_bytes": int(attn_f), "write_bytes": int(attn_w)},
+            "fetch_scale": round(fscale, 4), "write_scale": round(wscale, 4)}
+    with open(os.path.join(ROOT, "profiles", "traffic_counters.json"), "w") as fh:
+        json.dump(prof, fh, indent=1)
+        fh.write("\n")
+    print("| launch | grid | per step | FETCH KiB / dispatch | WRITE KiB / dispatch |")
+    print("|---|---:|---:|---:|---:|")
+    print("\n".join(rows))
+    print(json.dumps(prof, indent=1))
 
 
 TIER_KERNELS = {"chain": (("gemv_kernel", "split_fixup"), "gemv.hip"),
@@ -1613,6 +1755,12 @@ def main():
     if args.tier_profile:
         write_tier_profile(args.tier_profile)
         return
+    if args.traffic_profile:
+        write_traffic_profile(args.traffic_profile)
+        return
+    if args.summarize_trace:
+        print(summarize_trace(args.summarize_trace))
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); "
               "the library has no multi-GPU path.", file=sys.stderr)
@@ -1626,12 +1774,11 @@ def main():
     M = args.modulus or bd.boost_modulus_from_alpha(alpha)
     log(f"  hbm {bw_hbm:.1f} GB/s host {bw_host:.2f} GB/s alpha {alpha:.5f} M {M}")
     bd.boost_gemv_set_schedule(ctx, bd.SCHED_CAP, args.host_workers)
-    if args.pmc_ref:      # a plain 1 GiB device copy: scale reference of the counters
+    if args.pmc_ref:      # a plain 1 GiB device fill: write reference of the counters
         a = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
-        b = torch.empty_like(a)
-        b.copy_(a)
+        a.fill_(1)
         torch.cuda.synchronize()
-        del a, b
+        del a
     exp = {"host_share_sweep": lambda: host_share_sweep(args, bd, ctx, torch, bw_hbm,
                                                         bw_host, alpha, M),
            "cap_probe": lambda: cap_probe(args, bd, ctx, torch, bw_hbm, bw_host, alpha, M),
