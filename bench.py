@@ -479,7 +479,7 @@ CHAIN_GRIDS = {"qkv": (393216, 32), "o": (262144, 32), "gate_up": (1835008, 32),
                "down": (530432, 32)}
 
 
-def write_traffic_profile(dirs: str):
+def write_traffic_profile(dirs: str, out_dir: str = ""):
     """HBM traffic per launch from FETCH_SIZE and WRITE_SIZE runs of the default
     bench (with --pmc-ref), each scaled by what the counter reads for the
     plain 1 GiB device copy: the GEMV averaged over one tiered chain step
@@ -564,7 +564,8 @@ def write_traffic_profile(dirs: str):
                                "traffic_bytes_per_launch": int(attn_f + attn_w),
                                "fetch_bytes": int(attn_f), "write_bytes": int(attn_w)},
             "fetch_scale": round(fscale, 4), "write_scale": round(wscale, 4)}
-    with open(os.path.join(ROOT, "profiles", "traffic_counters.json"), "w") as fh:
+    with open(os.path.join(out_dir or os.path.join(ROOT, "profiles"), "traffic_counters.json"),
+              "w") as fh:
         json.dump(prof, fh, indent=1)
         fh.write("\n")
     print("| launch | grid | per step | FETCH KiB / dispatch | WRITE KiB / dispatch |")
@@ -578,7 +579,7 @@ TIER_KERNELS = {"chain": (("gemv_kernel", "split_fixup"), "gemv.hip"),
                 "attention": (("attn_partition", "attn_merge"), "attn.hip")}
 
 
-def write_tier_profile(directory: str):
+def write_tier_profile(directory: str, out_dir: str = ""):
     """Per-tier bytes of the tiered calls of a tier_counters run, summed over
     the part's kernels, against the placement's bytes; written to
     profiles/tier_counters.json with the kernel source's hash."""
@@ -616,7 +617,8 @@ def write_tier_profile(directory: str):
         lines.append(f"| {part} | {meta['modulus']} | {', '.join(sorted(used))} | {dram:,.0f} | "
                      f"{io:,.0f} | {hbm_p:,} | {host_p:,} | {dram / hbm_p:.5f} | "
                      + (f"{io / host_p:.5f} |" if host_p else "- |"))
-    with open(os.path.join(ROOT, "profiles", "tier_counters.json"), "w") as fh:
+    with open(os.path.join(out_dir or os.path.join(ROOT, "profiles"), "tier_counters.json"),
+              "w") as fh:
         json.dump(prof, fh, indent=1)
         fh.write("\n")
     print("\n".join(lines))
