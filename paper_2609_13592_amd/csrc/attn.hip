@@ -45,6 +45,7 @@ constexpr int kLanesTok = kD / 8;  // lanes per token row (16)
 #define BOOST_ATTN_UNROLL8 BOOST_ATTN_UNROLL
 #endif
 constexpr int kMaxPartBlocks = 256;         // blocks per partition, at most
+static_assert(kMaxPartBlocks <= kThreads, "one thread per partition size");
 // A work item of fewer than 16 blocks spends as long on its start (q loads)
 // and end (slot merge, partial stores) as on its K/V (batch 8 at 2048 tokens:
 // 1.2 TB/s with 4-block items, 2.2 TB/s with 16).
@@ -151,10 +152,10 @@ __device__ __forceinline__ void merge_state(float* m, float* l, float (*acc)[8],
 // log2 domain (q . k * scale * log2 e), so exp2 is one instruction.  With
 // MASKED false every token is valid; otherwise invalid tokens have score -inf
 // and contribute nothing.
-template <int G, int U, bool MASKED>
+template <int G, int U, bool MASKED, typename AfterK>
 __device__ __forceinline__ void consume(const uint32_t (*qp)[4], const uint4* kb,
                                         const uint4* vb, const bool* valid, float sc2,
-                                        float* m, float* l, float (*acc)[8]) {
+                                        float* m, float* l, float (*acc)[8], AfterK after_k) {
   float sc[U][G];
 #pragma unroll
   for (int u = 0; u < U; ++u)
@@ -167,6 +168,7 @@ __device__ __forceinline__ void consume(const uint32_t (*qp)[4], const uint4* kb
       d = row16_sum(d) * sc2;  // q . k over the 16 lanes of the token row
       sc[u][j] = (!MASKED || valid[u]) ? d : -INFINITY;
     }
+  after_k();  // the K registers are free from here on
 #pragma unroll
   for (int j = 0; j < G; ++j) {
     float mc = m[j];
@@ -247,11 +249,11 @@ __device__ __forceinline__ float score_of_lane_head(const float* d, bool b0, boo
   return f;
 }
 
-template <int G, int U, bool MASKED>
+template <int G, int U, bool MASKED, typename AfterK>
 __device__ __forceinline__ void consume_hd(const uint32_t (*qp)[4], const uint4* kb,
                                            const uint4* vb, const bool* valid, float sc2,
                                            bool b0, bool b1, float& mh, float& lh,
-                                           float (*acc)[8]) {
+                                           float (*acc)[8], AfterK after_k) {
   float s[U];
 #pragma unroll
   for (int u = 0; u < U; ++u) {
@@ -266,6 +268,7 @@ __device__ __forceinline__ void consume_hd(const uint32_t (*qp)[4], const uint4*
     const float f = score_of_lane_head<G>(d, b0, b1) * sc2;
     s[u] = (!MASKED || valid[u]) ? f : -INFINITY;
   }
+  after_k();  // the K registers are free from here on
   float mc = mh;
 #pragma unroll
   for (int u = 0; u < U; ++u) mc = fmaxf(mc, s[u]);
@@ -293,6 +296,135 @@ __device__ __forceinline__ void consume_hd(const uint32_t (*qp)[4], const uint4*
   }
 }
 
+// Blocks of request b in this call (0 for an empty context).
+__device__ __forceinline__ int blocks_of(const AttnParams& P, int b) {
+  const int L = P.lens[b];
+  return L <= 0 ? 0 : min((L + kT - 1) / kT, P.max_blocks);
+}
+
+// Sum of v over the workgroup; every thread gets it (red: 4 ints of LDS).
+__device__ __forceinline__ int wg_sum(int v, int* red) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
+  __syncthreads();  // red is free again
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  return red[0] + red[1] + red[2] + red[3];
+}
+
+// Exclusive prefix sum of v over the workgroup in thread order; total gets
+// the sum of every thread's v.
+__device__ __forceinline__ int wg_scan(int v, int* red, int& total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int x = v;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const int y = __shfl_up(x, d, 64);
+    if (lane >= d) x += y;
+  }
+  __syncthreads();
+  if (lane == 63) red[wave] = x;
+  __syncthreads();
+  int before = 0;
+  for (int w = 0; w < wave; ++w) before += red[w];
+  total = red[0] + red[1] + red[2] + red[3];
+  return before + x - v;
+}
+
+// Request whose count interval holds `target` in the running sum of
+// count(b, n_b) over b = 0, 1, ... (count > 0 there); pick[0] gets b,
+// pick[1] target minus the sum before b.  n0: this thread's n_b for
+// b = threadIdx.x (read once by the caller); later chunks read lens again.
+template <typename Count>
+__device__ __forceinline__ void find_request(const AttnParams& P, int target, int n0, Count count,
+                                             int* red, int* pick) {
+  int carry = 0;
+  for (int base = 0; base < P.B; base += kThreads) {  // uniform
+    const int b = base + static_cast<int>(threadIdx.x);
+    const int c = b < P.B ? count(base == 0 ? n0 : blocks_of(P, b)) : 0;
+    int total;
+    const int ex = carry + wg_scan(c, red, total);
+    if (c > 0 && ex <= target && target < ex + c) {
+      pick[0] = b;
+      pick[1] = target - ex;
+    }
+    carry += total;
+    if (carry > target) break;  // uniform
+  }
+  __syncthreads();
+}
+
+// Work item of workgroup idx, from the context lengths alone (so the same on
+// every pool: the order decides which items run together, never what an item
+// computes).  With n_b blocks, request b has full_b = n_b / part_blocks full
+// partitions and one partial one if rem_b = n_b % part_blocks > 0.  Order:
+//   1. every partition of head H-1 (where host data can lie), request by
+//      request: its slow reads start first;
+//   2. full partitions of heads H-2..0, request by request, head fastest;
+//   3. partial partitions of heads H-2..0, the largest first (rem_b
+//      descending, then b ascending), head fastest;
+//   4. workgroups past the last item return at once.
+// Empty partitions get no workgroup and the short ones run last, so the last
+// grid wave is short (config 3, reads alone: 104 -> 96 us).
+__device__ bool item_of(const AttnParams& P, int idx, int& b, int& g, int& part, int* red,
+                        int* hist, int* pick) {
+  const int tid = threadIdx.x, PB = P.part_blocks, H = P.H;
+  if (tid < 4) pick[tid] = -1;  // written by the sums' barriers below
+  const int n0 = tid < P.B ? blocks_of(P, tid) : 0;  // request tid, read once
+  int f = 0, r = 0;
+  for (int bb = tid; bb < P.B; bb += kThreads) {
+    const int n = bb == tid ? n0 : blocks_of(P, bb);
+    f += n / PB;
+    r += n % PB > 0;
+  }
+  const int F = wg_sum(f, red), R = wg_sum(r, red);
+  const int S0 = F + R;
+  if (idx < S0) {
+    find_request(P, idx, n0, [&](int n) { return n / PB + (n % PB > 0); }, red, pick);
+    b = pick[0];
+    part = pick[1];
+    g = H - 1;
+    return b >= 0 && b < P.B && part >= 0;
+  }
+  int j = idx - S0;
+  if (j < (H - 1) * F) {
+    find_request(P, j / (H - 1), n0, [&](int n) { return n / PB; }, red, pick);
+    b = pick[0];
+    part = pick[1];
+    g = H - 2 - j % (H - 1);
+    return b >= 0 && b < P.B && part >= 0;
+  }
+  j -= (H - 1) * F;
+  if (j >= (H - 1) * R) return false;
+  // partial partitions by size: a counting sort over rem in [1, PB)
+  const int rank = j / (H - 1);
+  for (int v = tid; v < PB; v += kThreads) hist[v] = 0;
+  __syncthreads();
+  for (int bb = tid; bb < P.B; bb += kThreads) {
+    const int rem = (bb == tid ? n0 : blocks_of(P, bb)) % PB;
+    if (rem > 0) atomicAdd(&hist[rem], 1);
+  }
+  __syncthreads();
+  {
+    const int v = PB - 1 - tid;  // thread order = rem descending (PB <= kThreads)
+    const int c = v >= 1 ? hist[v] : 0;
+    int total;
+    const int ex = wg_scan(c, red, total);
+    if (c > 0 && ex <= rank && rank < ex + c) {
+      pick[2] = v;
+      pick[3] = rank - ex;
+    }
+    __syncthreads();
+  }
+  const int vsel = pick[2];
+  find_request(P, pick[3], n0, [&](int n) { return n % PB == vsel ? 1 : 0; }, red, pick);
+  b = pick[0];
+  if (b < 0 || b >= P.B) return false;
+  part = blocks_of(P, b) / PB;
+  g = H - 2 - j % (H - 1);
+  return true;
+}
+
 // Waves per SIMD the register allocator targets for G <= 4: three (168
 // registers, no spill) against the two it picks by itself took config 3 from
 // 136 to 126 us; four spill and run at 306 us.  G = 8 keeps the allocator's
@@ -312,29 +444,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(
   const int tid = threadIdx.x;
   const int ts = tid / kLanesTok;  // token slot 0..15
   const int dc = tid % kLanesTok;  // 8-dim chunk
-  // Item order (uniform): first every item of the highest head, request by
-  // request (only those can read host pages, so their slow reads start
-  // first); then the other heads partition by partition, request by request,
-  // head fastest, so the items running together read the same blocks of one
-  // request in different head regions and every request's first (full)
-  // partition runs before its later, shorter ones.  (Against the order
-  // request by request, head slowest: batch 64 at contexts U[512, 4096]
-  // 138 -> 121 us, batch 64 at U[1024, 8192] 257 -> 228 us, batch 256 at
-  // U[1024, 8192] 970 -> 840 us; batch 8 at 2048 tokens unchanged.)
+  // the partition's block ids (staged once: a load per block from memory
+  // would put a round trip before every group of K/V loads); before that the
+  // item search's counting sort
+  __shared__ int32_t row[kMaxPartBlocks];
+  __shared__ int s_red[4], s_pick[4];
   int part, b, g;
-  {
-    const int idx = blockIdx.x, first = P.B * P.n_parts;
-    if (idx < first) {
-      part = idx % P.n_parts;
-      b = idx / P.n_parts;
-      g = P.H - 1;
-    } else {  // only reached with H > 1
-      const int j = idx - first, per_part = P.B * (P.H - 1);
-      part = j / per_part;
-      b = (j % per_part) / (P.H - 1);
-      g = P.H - 2 - (j % per_part) % (P.H - 1);
-    }
-  }
+  if (!item_of(P, blockIdx.x, b, g, part, s_red, row, s_pick)) return;  // uniform
   const int L = P.lens[b];
   const int n_blk = min((L + kT - 1) / kT, P.max_blocks);
   const int blk_beg = part * P.part_blocks;
@@ -343,9 +459,6 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(
   // leading blocks whose 16 tokens are all inside the context
   const int nfull = max(0, min(nbp, L / kT - blk_beg));
   const uint64_t head_off = static_cast<uint64_t>(g) * P.nb * (kT * kD * 2);
-  // the partition's block ids, read once into LDS: a load per block from
-  // memory would put a round trip before every group of K/V loads
-  __shared__ int32_t row[kMaxPartBlocks];
   if (tid < nbp) row[tid] = P.tables[static_cast<int64_t>(b) * P.max_blocks + blk_beg + tid];
   __syncthreads();
 
@@ -378,36 +491,66 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(
   // address of head-block (g, blk) of K and V: uniform scalar arithmetic
   // (a block id outside the pool reads nothing and its tokens are masked
   // out of the softmax, as if the block were not in the context)
-  auto fetch = [&](int bi, uint4& kq, uint4& vq) {
+  auto where = [&](int bi, bool& ok, bool& host) {
     const int32_t blk = row[bi];
-    const bool ok = blk >= 0 && blk < P.nb;
+    ok = blk >= 0 && blk < P.nb;
     const uint64_t byte = head_off + static_cast<uint64_t>(ok ? blk : 0) * (kT * kD * 2);
-    const bool host = byte >= P.host_from;
-    const uint64_t off = host ? byte - P.host_from : byte;
+    host = byte >= P.host_from;
+    return host ? byte - P.host_from : byte;
+  };
+  auto fetch_k = [&](int bi, uint4& kq) {
+    bool ok, host;
+    const uint64_t off = where(bi, ok, host);
     kq = load_block((host ? P.k_host : P.k_hbm) + off, ok, lane_off);
-    vq = load_block((host ? P.v_host : P.v_hbm) + off, ok, lane_off);
     return ok;
   };
+  auto fetch_v = [&](int bi, uint4& vq) {
+    bool ok, host;
+    const uint64_t off = where(bi, ok, host);
+    vq = load_block((host ? P.v_host : P.v_hbm) + off, ok, lane_off);
+  };
+  auto none = [] {};
+  // Full groups of kUnroll blocks, software-pipelined across K and V: the
+  // next group's K loads go out as soon as the scores have used this group's
+  // K, its V loads as soon as P.V has used this group's V, so each workgroup
+  // keeps loads in flight while it computes, with no extra registers.
   int i = 0;
-  for (; i + kUnroll <= nfull; i += kUnroll) {
+  if (nfull >= kUnroll) {
     uint4 kb[kUnroll], vb[kUnroll];
-    bool valid[kUnroll];
-    bool all_ok = true;  // uniform: block ids are the same for every lane
+    bool valid[kUnroll], vnext[kUnroll];
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
-      valid[u] = fetch(i + u, kb[u], vb[u]);
-      all_ok = all_ok && valid[u];
+      valid[u] = fetch_k(u, kb[u]);
+      fetch_v(u, vb[u]);
     }
-    if constexpr (kHD) {
-      if (all_ok)
-        consume_hd<G, kUnroll, false>(qp, kb, vb, valid, sc2, b0, b1, mh, lh, acc);
-      else
-        consume_hd<G, kUnroll, true>(qp, kb, vb, valid, sc2, b0, b1, mh, lh, acc);
-    } else {
-      if (all_ok)
-        consume<G, kUnroll, false>(qp, kb, vb, valid, sc2, m, l, acc);
-      else
-        consume<G, kUnroll, true>(qp, kb, vb, valid, sc2, m, l, acc);
+    for (; i + kUnroll <= nfull; i += kUnroll) {
+      const bool more = i + 2 * kUnroll <= nfull;  // uniform
+      bool all_ok = true;  // uniform: block ids are the same for every lane
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) all_ok = all_ok && valid[u];
+      auto next_k = [&] {
+        if (more)
+#pragma unroll
+          for (int u = 0; u < kUnroll; ++u) vnext[u] = fetch_k(i + kUnroll + u, kb[u]);
+      };
+      if constexpr (kHD) {
+        if (all_ok)
+          consume_hd<G, kUnroll, false>(qp, kb, vb, valid, sc2, b0, b1, mh, lh, acc, next_k);
+        else
+          consume_hd<G, kUnroll, true>(qp, kb, vb, valid, sc2, b0, b1, mh, lh, acc, next_k);
+      } else {
+        if (all_ok)
+          consume<G, kUnroll, false>(qp, kb, vb, valid, sc2, m, l, acc, next_k);
+        else
+          consume<G, kUnroll, true>(qp, kb, vb, valid, sc2, m, l, acc, next_k);
+      }
+      if (more) {
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+          fetch_v(i + kUnroll + u, vb[u]);
+          valid[u] = vnext[u];
+        }
+      }
     }
   }
   if (i < nbp) {  // the rest (fewer than kUnroll full blocks, then a partial
@@ -416,14 +559,15 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(
     bool valid[kUnroll];
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
-      const bool ok = i + u < nbp && fetch(i + u, kb[u], vb[u]);
+      const bool ok = i + u < nbp && fetch_k(i + u, kb[u]);
+      if (i + u < nbp) fetch_v(i + u, vb[u]);
       if (i + u >= nbp) kb[u] = vb[u] = make_uint4(0, 0, 0, 0);
       valid[u] = ok && (blk_beg + i + u) * kT + ts < L;
     }
     if constexpr (kHD)
-      consume_hd<G, kUnroll, true>(qp, kb, vb, valid, sc2, b0, b1, mh, lh, acc);
+      consume_hd<G, kUnroll, true>(qp, kb, vb, valid, sc2, b0, b1, mh, lh, acc, none);
     else
-      consume<G, kUnroll, true>(qp, kb, vb, valid, sc2, m, l, acc);
+      consume<G, kUnroll, true>(qp, kb, vb, valid, sc2, m, l, acc, none);
   }
   if constexpr (kHD) {  // every head's maximum and sum in every lane again
     bcast_heads<G>(mh, m);
