@@ -148,6 +148,37 @@ __device__ __forceinline__ void merge_state(float* m, float* l, float (*acc)[8],
   }
 }
 
+// Pair of lanes D apart (D = 16 or 32; v is the same register in both
+// operands): {v of the lower lane, v of the upper lane} in both lanes.
+template <int D>
+__device__ __forceinline__ void pair_of(float v, float& lo, float& hi) {
+  const uint32_t u = __float_as_uint(v);
+  if constexpr (D == 16) {
+    const auto r = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+    lo = __uint_as_float(r[0]);
+    hi = __uint_as_float(r[1]);
+  } else {
+    const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+    lo = __uint_as_float(r[0]);
+    hi = __uint_as_float(r[1]);
+  }
+}
+
+// The running states of the lane pairs D apart merged, lower lane's state
+// first; afterwards both lanes hold the result.
+template <int G, int D>
+__device__ __forceinline__ void slot_merge(float* m, float* l, float (*acc)[8]) {
+  float m2[G], l2[G], a2[G][8];
+#pragma unroll
+  for (int j = 0; j < G; ++j) {
+    pair_of<D>(m[j], m[j], m2[j]);
+    pair_of<D>(l[j], l[j], l2[j]);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) pair_of<D>(acc[j][e], acc[j][e], a2[j][e]);
+  }
+  merge_state<G>(m, l, acc, m2, l2, a2);
+}
+
 // Online-softmax update of one token slot with U blocks.  Scores are in the
 // log2 domain (q . k * scale * log2 e), so exp2 is one instruction.  With
 // MASKED false every token is valid; otherwise invalid tokens have score -inf
@@ -574,19 +605,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(
     bcast_heads<G>(lh, l);
   }
 
-  // merge the 4 slots of a wavefront (lanes 16 and 32 apart hold the same dims)
-#pragma unroll
-  for (int off = 16; off <= 32; off <<= 1) {
-    float m2[G], l2[G], a2[G][8];
-#pragma unroll
-    for (int j = 0; j < G; ++j) {
-      m2[j] = __shfl_xor(m[j], off, 64);
-      l2[j] = __shfl_xor(l[j], off, 64);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) a2[j][e] = __shfl_xor(acc[j][e], off, 64);
-    }
-    merge_state<G>(m, l, acc, m2, l2, a2);
-  }
+  // merge the 4 slots of a wavefront (lanes 16 and 32 apart hold the same
+  // dims) with the row-swap instructions: permlane16_swap(v, v) gives every
+  // lane the pair (v of the lower lane, v of the lane 16 above it) of its
+  // 16-apart pair, permlane32_swap the same for lanes 32 apart, so both
+  // lanes of a pair merge the same two states in the same order
+  slot_merge<G, 16>(m, l, acc);
+  slot_merge<G, 32>(m, l, acc);
   const int wave = tid >> 6, lane = tid & 63;
   if (lane < kLanesTok) {
 #pragma unroll
@@ -600,29 +625,33 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(
     }
   }
   __syncthreads();
-  if (wave != 0 || lane >= kLanesTok) return;
-  // wavefront 0 folds in wavefronts 1..3 in order
-  for (int w = 1; w < 4; ++w) {
-    float m2[G], l2[G], a2[G][8];
+  if (lane >= kLanesTok) return;
+  // head j is folded by wavefront j % 4 (the heads in parallel): wavefront
+  // 0's state, then wavefronts 1, 2, 3 in order, as the same values in the
+  // same order whichever wavefront does it
+  constexpr int kHeadsPerWave = (G + 3) / 4;
 #pragma unroll
-    for (int j = 0; j < G; ++j) {
-      m2[j] = s_ml[w][j][0];
-      l2[j] = s_ml[w][j][1];
+  for (int jj = 0; jj < kHeadsPerWave; ++jj) {
+    const int j = wave + 4 * jj;  // uniform over the wavefront
+    if (j >= G) break;
+    float mj = s_ml[0][j][0], lj = s_ml[0][j][1], aj[1][8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) a2[j][e] = s_acc[w][j][dc * 8 + e];
+    for (int e = 0; e < 8; ++e) aj[0][e] = s_acc[0][j][dc * 8 + e];
+    for (int w = 1; w < 4; ++w) {
+      const float m2 = s_ml[w][j][0], l2 = s_ml[w][j][1];
+      float a2[1][8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) a2[0][e] = s_acc[w][j][dc * 8 + e];
+      merge_state<1>(&mj, &lj, aj, &m2, &l2, a2);
     }
-    merge_state<G>(m, l, acc, m2, l2, a2);
-  }
-#pragma unroll
-  for (int j = 0; j < G; ++j) {
     const int64_t rowi = (static_cast<int64_t>(b) * P.Hq + g * G + j) * P.max_parts + part;
     if (dc == 0) {
-      P.part_ml[rowi * 2] = m[j];
-      P.part_ml[rowi * 2 + 1] = l[j];
+      P.part_ml[rowi * 2] = mj;
+      P.part_ml[rowi * 2 + 1] = lj;
     }
     float4* dst = reinterpret_cast<float4*>(P.part_acc + rowi * kD + dc * 8);
-    dst[0] = make_float4(acc[j][0], acc[j][1], acc[j][2], acc[j][3]);
-    dst[1] = make_float4(acc[j][4], acc[j][5], acc[j][6], acc[j][7]);
+    dst[0] = make_float4(aj[0][0], aj[0][1], aj[0][2], aj[0][3]);
+    dst[1] = make_float4(aj[0][4], aj[0][5], aj[0][6], aj[0][7]);
   }
 }
 
