@@ -63,6 +63,36 @@ def test_small_parity_and_placement_invariance(gpu_ctx, Hq, H):
         assert np.array_equal(o.view(np.uint32), outs[0].view(np.uint32))
 
 
+@pytest.mark.parametrize("Hq,H", [(4, 2), (8, 1), (32, 8)])
+def test_more_than_256_requests(gpu_ctx, Hq, H):
+    """300 requests: each workgroup finds its work item from the context
+    lengths with sums, prefix scans and a counting sort over chunks of 256
+    requests, so the second chunk is exercised; empty contexts and partial
+    partitions of every size (16-block partitions) are included, and the
+    LPP pool gives the same bits as the all-HBM one."""
+    rng = np.random.default_rng(31)
+    B = 300
+    lengths = rng.integers(1, 700, size=B)
+    lengths[::17] = 0
+    _, q, ks, vs = synth.attention_inputs(B, Hq, H, 128, 0, 0, seed=32, kv_seed=33,
+                                          lengths=lengths)
+    ref = oa.decode_attention(q, ks, vs)
+    nb = int(sum((int(L) + 15) // 16 for L in lengths)) + 64
+    outs = []
+    for mode, M in ((bd.KV_ALL_HBM, 0), (bd.KV_LPP, 3)):
+        pool = new_pool(gpu_ctx, H, Hq, nb, M, mode, max_batch=B, max_blocks=48)
+        try:
+            tables = fill_pool(bd, gpu_ctx, pool, 0, lengths, ks, vs)
+            o = run_attn(gpu_ctx, pool, 0, q, tables, lengths)
+            assert og.rel_err(o, ref) <= TOL
+            assert np.max(np.abs(o - ref)) < 1e-4
+            assert np.all(o[lengths == 0] == 0)
+            outs.append(o)
+        finally:
+            bd.boost_kv_pool_destroy(pool)
+    assert np.array_equal(outs[1].view(np.uint32), outs[0].view(np.uint32))
+
+
 def test_host_heads_follow_block_types(gpu_ctx):
     """LPP with H = 8 and a modulus above H: the tail lies in head 7, so an SHH
     request has exactly its head-7 data on host; output still exact."""
