@@ -1855,7 +1855,10 @@ def main():
     ms_pre = float(np.median(pre_ms))
 
     # roofline of the dominant kernel: the timed region's HIP events (on the
-    # launching stream) over the step's GEMV launches, back to back
+    # launching stream) over the step's GEMV launches, back to back, so each
+    # launch's share includes its kernel boundary.  (A pair of events around
+    # every launch reads ~2 us more per launch than this: the events' own
+    # packets between the kernels cost about as much as a boundary.)
     launches = len(chain.ops)
     avg_launch_ms = ms / launches
     bytes_per_launch = chain.alg_bytes / launches
