@@ -363,12 +363,13 @@ __device__ __forceinline__ int wg_scan(int v, int* red, int& total) {
 }
 
 // Request whose count interval holds `target` in the running sum of
-// count(b, n_b) over b = 0, 1, ... (count > 0 there); pick[0] gets b,
-// pick[1] target minus the sum before b.  n0: this thread's n_b for
-// b = threadIdx.x (read once by the caller); later chunks read lens again.
+// count(n_b) over b = 0, 1, ... (count > 0 there); pick[0] gets b, pick[1]
+// target minus the sum before b, pick[4] b's context length.  n0, L0: this
+// thread's n_b and length for b = threadIdx.x (read once by the caller);
+// later chunks read the lengths again.
 template <typename Count>
-__device__ __forceinline__ void find_request(const AttnParams& P, int target, int n0, Count count,
-                                             int* red, int* pick) {
+__device__ __forceinline__ void find_request(const AttnParams& P, int target, int n0, int L0,
+                                             Count count, int* red, int* pick) {
   int carry = 0;
   for (int base = 0; base < P.B; base += kThreads) {  // uniform
     const int b = base + static_cast<int>(threadIdx.x);
@@ -378,6 +379,7 @@ __device__ __forceinline__ void find_request(const AttnParams& P, int target, in
     if (c > 0 && ex <= target && target < ex + c) {
       pick[0] = b;
       pick[1] = target - ex;
+      pick[4] = base == 0 ? L0 : P.lens[b];
     }
     carry += total;
     if (carry > target) break;  // uniform
@@ -397,11 +399,13 @@ __device__ __forceinline__ void find_request(const AttnParams& P, int target, in
 //   4. workgroups past the last item return at once.
 // Empty partitions get no workgroup and the short ones run last, so the last
 // grid wave is short (config 3, reads alone: 104 -> 96 us).
-__device__ bool item_of(const AttnParams& P, int idx, int& b, int& g, int& part, int* red,
-                        int* hist, int* pick) {
+// L gets the request's context length (so the caller does not read it again).
+__device__ bool item_of(const AttnParams& P, int idx, int& b, int& g, int& part, int& L,
+                        int* red, int* hist, int* pick) {
   const int tid = threadIdx.x, PB = P.part_blocks, H = P.H;
-  if (tid < 4) pick[tid] = -1;  // written by the sums' barriers below
-  const int n0 = tid < P.B ? blocks_of(P, tid) : 0;  // request tid, read once
+  if (tid < 5) pick[tid] = -1;  // written by the sums' barriers below
+  const int L0 = tid < P.B ? P.lens[tid] : 0;  // request tid, read once
+  const int n0 = L0 <= 0 ? 0 : min((L0 + kT - 1) / kT, P.max_blocks);
   int f = 0, r = 0;
   for (int bb = tid; bb < P.B; bb += kThreads) {
     const int n = bb == tid ? n0 : blocks_of(P, bb);
@@ -411,17 +415,19 @@ __device__ bool item_of(const AttnParams& P, int idx, int& b, int& g, int& part,
   const int F = wg_sum(f, red), R = wg_sum(r, red);
   const int S0 = F + R;
   if (idx < S0) {
-    find_request(P, idx, n0, [&](int n) { return n / PB + (n % PB > 0); }, red, pick);
+    find_request(P, idx, n0, L0, [&](int n) { return n / PB + (n % PB > 0); }, red, pick);
     b = pick[0];
     part = pick[1];
+    L = pick[4];
     g = H - 1;
     return b >= 0 && b < P.B && part >= 0;
   }
   int j = idx - S0;
   if (j < (H - 1) * F) {
-    find_request(P, j / (H - 1), n0, [&](int n) { return n / PB; }, red, pick);
+    find_request(P, j / (H - 1), n0, L0, [&](int n) { return n / PB; }, red, pick);
     b = pick[0];
     part = pick[1];
+    L = pick[4];
     g = H - 2 - j % (H - 1);
     return b >= 0 && b < P.B && part >= 0;
   }
@@ -448,10 +454,11 @@ __device__ bool item_of(const AttnParams& P, int idx, int& b, int& g, int& part,
     __syncthreads();
   }
   const int vsel = pick[2];
-  find_request(P, pick[3], n0, [&](int n) { return n % PB == vsel ? 1 : 0; }, red, pick);
+  find_request(P, pick[3], n0, L0, [&](int n) { return n % PB == vsel ? 1 : 0; }, red, pick);
   b = pick[0];
   if (b < 0 || b >= P.B) return false;
-  part = blocks_of(P, b) / PB;
+  L = pick[4];
+  part = (L <= 0 ? 0 : min((L + kT - 1) / kT, P.max_blocks)) / PB;
   g = H - 2 - j % (H - 1);
   return true;
 }
@@ -479,18 +486,20 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(
   // would put a round trip before every group of K/V loads); before that the
   // item search's counting sort
   __shared__ int32_t row[kMaxPartBlocks];
-  __shared__ int s_red[4], s_pick[4];
-  int part, b, g;
-  if (!item_of(P, blockIdx.x, b, g, part, s_red, row, s_pick)) return;  // uniform
-  const int L = P.lens[b];
-  const int n_blk = min((L + kT - 1) / kT, P.max_blocks);
+  __shared__ int s_red[4], s_pick[5];
+  int part, b, g, L;
+  if (!item_of(P, blockIdx.x, b, g, part, L, s_red, row, s_pick)) return;  // uniform
+  const int n_blk = L <= 0 ? 0 : min((L + kT - 1) / kT, P.max_blocks);
   const int blk_beg = part * P.part_blocks;
-  if (L <= 0 || blk_beg >= n_blk) return;  // uniform: empty partition
+  if (blk_beg >= n_blk) return;  // uniform: empty partition (not produced by item_of)
   const int nbp = min(n_blk, blk_beg + P.part_blocks) - blk_beg;
   // leading blocks whose 16 tokens are all inside the context
   const int nfull = max(0, min(nbp, L / kT - blk_beg));
   const uint64_t head_off = static_cast<uint64_t>(g) * P.nb * (kT * kD * 2);
-  if (tid < nbp) row[tid] = P.tables[static_cast<int64_t>(b) * P.max_blocks + blk_beg + tid];
+  // the partition's width of the table row (entries past the context are
+  // read but not used)
+  if (tid < min(P.part_blocks, P.max_blocks - blk_beg))
+    row[tid] = P.tables[static_cast<int64_t>(b) * P.max_blocks + blk_beg + tid];
   __syncthreads();
 
   // q stays in bf16 pairs for the dot2 instruction
