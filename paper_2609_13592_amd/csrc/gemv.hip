@@ -1203,11 +1203,18 @@ template <int BT>
 int launch_gemm(GemvParams& P, int n_pages, bool need_fixup, const boost_ctx* ctx,
                 hipStream_t s) {
   // 128-row units where a page fills them and they still give a workgroup
-  // per CU, or where a page holds 64..127 rows (one unit per page either
-  // way); 64-row units otherwise
+  // per CU (three per four CUs above four batch tiles, where halving x's
+  // share of the ring counts for more: 8B gate_up's 224 units take 64-row
+  // units at B = 64, 58.2 against 61.3 us, but keep 128-row units at B = 128
+  // and 256, 70.5 and 92.9 against 83.4 and 119.0), or where a page holds
+  // 64..127 rows (one unit per page either way); 64-row units otherwise.
   const int64_t rpp = kPageElems / P.K;  // whole rows per page
-  const int64_t u2 = static_cast<int64_t>(n_pages) * ((std::min<int64_t>(P.N, rpp + 1) + 127) / 128);
-  if ((rpp >= 128 && u2 >= ctx->n_cu) || (rpp >= 64 && rpp < 128))
+  // rows a page meets at most: one more than it holds whole when rows
+  // straddle page boundaries
+  const int64_t meet = std::min<int64_t>(P.N, rpp + (kPageElems % P.K != 0));
+  const int64_t u2 = static_cast<int64_t>(n_pages) * ((meet + 127) / 128);
+  const int64_t enough = BT > 4 ? ctx->n_cu * 3 / 4 : ctx->n_cu;
+  if ((rpp >= 128 && u2 >= enough) || (rpp >= 64 && rpp < 128))
     return launch_gemm_shape<BT, 2>(P, n_pages, need_fixup, ctx, s);
   return launch_gemm_shape<BT, 1>(P, n_pages, need_fixup, ctx, s);
 }
