@@ -301,6 +301,25 @@ int boost_gemv_set_schedule(boost_ctx *ctx, int schedule, int host_workers);
 int boost_decode_gemv(boost_ctx *ctx, const boost_tensor *W, int N, int K,
                       const void *x, int B, void *y, int y_dtype, void *stream);
 
+/* The same product with the split-K reduction left to the consumer (§3.1
+ * matmul; the fold saves the reduction launch and its round trip through
+ * HBM between the projection and the element-wise step after it).  Writes
+ * the S partial sums to `slices`, fp32 [S][B][N] contiguous (caller-owned
+ * device memory of at least max_slices * B * N floats, 16-byte aligned), and
+ * S to *n_slices (host int): y[b, n] equals, bit for bit, the sum of
+ * slices[s][b][n] over s = 0..S-1 added in that order to 0.0f, the value
+ * boost_decode_gemv returns (fp32); S == 1 means slices[0] is y itself.  S
+ * is chosen as boost_decode_gemv chooses it, halved until the slices fit
+ * max_slices; it depends only on the shapes, the placement and the context,
+ * so it is known on the host when the call returns.  Only for tensors whose
+ * rows never cross a 2 MiB page (K divides 2^20; EINVAL otherwise), whose
+ * partials have no second part.  1 <= max_slices <= BOOST_MAX_GEMV_SLICES.
+ * Other arguments and errors as boost_decode_gemv. */
+#define BOOST_MAX_GEMV_SLICES 8
+int boost_decode_gemv_slices(boost_ctx *ctx, const boost_tensor *W, int N, int K,
+                             const void *x, int B, float *slices, int max_slices,
+                             int *n_slices, void *stream);
+
 /* ------------------------------------------- a2/a3: KV pool and allocator */
 
 /* KV pool placement modes. */
@@ -474,6 +493,14 @@ int boost_rmsnorm(boost_ctx *ctx, const float *x, const void *w, int B, int d,
 int boost_add_rmsnorm(boost_ctx *ctx, float *x, const float *r, const void *w, int B,
                       int d, float eps, void *out, void *stream);
 
+/* boost_add_rmsnorm with r handed over as the S split-K slices of
+ * boost_decode_gemv_slices (fp32 [S][B][d], 16-byte aligned): r is their
+ * slice-order sum, so x and out get the same bits as boost_decode_gemv
+ * followed by boost_add_rmsnorm.  1 <= S <= BOOST_MAX_GEMV_SLICES. */
+int boost_add_rmsnorm_slices(boost_ctx *ctx, float *x, const float *r, int S,
+                             const void *w, int B, int d, float eps, void *out,
+                             void *stream);
+
 /* Split the fused qkv output fp32 [B, (Hq + 2H) D] (query heads, then key
  * heads, then value heads) into bf16 q [B, Hq, D], k [B, H, D], v [B, H, D],
  * rotating query and key heads by RoPE at positions[b]: element i pairs with
@@ -499,6 +526,15 @@ int boost_rope_kv_append(boost_ctx *ctx, const boost_kv_pool *pool, int layer,
                          const float *qkv, const int32_t *positions, int B, int Hq,
                          double theta, const int32_t *block_tables, int max_blocks,
                          void *q, void *stream);
+
+/* boost_rope_kv_append with qkv handed over as the S split-K slices of
+ * boost_decode_gemv_slices (fp32 [S][B][(Hq + 2H) D]): every element is their
+ * slice-order sum, so q and the pool get the same bits as boost_decode_gemv
+ * followed by boost_rope_kv_append.  1 <= S <= BOOST_MAX_GEMV_SLICES. */
+int boost_rope_kv_append_slices(boost_ctx *ctx, const boost_kv_pool *pool, int layer,
+                                const float *qkv, int S, const int32_t *positions, int B,
+                                int Hq, double theta, const int32_t *block_tables,
+                                int max_blocks, void *q, void *stream);
 
 /* out[b, j] = bf16(silu(gu[b, j]) * gu[b, F + j]) for the fused gate_up
  * output fp32 [B, 2F] (gate rows first). */

@@ -55,6 +55,10 @@ struct GemvParams {
   int S;     // K slices per row group (matrix-core path; 1 = no split)
   float* ws;  // S > 1: [S][B][N] partials, then [(n_pages + 1) * 2][S][B] of cut rows
   float* partial;  // [(n_pages + 1) boundaries][2 sides][kMaxGemvBatch]
+  // host side only: a caller's buffer for the K slices ([S][B][N] partial
+  // sums, summed by the consumer instead of split_reduce) and its size
+  float* slices;
+  int64_t slice_floats;
 };
 
 __device__ __forceinline__ float lo_bf16(uint32_t v) { return __uint_as_float(v << 16); }
@@ -1068,6 +1072,18 @@ int64_t plan_grid(GemvParams& P, int n_pages, int rows_wg, const boost_ctx* ctx,
   return grid > 0x7fffffff ? -1 : grid;
 }
 
+// Largest S (halving from `want`) whose partials fit: the context's
+// workspace ([S][B][N] plus the cut rows' parts), or the caller's slice
+// buffer ([S][B][N]; a tensor without cut rows).
+int fit_slices(const GemvParams& P, int n_pages, int want, const boost_ctx* ctx) {
+  int S = want;
+  const uint64_t per = P.slices ? static_cast<uint64_t>(P.B) * P.N
+                                : static_cast<uint64_t>(P.B) * (P.N + 2ull * (n_pages + 1));
+  const uint64_t cap = P.slices ? static_cast<uint64_t>(P.slice_floats) : ctx->gemm_ws_floats;
+  while (S > 1 && S * per > cap) S /= 2;
+  return S;
+}
+
 int launch_fixup(GemvParams& P, int n_pages, bool need_fixup, hipStream_t s) {
   if (need_fixup) {
     const int lanes = (n_pages - 1) * P.B;
@@ -1116,12 +1132,10 @@ int launch_mfma_shape(GemvParams& P, int n_pages, bool need_fixup, const boost_c
   const int64_t units = static_cast<int64_t>(n_pages) * P.units_per_page;
   int S = 1;
   while (S < kMaxSlices && units * S < 2 * ctx->n_cu && P.K / (2 * S) >= 512) S *= 2;
-  while (S > 1 && static_cast<uint64_t>(S) * P.B * (P.N + 2ull * (n_pages + 1)) >
-                      ctx->gemm_ws_floats)
-    S /= 2;
+  S = fit_slices(P, n_pages, S, ctx);
   if (S > 1) {
     P.S = S;
-    P.ws = ctx->gemm_ws;
+    P.ws = P.slices ? P.slices : ctx->gemm_ws;
     P.units_per_page *= S;
     grid = P.address_order ? static_cast<int64_t>(n_pages) * P.units_per_page
                            : P.host_workers + static_cast<int64_t>(P.n_hbm_pages) *
@@ -1131,6 +1145,7 @@ int launch_mfma_shape(GemvParams& P, int n_pages, bool need_fixup, const boost_c
                      dim3(kThreads), 0, s, P);
   BOOST_HIP(hipGetLastError());
   if (S == 1) return launch_fixup(P, n_pages, need_fixup, s);
+  if (P.slices) return BOOST_OK;  // the consumer sums the slices
   const int64_t lanes = static_cast<int64_t>(P.B) * P.N;
   hipLaunchKernelGGL(split_reduce, dim3(static_cast<unsigned>((lanes + 255) / 256)), dim3(256),
                      0, s, P);
@@ -1167,12 +1182,10 @@ int launch_gemm_shape(GemvParams& P, int n_pages, bool need_fixup, const boost_c
   while (S < kMaxSlices && P.K / (2 * S) >= 512 &&
          (units * S < ctx->n_cu * BOOST_GEMM_WG_X4 / 4 || P.K / S > 16384))
     S *= 2;
-  while (S > 1 && static_cast<uint64_t>(S) * P.B * (P.N + 2ull * (n_pages + 1)) >
-                      ctx->gemm_ws_floats)
-    S /= 2;
+  S = fit_slices(P, n_pages, S, ctx);
   if (S > 1) {
     P.S = S;
-    P.ws = ctx->gemm_ws;
+    P.ws = P.slices ? P.slices : ctx->gemm_ws;
     P.units_per_page *= S;
   }
   if (P.address_order) {
@@ -1192,6 +1205,7 @@ int launch_gemm_shape(GemvParams& P, int n_pages, bool need_fixup, const boost_c
                        dim3(kThreads), 0, s, P);
   BOOST_HIP(hipGetLastError());
   if (S == 1) return launch_fixup(P, n_pages, need_fixup, s);
+  if (P.slices) return BOOST_OK;  // the consumer sums the slices
   const int64_t lanes = static_cast<int64_t>(P.B) * P.N;
   hipLaunchKernelGGL(split_reduce, dim3(static_cast<unsigned>((lanes + 255) / 256)), dim3(256),
                      0, s, P);
@@ -1265,20 +1279,16 @@ int launch_b(GemvParams& P, int n_pages, bool need_fixup, const boost_ctx* ctx,
 
 using namespace bst;
 
-extern "C" {
+namespace {
 
-int boost_gemv_set_schedule(boost_ctx* ctx, int schedule, int host_workers) {
-  if (!ctx) return fail(BOOST_EINVAL, "null ctx");
-  if (schedule != BOOST_SCHED_ADDRESS && schedule != BOOST_SCHED_CAP)
-    return fail(BOOST_EINVAL, "schedule %d", schedule);
-  if (host_workers < 0) return fail(BOOST_EINVAL, "host_workers %d", host_workers);
-  ctx->gemv_schedule = schedule;
-  ctx->gemv_host_workers = host_workers;
-  return BOOST_OK;
-}
+int dispatch(GemvParams& P, const boost_tensor* W, int K, int B, const boost_ctx* ctx,
+             hipStream_t s);
 
-int boost_decode_gemv(boost_ctx* ctx, const boost_tensor* W, int N, int K, const void* x,
-                      int B, void* y, int y_dtype, void* stream) {
+// The decode GEMV behind both entry points: y, or with `slices` the split-K
+// partial sums [S][B][N] in fp32 (S reported through n_slices).
+int decode_gemv(boost_ctx* ctx, const boost_tensor* W, int N, int K, const void* x, int B,
+                void* y, int y_dtype, float* slices, int64_t slice_floats, int* n_slices,
+                void* stream) {
   if (!ctx || !W || !x || !y) return fail(BOOST_EINVAL, "null argument");
   if (ctx->device < 0) return fail(BOOST_ENODEV, "plan-only context");
   if (N < 1 || K < 8 || K % 8) return fail(BOOST_EINVAL, "N=%d K=%d (K %% 8 == 0)", N, K);
@@ -1307,8 +1317,16 @@ int boost_decode_gemv(boost_ctx* ctx, const boost_tensor* W, int N, int K, const
   P.y = y;
   P.y_bf16 = y_dtype == BOOST_DTYPE_BF16;
   P.partial = W->d_partial;
+  P.slices = slices;
+  P.slice_floats = slice_floats;
   P.B = B;
-  auto s = static_cast<hipStream_t>(stream);
+  const int r = dispatch(P, W, K, B, ctx, static_cast<hipStream_t>(stream));
+  if (r == BOOST_OK && n_slices) *n_slices = std::max(1, P.S);
+  return r;
+}
+
+int dispatch(GemvParams& P, const boost_tensor* W, int K, int B, const boost_ctx* ctx,
+             hipStream_t s) {
   const int n = static_cast<int>(W->n_pages);
   P.n_pages = n;
   P.tiers = W->d_tiers;
@@ -1345,6 +1363,43 @@ int boost_decode_gemv(boost_ctx* ctx, const boost_tensor* W, int N, int K, const
     case 7: return launch_b<7>(P, n, fix, ctx, s);
     default: return launch_b<8>(P, n, fix, ctx, s);
   }
+}
+
+}  // namespace
+
+extern "C" {
+
+int boost_gemv_set_schedule(boost_ctx* ctx, int schedule, int host_workers) {
+  if (!ctx) return fail(BOOST_EINVAL, "null ctx");
+  if (schedule != BOOST_SCHED_ADDRESS && schedule != BOOST_SCHED_CAP)
+    return fail(BOOST_EINVAL, "schedule %d", schedule);
+  if (host_workers < 0) return fail(BOOST_EINVAL, "host_workers %d", host_workers);
+  ctx->gemv_schedule = schedule;
+  ctx->gemv_host_workers = host_workers;
+  return BOOST_OK;
+}
+
+
+int boost_decode_gemv(boost_ctx* ctx, const boost_tensor* W, int N, int K, const void* x,
+                      int B, void* y, int y_dtype, void* stream) {
+  return decode_gemv(ctx, W, N, K, x, B, y, y_dtype, nullptr, 0, nullptr, stream);
+}
+
+int boost_decode_gemv_slices(boost_ctx* ctx, const boost_tensor* W, int N, int K,
+                             const void* x, int B, float* slices, int max_slices,
+                             int* n_slices, void* stream) {
+  if (!slices || !n_slices) return fail(BOOST_EINVAL, "null argument");
+  if (max_slices < 1 || max_slices > BOOST_MAX_GEMV_SLICES)
+    return fail(BOOST_EINVAL, "max_slices %d outside [1, %d]", max_slices, BOOST_MAX_GEMV_SLICES);
+  if (K < 1 || kPageElems % K != 0)
+    return fail(BOOST_EINVAL, "K=%d: rows cross page boundaries (K must divide %lld)", K,
+                static_cast<long long>(kPageElems));
+  if (reinterpret_cast<uintptr_t>(slices) & 15)
+    return fail(BOOST_EINVAL, "slices must be 16-byte aligned");
+  *n_slices = 0;
+  const int64_t cap = static_cast<int64_t>(max_slices) * B * N;
+  return decode_gemv(ctx, W, N, K, x, B, slices, BOOST_DTYPE_F32, slices, cap, n_slices,
+                     stream);
 }
 
 }  // extern "C"

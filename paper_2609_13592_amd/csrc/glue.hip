@@ -21,6 +21,25 @@ __device__ __forceinline__ uint16_t to_bf16(float f) {
   return static_cast<uint16_t>(u >> 16);
 }
 
+// Element i of a split-K GEMV output handed over as its S partial slices
+// (slice stride `stride` floats): the slices summed in slice order from zero,
+// the additions the GEMV's own reduction kernel makes, so a consumer that
+// takes the slices sees the same bits as one that takes the reduced output.
+// S == 1 is the unsplit output itself.
+// All S loads go out together (a loop over a run-time S would wait for
+// each in turn), then the sums in slice order.
+__device__ __forceinline__ float slice_sum(const float* p, int S, int64_t stride, int64_t i) {
+  if (S == 1) return p[i];
+  float part[BOOST_MAX_GEMV_SLICES];
+#pragma unroll
+  for (int s = 0; s < BOOST_MAX_GEMV_SLICES; ++s) part[s] = s < S ? p[s * stride + i] : 0.f;
+  float v = 0.f;
+#pragma unroll
+  for (int s = 0; s < BOOST_MAX_GEMV_SLICES; ++s)
+    if (s < S) v += part[s];
+  return v;
+}
+
 // One lane per 8 elements of one row; the row of token t is read through the
 // embedding tensor's page table.
 __global__ __launch_bounds__(256) void embed_gather_kernel(const char* const* __restrict__ pt,
@@ -47,10 +66,12 @@ __global__ __launch_bounds__(256) void embed_gather_kernel(const char* const* __
 // One workgroup per row: sum of squares in a fixed order, then
 // y = bf16(x * (1 / sqrt(mean + eps)) * w).  With ADD the row first takes
 // the residual r (x += r in fp32, stored back), the same additions the
-// separate residual add makes, so the fused call gives the same bits.
+// separate residual add makes, so the fused call gives the same bits; r may
+// come as S split-K slices of stride rs floats (see slice_sum).
 template <bool ADD>
 __global__ __launch_bounds__(256) void rmsnorm_kernel(float* __restrict__ x,
-                                                      const float* __restrict__ r,
+                                                      const float* __restrict__ r, int S,
+                                                      int64_t rs,
                                                       const uint16_t* __restrict__ w, int d,
                                                       float eps, uint16_t* __restrict__ y) {
   __shared__ float part[4];
@@ -59,7 +80,7 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(float* __restrict__ x,
   for (int i = threadIdx.x; i < d; i += 256) {
     float v = row[i];
     if constexpr (ADD) {
-      v += r[static_cast<int64_t>(blockIdx.x) * d + i];
+      v += slice_sum(r, S, rs, static_cast<int64_t>(blockIdx.x) * d + i);
       row[i] = v;  // read back below by this same lane
     }
     s = fmaf(v, v, s);
@@ -82,7 +103,8 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(float* __restrict__ x,
 constexpr int kNormVec = 8;
 template <bool ADD>
 __global__ __launch_bounds__(256) void rmsnorm_vec_kernel(float* __restrict__ x,
-                                                          const float* __restrict__ r,
+                                                          const float* __restrict__ r, int S,
+                                                          int64_t rs,
                                                           const uint16_t* __restrict__ w,
                                                           int d, float eps,
                                                           uint16_t* __restrict__ y) {
@@ -96,17 +118,52 @@ __global__ __launch_bounds__(256) void rmsnorm_vec_kernel(float* __restrict__ x,
     v[u] = i < n4 ? row[i] : make_float4(0.f, 0.f, 0.f, 0.f);
   }
   if constexpr (ADD) {
-    const float4* res =
-        reinterpret_cast<const float4*>(r + static_cast<int64_t>(blockIdx.x) * d);
+    // the residual, or the slice-order sum of its S slices (see slice_sum),
+    // taken in groups of four slices whose loads of the whole row go out
+    // before the group's additions (uniform guards, no waits between)
+    float4 a[kNormVec];
+    const float* r0 = r + static_cast<int64_t>(blockIdx.x) * d;
+    if (S == 1) {
+#pragma unroll
+      for (int u = 0; u < kNormVec; ++u) {
+        const int i = threadIdx.x + u * 256;
+        a[u] = i < n4 ? reinterpret_cast<const float4*>(r0)[i] : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+    } else {
+      const int nu = (n4 + 255) / 256;
+#pragma unroll
+      for (int u = 0; u < kNormVec; ++u) a[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+      for (int s0 = 0; s0 < S; s0 += 4) {
+        float4 t[kNormVec][4];
+#pragma unroll
+        for (int u = 0; u < kNormVec; ++u)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int i = threadIdx.x + u * 256;
+            t[u][j] = u < nu && s0 + j < S && i < n4
+                          ? reinterpret_cast<const float4*>(r0 + (s0 + j) * rs)[i]
+                          : make_float4(0.f, 0.f, 0.f, 0.f);
+          }
+#pragma unroll
+        for (int u = 0; u < kNormVec; ++u)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            if (s0 + j < S) {
+              a[u].x += t[u][j].x;
+              a[u].y += t[u][j].y;
+              a[u].z += t[u][j].z;
+              a[u].w += t[u][j].w;
+            }
+      }
+    }
 #pragma unroll
     for (int u = 0; u < kNormVec; ++u) {
       const int i = threadIdx.x + u * 256;
       if (i < n4) {
-        const float4 a = res[i];
-        v[u].x += a.x;
-        v[u].y += a.y;
-        v[u].z += a.z;
-        v[u].w += a.w;
+        v[u].x += a[u].x;
+        v[u].y += a[u].y;
+        v[u].z += a[u].z;
+        v[u].w += a[u].w;
         row[i] = v[u];
       }
     }
@@ -156,9 +213,11 @@ struct PoolSlot {
 // double precision); value heads are converted.  With POOL the key and value
 // heads go to the token's slot of the pool (the same bits the KV append
 // copies there), skipped like the append skips a position or block outside
-// the table or the pool.
+// the table or the pool.  qkv may come as S split-K slices of stride qs
+// floats (see slice_sum).
 template <bool POOL>
-__global__ __launch_bounds__(64) void rope_qkv_kernel(const float* __restrict__ qkv,
+__global__ __launch_bounds__(64) void rope_qkv_kernel(const float* __restrict__ qkv, int S,
+                                                      int64_t qs,
                                                       const int32_t* __restrict__ pos,
                                                       int Hq, int H, int D, double log2_theta,
                                                       uint16_t* __restrict__ q,
@@ -188,7 +247,7 @@ __global__ __launch_bounds__(64) void rope_qkv_kernel(const float* __restrict__ 
     dst = v + (static_cast<int64_t>(b) * H + (h - Hq - H)) * D;
   }
   for (int i = threadIdx.x; i < half; i += blockDim.x) {
-    const float a = src[i], c = src[i + half];
+    const float a = slice_sum(src, S, qs, i), c = slice_sum(src, S, qs, i + half);
     if (h >= Hq + H) {
       dst[i] = to_bf16(a);
       dst[i + half] = to_bf16(c);
@@ -329,8 +388,8 @@ int boost_embed_gather(boost_ctx* ctx, const boost_tensor* E, int V, int d,
 namespace {
 // x (+= r when r is given), then the norm; the row layout decides the
 // kernel, never r, so the fused and the separate calls take the same one
-int launch_rmsnorm(boost_ctx* ctx, float* x, const float* r, const void* w, int B, int d,
-                   float eps, void* out, void* stream) {
+int launch_rmsnorm(boost_ctx* ctx, float* x, const float* r, int S, const void* w, int B,
+                   int d, float eps, void* out, void* stream) {
   if (!ctx || !x || !w || !out) return fail(BOOST_EINVAL, "null argument");
   if (ctx->device < 0) return fail(BOOST_ENODEV, "plan-only context");
   if (B < 1 || d < 1 || !(eps >= 0.f)) return fail(BOOST_EINVAL, "B=%d d=%d eps=%g", B, d, eps);
@@ -342,14 +401,19 @@ int launch_rmsnorm(boost_ctx* ctx, float* x, const float* r, const void* w, int 
   auto s = static_cast<hipStream_t>(stream);
   auto wp = static_cast<const uint16_t*>(w);
   auto op = static_cast<uint16_t*>(out);
+  const int64_t rs = static_cast<int64_t>(B) * d;
   if (vec && r)
-    hipLaunchKernelGGL(rmsnorm_vec_kernel<true>, dim3(B), dim3(256), 0, s, x, r, wp, d, eps, op);
+    hipLaunchKernelGGL(rmsnorm_vec_kernel<true>, dim3(B), dim3(256), 0, s, x, r, S, rs, wp, d,
+                       eps, op);
   else if (vec)
-    hipLaunchKernelGGL(rmsnorm_vec_kernel<false>, dim3(B), dim3(256), 0, s, x, r, wp, d, eps, op);
+    hipLaunchKernelGGL(rmsnorm_vec_kernel<false>, dim3(B), dim3(256), 0, s, x, r, S, rs, wp, d,
+                       eps, op);
   else if (r)
-    hipLaunchKernelGGL(rmsnorm_kernel<true>, dim3(B), dim3(256), 0, s, x, r, wp, d, eps, op);
+    hipLaunchKernelGGL(rmsnorm_kernel<true>, dim3(B), dim3(256), 0, s, x, r, S, rs, wp, d, eps,
+                       op);
   else
-    hipLaunchKernelGGL(rmsnorm_kernel<false>, dim3(B), dim3(256), 0, s, x, r, wp, d, eps, op);
+    hipLaunchKernelGGL(rmsnorm_kernel<false>, dim3(B), dim3(256), 0, s, x, r, S, rs, wp, d, eps,
+                       op);
   BOOST_HIP(hipGetLastError());
   return BOOST_OK;
 }
@@ -360,14 +424,23 @@ extern "C" {
 int boost_rmsnorm(boost_ctx* ctx, const float* x, const void* w, int B, int d, float eps,
                   void* out, void* stream) {
   // the kernel without the residual never writes x
-  return launch_rmsnorm(ctx, const_cast<float*>(x), nullptr, w, B, d, eps, out, stream);
+  return launch_rmsnorm(ctx, const_cast<float*>(x), nullptr, 1, w, B, d, eps, out, stream);
 }
 
 int boost_add_rmsnorm(boost_ctx* ctx, float* x, const float* r, const void* w, int B, int d,
                       float eps, void* out, void* stream) {
   if (!r) return fail(BOOST_EINVAL, "null argument");
   if (reinterpret_cast<uintptr_t>(r) & 15) return fail(BOOST_EINVAL, "r must be 16-byte aligned");
-  return launch_rmsnorm(ctx, x, r, w, B, d, eps, out, stream);
+  return launch_rmsnorm(ctx, x, r, 1, w, B, d, eps, out, stream);
+}
+
+int boost_add_rmsnorm_slices(boost_ctx* ctx, float* x, const float* r, int S, const void* w,
+                             int B, int d, float eps, void* out, void* stream) {
+  if (!r) return fail(BOOST_EINVAL, "null argument");
+  if (reinterpret_cast<uintptr_t>(r) & 15) return fail(BOOST_EINVAL, "r must be 16-byte aligned");
+  if (S < 1 || S > BOOST_MAX_GEMV_SLICES)
+    return fail(BOOST_EINVAL, "S=%d outside [1, %d]", S, BOOST_MAX_GEMV_SLICES);
+  return launch_rmsnorm(ctx, x, r, S, w, B, d, eps, out, stream);
 }
 
 int boost_rope_qkv(boost_ctx* ctx, const float* qkv, const int32_t* positions, int B, int Hq,
@@ -377,7 +450,8 @@ int boost_rope_qkv(boost_ctx* ctx, const float* qkv, const int32_t* positions, i
   if (B < 1 || Hq < 1 || H < 1 || D < 2 || D % 2 || !(theta > 1.0))
     return fail(BOOST_EINVAL, "B=%d Hq=%d H=%d D=%d theta=%g", B, Hq, H, D, theta);
   hipLaunchKernelGGL(rope_qkv_kernel<false>, dim3(B * (Hq + 2 * H)), dim3(64), 0,
-                     static_cast<hipStream_t>(stream), qkv, positions, Hq, H, D, std::log2(theta),
+                     static_cast<hipStream_t>(stream), qkv, 1, int64_t{0}, positions, Hq, H, D,
+                     std::log2(theta),
                      static_cast<uint16_t*>(q), static_cast<uint16_t*>(k),
                      static_cast<uint16_t*>(v), PoolSlot{});
   BOOST_HIP(hipGetLastError());
@@ -387,6 +461,14 @@ int boost_rope_qkv(boost_ctx* ctx, const float* qkv, const int32_t* positions, i
 int boost_rope_kv_append(boost_ctx* ctx, const boost_kv_pool* p, int layer, const float* qkv,
                          const int32_t* positions, int B, int Hq, double theta,
                          const int32_t* block_tables, int max_blocks, void* q, void* stream) {
+  return boost_rope_kv_append_slices(ctx, p, layer, qkv, 1, positions, B, Hq, theta,
+                                     block_tables, max_blocks, q, stream);
+}
+
+int boost_rope_kv_append_slices(boost_ctx* ctx, const boost_kv_pool* p, int layer,
+                                const float* qkv, int S, const int32_t* positions, int B,
+                                int Hq, double theta, const int32_t* block_tables,
+                                int max_blocks, void* q, void* stream) {
   if (!ctx || !p || !qkv || !positions || !block_tables || !q)
     return fail(BOOST_EINVAL, "null argument");
   if (ctx->device < 0 || !p->d_page_table) return fail(BOOST_ENODEV, "plan-only pool");
@@ -396,12 +478,16 @@ int boost_rope_kv_append(boost_ctx* ctx, const boost_kv_pool* p, int layer, cons
   if (B < 1 || max_blocks < 1 || Hq < 1 || !(theta > 1.0) || kPage % (2ull * D) != 0)
     return fail(BOOST_EINVAL, "B=%d max_blocks=%d Hq=%d theta=%g D=%d", B, max_blocks, Hq,
                 theta, D);
+  if (S < 1 || S > BOOST_MAX_GEMV_SLICES)
+    return fail(BOOST_EINVAL, "S=%d outside [1, %d]", S, BOOST_MAX_GEMV_SLICES);
   const uint64_t P = p->geom.pages;
   const PoolSlot ps{p->d_page_table + 2ull * layer * P, p->d_page_table + (2ull * layer + 1) * P,
                     block_tables, max_blocks, static_cast<int>(p->cfg.block_tokens),
                     static_cast<int>(p->geom.nb)};
+  const int64_t qs = static_cast<int64_t>(B) * (Hq + 2 * H) * D;
   hipLaunchKernelGGL(rope_qkv_kernel<true>, dim3(B * (Hq + 2 * H)), dim3(64), 0,
-                     static_cast<hipStream_t>(stream), qkv, positions, Hq, H, D, std::log2(theta),
+                     static_cast<hipStream_t>(stream), qkv, S, qs, positions, Hq, H, D,
+                     std::log2(theta),
                      static_cast<uint16_t*>(q), nullptr, nullptr, ps);
   BOOST_HIP(hipGetLastError());
   return BOOST_OK;

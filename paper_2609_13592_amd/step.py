@@ -11,6 +11,11 @@ This module only sequences C-ABI calls and owns the activation buffers
 where every "residual_add -> rmsnorm" pair is one add_rmsnorm launch (the
 down projection's residual is added by the next layer's first norm, or by
 the final norm) and "rope_qkv -> kv_append" is one rope_kv_append launch.
+Where the qkv and o projections split K over workgroups, their partial
+slices go straight to the RoPE + KV append and to the residual norm, which
+sum them in the order the GEMV's own reduction kernel does (the same bits,
+one launch fewer per projection); a matrix whose rows cross page boundaries
+(K not dividing 2^20) keeps the reduction kernel.
 
 Weights are [out, in] bf16 matrices placed page by page (each tensor on its
 own, so modulo placement restarts per tensor); norm weights are small bf16
@@ -46,10 +51,11 @@ class Dims:
 
 class DecodeModel:
     def __init__(self, ctx: int, dims: Dims, batch: int, max_blocks: int, pool: int,
-                 matrices: dict, norms: dict):
+                 matrices: dict, norms: dict, fold_slices: bool = True):
         """matrices: name -> placed tensor handle for 'embed', 'lm_head' and
         '<kind>.<layer>'; norms: name -> device bf16 tensor for 'norm1.<l>',
-        'norm2.<l>', 'norm_f'."""
+        'norm2.<l>', 'norm_f'.  fold_slices: hand the split-K slices of qkv
+        and o to their consumers (False: every projection reduces its own)."""
         import torch
         self.ctx, self.dims, self.B, self.mb, self.pool = ctx, dims, batch, max_blocks, pool
         self.mat, self.norms = matrices, norms
@@ -59,7 +65,12 @@ class DecodeModel:
         B = batch
         self.x = torch.zeros((B, D.d), dtype=f32, device=dev)
         self.h = torch.zeros((B, D.d), dtype=b16, device=dev)
-        self.qkv = torch.zeros((B, (D.hq + 2 * D.hkv) * D.hd), dtype=f32, device=dev)
+        qkv_n = (D.hq + 2 * D.hkv) * D.hd
+        folds = lambda K: fold_slices and bd.PAGE_BYTES // 2 % K == 0
+        self.fold_qkv, self.fold_o = folds(D.d), folds(D.hq * D.hd)
+        S = bd.MAX_GEMV_SLICES
+        self.qkv = torch.zeros((S if self.fold_qkv else 1, B, qkv_n), dtype=f32, device=dev)
+        self.o_sl = torch.zeros((S, B, D.d), dtype=f32, device=dev) if self.fold_o else None
         self.q = torch.zeros((B, D.hq, D.hd), dtype=b16, device=dev)
         self.o = torch.zeros((B, D.hq, D.hd), dtype=b16, device=dev)
         self.tmp = torch.zeros((B, D.d), dtype=f32, device=dev)
@@ -90,15 +101,28 @@ class DecodeModel:
                                      EPS, self.h, s)
             else:
                 bd.boost_rmsnorm(c, self.x, self.norms[f"norm1.{l}"], B, D.d, EPS, self.h, s)
-            bd.boost_decode_gemv(c, self.mat[f"qkv.{l}"], qkv_n, D.d, self.h, B, self.qkv, F32, s)
-            bd.boost_rope_kv_append(c, self.pool, l, self.qkv, positions, B, D.hq, THETA,
-                                    tables, self.mb, self.q, s)
+            if self.fold_qkv:
+                S = bd.boost_decode_gemv_slices(c, self.mat[f"qkv.{l}"], qkv_n, D.d, self.h, B,
+                                                self.qkv, bd.MAX_GEMV_SLICES, s)
+                bd.boost_rope_kv_append_slices(c, self.pool, l, self.qkv, S, positions, B, D.hq,
+                                               THETA, tables, self.mb, self.q, s)
+            else:
+                bd.boost_decode_gemv(c, self.mat[f"qkv.{l}"], qkv_n, D.d, self.h, B, self.qkv,
+                                     F32, s)
+                bd.boost_rope_kv_append(c, self.pool, l, self.qkv, positions, B, D.hq, THETA,
+                                        tables, self.mb, self.q, s)
             bd.boost_paged_attn_decode(c, self.pool, l, self.q, B, D.hq, tables, self.mb,
                                        lens, 0.0, self.o, BF16, s)
-            bd.boost_decode_gemv(c, self.mat[f"o.{l}"], D.d, D.hq * D.hd, self.o, B,
-                                 self.tmp, F32, s)
-            bd.boost_add_rmsnorm(c, self.x, self.tmp, self.norms[f"norm2.{l}"], B, D.d, EPS,
-                                 self.h, s)
+            if self.fold_o:
+                S = bd.boost_decode_gemv_slices(c, self.mat[f"o.{l}"], D.d, D.hq * D.hd, self.o,
+                                                B, self.o_sl, bd.MAX_GEMV_SLICES, s)
+                bd.boost_add_rmsnorm_slices(c, self.x, self.o_sl, S, self.norms[f"norm2.{l}"], B,
+                                            D.d, EPS, self.h, s)
+            else:
+                bd.boost_decode_gemv(c, self.mat[f"o.{l}"], D.d, D.hq * D.hd, self.o, B,
+                                     self.tmp, F32, s)
+                bd.boost_add_rmsnorm(c, self.x, self.tmp, self.norms[f"norm2.{l}"], B, D.d, EPS,
+                                     self.h, s)
             bd.boost_decode_gemv(c, self.mat[f"gate_up.{l}"], 2 * D.ffn, D.d, self.h, B,
                                  self.gu, F32, s)
             bd.boost_silu_mul(c, self.gu, B, D.ffn, self.act, s)

@@ -171,6 +171,90 @@ def test_add_rmsnorm_equals_add_then_norm(gpu_ctx, d):
     assert e.value.code == bd.EINVAL
 
 
+@pytest.mark.parametrize("d,S", [(4096, 1), (4096, 4), (8192, 8), (1026, 3)])
+def test_add_rmsnorm_slices_equals_sum_then_fused(gpu_ctx, d, S):
+    """With the residual handed over as S split-K slices, x and the norm get
+    the same bits as the fused call on the slices' slice-order fp32 sum
+    (vector path and plain loop); bad slice counts are refused."""
+    import torch
+    rng = np.random.default_rng(200 + d + S)
+    Bn = 6
+    x = (rng.standard_normal((Bn, d)) * 2).astype(np.float32)
+    sl = (rng.standard_normal((S, Bn, d)) * 2).astype(np.float32)
+    r = sl[0].copy()
+    if S > 1:
+        r = np.zeros((Bn, d), np.float32)
+        for s in range(S):
+            r = r + sl[s]
+    w = synth.round_bf16((1 + 0.1 * rng.standard_normal(d)).astype(np.float32))
+    wd = to_dev_u16(w)
+    x1, x2 = dev(x), dev(x)
+    o1 = torch.empty((Bn, d), dtype=torch.int16, device="cuda")
+    o2 = torch.empty((Bn, d), dtype=torch.int16, device="cuda")
+    bd.boost_add_rmsnorm(gpu_ctx, x1, dev(r), wd, Bn, d, 1e-5, o1, stream())
+    bd.boost_add_rmsnorm_slices(gpu_ctx, x2, dev(sl), S, wd, Bn, d, 1e-5, o2, stream())
+    sync()
+    assert np.array_equal(x2.cpu().numpy().view(np.uint32), (x + r).view(np.uint32))
+    assert np.array_equal(x1.cpu().numpy().view(np.uint32), x2.cpu().numpy().view(np.uint32))
+    assert np.array_equal(host_u16(o1), host_u16(o2))
+    assert_bf16_close(host_u16(o2), ods.to_bf16(ods.rmsnorm((x + r).astype(np.float64), w)))
+    for bad in (0, bd.MAX_GEMV_SLICES + 1):
+        with pytest.raises(bd.BoostError) as e:
+            bd.boost_add_rmsnorm_slices(gpu_ctx, x2, dev(sl), bad, wd, Bn, d, 1e-5, o2,
+                                        stream())
+        assert e.value.code == bd.EINVAL
+
+
+@pytest.mark.parametrize("S", [1, 2, 8])
+def test_rope_kv_append_slices_equals_sum(gpu_ctx, S):
+    """RoPE + KV append of S qkv slices writes the same q and pool slots as the
+    call on their slice-order fp32 sum (attention over the two pools agrees
+    bitwise)."""
+    import torch
+    rng = np.random.default_rng(30 + S)
+    heads = HQ + 2 * HKV
+    mb = 8
+    pos = np.array([0, 3, 15, 16, 40, 77, 100, 127], dtype=np.int32)
+    sl = rng.standard_normal((S, B, heads * HD)).astype(np.float32)
+    qkv = sl[0].copy()
+    if S > 1:
+        qkv = np.zeros((B, heads * HD), np.float32)
+        for s in range(S):
+            qkv = qkv + sl[s]
+    pools, outs, qs = [], [], []
+    try:
+        for sliced in (False, True):
+            pool = bd.boost_kv_pool_create(gpu_ctx, 1, HKV, HD, B * mb, 0, bd.KV_ALL_HBM,
+                                           q_heads=HQ, max_batch=B, max_blocks_per_seq=mb)
+            pools.append(pool)
+            tables = np.stack([bd.boost_kv_alloc(pool, b, mb) for b in range(B)]).astype(np.int32)
+            td, pd = dev(tables), dev(pos)
+            q = torch.empty((B, HQ, HD), dtype=torch.int16, device="cuda")
+            if sliced:
+                bd.boost_rope_kv_append_slices(gpu_ctx, pool, 0, dev(sl), S, pd, B, HQ,
+                                               500000.0, td, mb, q, stream())
+            else:
+                bd.boost_rope_kv_append(gpu_ctx, pool, 0, dev(qkv), pd, B, HQ, 500000.0, td, mb,
+                                        q, stream())
+            lens = (pos + 1).astype(np.int32)
+            out = torch.empty((B, HQ, HD), dtype=torch.float32, device="cuda")
+            bd.boost_paged_attn_decode(gpu_ctx, pool, 0, q, B, HQ, td, mb, dev(lens), 0.0, out,
+                                       bd.DTYPE_F32, stream())
+            sync()
+            qs.append(host_u16(q))
+            outs.append(out.cpu().numpy())
+        assert np.array_equal(qs[0], qs[1])
+        assert np.array_equal(outs[0].view(np.uint32), outs[1].view(np.uint32))
+        with pytest.raises(bd.BoostError) as e:
+            bd.boost_rope_kv_append_slices(gpu_ctx, pools[1], 0, dev(sl), 0, dev(pos), B, HQ,
+                                           500000.0, dev(np.zeros((B, mb), np.int32)), mb,
+                                           dev(qs[1]), stream())
+        assert e.value.code == bd.EINVAL
+    finally:
+        for p in pools:
+            bd.boost_kv_pool_destroy(p)
+
+
 def test_rope_kv_append_equals_pair(gpu_ctx):
     """The fused RoPE + KV append writes the same q as the RoPE call and the
     same pool slots as the KV append (two identical all-HBM pools, one filled
