@@ -1896,6 +1896,7 @@ def main():
     if not args.no_cpu_baseline:
         log("step: cpu baseline (oracle)")
         cpu = cpu_baseline(args.cpu_seconds)
+    host_numa = bd.boost_host_numa_info(ctx)
     chain.free()
     bd.boost_shutdown(ctx)
 
@@ -1924,7 +1925,8 @@ def main():
         },
         "tokens_per_s": round(1000.0 / ms, 2),
         "calibration": {"hbm_gbps": round(bw_hbm, 1), "host_gbps": round(bw_host, 2),
-                        "alpha": round(alpha, 6)},
+                        "alpha": round(alpha, 6),
+                        "host_numa": host_numa},
         "pct_combined_roofline": round(100 * eff / (bw_hbm + bw_host), 2),
         "hbm_only": {"ms_per_step": round(ms_hbm, 4), "value": round(eff_hbm, 2),
                      "pct_of_hbm_roofline": round(100 * eff_hbm / bw_hbm, 2)},

@@ -85,6 +85,22 @@ int boost_ctx_info(const boost_ctx *ctx, int *device, int *n_cu);
  * the GPU; default), 0 = non-coherent.  Affects pages placed afterwards. */
 int boost_set_host_coherent(boost_ctx *ctx, int coherent);
 
+/* NUMA node of host-tier pages (§4.4 binds every 2 MB host region to a
+ * chosen node).  BOOST_NUMA_DEVICE (default): HIP's choice, the node nearest
+ * the GPU; node >= 0: pages placed afterwards (weights, KV pool, calibration
+ * buffers) are pinned while the calling thread's memory policy binds them to
+ * that node, and the thread's previous policy is put back after each
+ * allocation.  Errors: EINVAL (null ctx, node not online; a refused policy
+ * call surfaces as EINVAL from the allocating call). */
+#define BOOST_NUMA_DEVICE (-1)
+int boost_set_host_numa(boost_ctx *ctx, int node);
+
+/* Host NUMA facts (any output may be NULL): the NUMA node of the context's
+ * GPU (-1 when the platform reports none or the context is plan-only), the
+ * number of online nodes, and the node set by boost_set_host_numa. */
+int boost_host_numa_info(const boost_ctx *ctx, int *device_node, int *n_nodes,
+                         int *node);
+
 /* ------------------------------------------------------- a0: calibration */
 
 /* Measure alpha (§2.3: host read bandwidth over HBM read bandwidth; the paper

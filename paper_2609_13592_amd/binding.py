@@ -66,6 +66,8 @@ _SIGS = {
     "boost_shutdown": (_i32, [_vp]),
     "boost_ctx_info": (_i32, [_vp, C.POINTER(_i32), C.POINTER(_i32)]),
     "boost_set_host_coherent": (_i32, [_vp, _i32]),
+    "boost_set_host_numa": (_i32, [_vp, _i32]),
+    "boost_host_numa_info": (_i32, [_vp, C.POINTER(_i32), C.POINTER(_i32), C.POINTER(_i32)]),
     "boost_calibrate": (_i32, [_vp, _u64, _u64, _i32, C.POINTER(_dbl),
                                C.POINTER(_dbl), C.POINTER(_dbl)]),
     "boost_stream_read_gbps": (_i32, [_vp, _vp, _u64, _i32, _i32, C.POINTER(_dbl)]),
@@ -215,6 +217,19 @@ def boost_ctx_info(ctx: int):
 
 def boost_set_host_coherent(ctx: int, coherent: bool):
     _check(load().boost_set_host_coherent(ctx, int(bool(coherent))))
+
+
+NUMA_DEVICE = -1
+
+
+def boost_set_host_numa(ctx: int, node: int):
+    _check(load().boost_set_host_numa(ctx, node))
+
+
+def boost_host_numa_info(ctx: int) -> dict:
+    dn, n, node = C.c_int32(0), C.c_int32(0), C.c_int32(0)
+    _check(load().boost_host_numa_info(ctx, C.byref(dn), C.byref(n), C.byref(node)))
+    return {"device_node": dn.value, "n_nodes": n.value, "node": node.value}
 
 
 # -------------------------------------------------------------- calibration

@@ -16,6 +16,7 @@ struct boost_ctx {
   int device = -1;          // -1: plan-only
   int n_cu = 0;
   int host_coherent = 1;
+  int host_numa = BOOST_NUMA_DEVICE;  // node that host-tier pages are bound to
   int gemv_schedule = BOOST_SCHED_CAP;
   int gemv_host_workers = 0;  // 0: default
   // split-K partials of the matrix-core GEMM (slices of K run by different

@@ -3,12 +3,100 @@
 // live in pinned, device-mapped host memory from hipHostMalloc (the MI355X
 // counterpart of the paper's mmap + mbind + host registration per 2 MB page);
 // a device page table gives every page's device-visible address.
+#include <linux/mempolicy.h>
+#include <sys/syscall.h>
+#include <unistd.h>
+
 #include <algorithm>
+#include <cerrno>
+#include <cstdio>
 #include <cstring>
 
 #include "runtime.h"
 
 namespace bst {
+
+namespace {
+
+// Bits of the node masks passed to the memory-policy calls (the kernel asks
+// get_mempolicy for at least its own node count).
+constexpr int kMaskWords = 16;
+constexpr unsigned long kMaskBits = 64ul * kMaskWords;
+
+// Online host NUMA nodes: a list of ids and ranges ("0", "0-3", "0,2-3").
+// Writes whether `node` is online; returns the count (1 when unreadable).
+int online_nodes(int node, bool* is_online) {
+  if (is_online) *is_online = node == 0;
+  FILE* f = std::fopen("/sys/devices/system/node/online", "r");
+  if (!f) return 1;
+  char buf[256] = {0};
+  const bool ok = std::fgets(buf, sizeof buf, f) != nullptr;
+  std::fclose(f);
+  if (!ok) return 1;
+  int count = 0;
+  if (is_online) *is_online = false;
+  for (char* p = buf; *p && *p != '\n';) {
+    char* end = nullptr;
+    const long a = std::strtol(p, &end, 10);
+    if (end == p) break;
+    long b = a;
+    p = end;
+    if (*p == '-') {
+      b = std::strtol(p + 1, &end, 10);
+      p = end;
+    }
+    count += static_cast<int>(b - a + 1);
+    if (is_online && node >= a && node <= b) *is_online = true;
+    if (*p == ',') ++p;
+  }
+  return std::max(count, 1);
+}
+
+// NUMA node of the GPU's PCIe function (sysfs), -1 when the platform gives
+// none.
+int device_numa_node(int device) {
+  char bus[64] = {0};
+  if (device < 0 || hipDeviceGetPCIBusId(bus, sizeof bus, device) != hipSuccess) return -1;
+  for (char* c = bus; *c; ++c)
+    if (*c >= 'A' && *c <= 'F') *c = static_cast<char>(*c - 'A' + 'a');
+  char path[160];
+  std::snprintf(path, sizeof path, "/sys/bus/pci/devices/%s/numa_node", bus);
+  FILE* f = std::fopen(path, "r");
+  if (!f) return -1;
+  int node = -1;
+  if (std::fscanf(f, "%d", &node) != 1) node = -1;
+  std::fclose(f);
+  return node;
+}
+
+// The calling thread's memory policy, saved around a bound allocation.
+struct ThreadPolicy {
+  int mode = MPOL_DEFAULT;
+  unsigned long mask[kMaskWords] = {};
+  bool saved = false;
+};
+
+// Bind this thread's page allocations to `node` (§4.4 binds each 2 MiB
+// region of the host tier to a chosen node); `old` keeps the policy to put
+// back.
+int bind_thread(int node, ThreadPolicy& old) {
+  if (syscall(SYS_get_mempolicy, &old.mode, old.mask, kMaskBits, nullptr, 0) != 0)
+    return fail(BOOST_EINVAL, "get_mempolicy failed (errno %d)", errno);
+  old.saved = true;
+  unsigned long mask[kMaskWords] = {};
+  mask[node / 64] = 1ul << (node % 64);
+  if (syscall(SYS_set_mempolicy, MPOL_BIND, mask, kMaskBits) != 0)
+    return fail(BOOST_EINVAL, "set_mempolicy(node %d) failed (errno %d)", node, errno);
+  return BOOST_OK;
+}
+
+void restore_thread(const ThreadPolicy& old) {
+  if (!old.saved) return;
+  const bool none = (old.mode & ~(MPOL_F_STATIC_NODES | MPOL_F_RELATIVE_NODES)) == MPOL_DEFAULT;
+  (void)syscall(SYS_set_mempolicy, old.mode, none ? nullptr : old.mask, none ? 0 : kMaskBits);
+}
+
+}  // namespace
 
 int slab_alloc(boost_ctx* ctx, uint64_t pages, bool host, Slab& s) {
   s = Slab{};
@@ -23,7 +111,19 @@ int slab_alloc(boost_ctx* ctx, uint64_t pages, bool host, Slab& s) {
     unsigned flags = hipHostMallocMapped |
                      (ctx->host_coherent ? hipHostMallocCoherent
                                          : hipHostMallocNonCoherent);
+    // a chosen node: the pages follow this thread's policy while they are
+    // pinned; by default HIP takes the node nearest the GPU
+    ThreadPolicy old;
+    if (ctx->host_numa >= 0) {
+      flags |= hipHostMallocNumaUser;
+      const int rc = bind_thread(ctx->host_numa, old);
+      if (rc) {
+        restore_thread(old);
+        return rc;
+      }
+    }
     hipError_t e = hipHostMalloc(&s.raw, bytes, flags);
+    restore_thread(old);
     if (e != hipSuccess || !s.raw)
       return fail(BOOST_ENOMEM, "hipHostMalloc(%zu) failed: %s", bytes,
                   hipGetErrorString(e));
@@ -233,6 +333,26 @@ int boost_ctx_info(const boost_ctx* ctx, int* device, int* n_cu) {
 int boost_set_host_coherent(boost_ctx* ctx, int coherent) {
   if (!ctx) return fail(BOOST_EINVAL, "null ctx");
   ctx->host_coherent = coherent ? 1 : 0;
+  return BOOST_OK;
+}
+
+int boost_set_host_numa(boost_ctx* ctx, int node) {
+  if (!ctx) return fail(BOOST_EINVAL, "null ctx");
+  if (node != BOOST_NUMA_DEVICE) {
+    bool online = false;
+    online_nodes(node, &online);
+    if (node < 0 || node >= static_cast<int>(kMaskBits) - 1 || !online)
+      return fail(BOOST_EINVAL, "NUMA node %d is not online", node);
+  }
+  ctx->host_numa = node;
+  return BOOST_OK;
+}
+
+int boost_host_numa_info(const boost_ctx* ctx, int* device_node, int* n_nodes, int* node) {
+  if (!ctx) return fail(BOOST_EINVAL, "null ctx");
+  if (device_node) *device_node = device_numa_node(ctx->device);
+  if (n_nodes) *n_nodes = online_nodes(-1, nullptr);
+  if (node) *node = ctx->host_numa;
   return BOOST_OK;
 }
 

@@ -42,6 +42,41 @@ def test_plan_only_context():
     bd.boost_shutdown(ctx)
 
 
+def _online_nodes():
+    """Node ids listed in /sys/devices/system/node/online ("0", "0-3", "0,2")."""
+    try:
+        txt = open("/sys/devices/system/node/online").read().strip()
+    except OSError:
+        return [0]
+    ids = []
+    for part in txt.split(","):
+        lo, _, hi = part.partition("-")
+        ids += list(range(int(lo), int(hi or lo) + 1))
+    return ids
+
+
+def test_host_numa_setting():
+    """The host-tier NUMA node: HIP's choice by default, any online node on
+    request, anything else refused; a plan-only context has no device node."""
+    ctx = bd.boost_init(-1)
+    try:
+        nodes = _online_nodes()
+        info = bd.boost_host_numa_info(ctx)
+        assert info == {"device_node": -1, "n_nodes": len(nodes), "node": bd.NUMA_DEVICE}
+        for n in nodes:
+            bd.boost_set_host_numa(ctx, n)
+            assert bd.boost_host_numa_info(ctx)["node"] == n
+        for bad in (-2, max(nodes) + 1, 5000):
+            with pytest.raises(bd.BoostError) as e:
+                bd.boost_set_host_numa(ctx, bad)
+            assert e.value.code == bd.EINVAL
+        assert bd.boost_host_numa_info(ctx)["node"] == nodes[-1]
+        bd.boost_set_host_numa(ctx, bd.NUMA_DEVICE)
+        assert bd.boost_host_numa_info(ctx)["node"] == bd.NUMA_DEVICE
+    finally:
+        bd.boost_shutdown(ctx)
+
+
 def test_cap_sweep_needs_a_device():
     ctx = bd.boost_init(-1)
     try:

@@ -442,3 +442,28 @@ def test_slices_bad_arguments(gpu_ctx):
             assert e.value.code == bd.EINVAL
     finally:
         bd.boost_tensor_free(t)
+
+
+def test_host_pages_bound_to_a_numa_node(gpu_ctx):
+    """Host pages pinned under a policy bound to node 0 (present on every
+    host) serve the GEMV with the same bits as HIP's default node."""
+    w, x = synth.gemv_inputs(5, 1024, 4096, 2)
+    tiers = (np.arange(opl.n_pages(w.nbytes)) % 2).astype(np.uint8)
+    xd = to_dev_u16(x)
+    info = bd.boost_host_numa_info(gpu_ctx)
+    assert info["n_nodes"] >= 1 and info["node"] == bd.NUMA_DEVICE
+    assert info["device_node"] >= -1
+    ys = []
+    try:
+        for node in (0, bd.NUMA_DEVICE):
+            bd.boost_set_host_numa(gpu_ctx, node)
+            t = place(gpu_ctx, w, tiers=tiers)
+            try:
+                assert int(bd.boost_tensor_tiers(t).sum()) == int(tiers.sum())
+                ys.append(run_gemv(gpu_ctx, t, 1024, 4096, xd, 2))
+            finally:
+                bd.boost_tensor_free(t)
+    finally:
+        bd.boost_set_host_numa(gpu_ctx, bd.NUMA_DEVICE)
+    assert og.rel_err(ys[0], og.gemv_f64(w, x)) <= TOL
+    assert np.array_equal(ys[0].view(np.uint32), ys[1].view(np.uint32))
