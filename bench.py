@@ -72,7 +72,7 @@ def parse():
     p.add_argument("--workload", default="chain8b",
                    choices=("chain8b", "llama70b", "throughput8b", "host_share_sweep",
                             "cap_probe", "batch_sweep", "placements", "dsr_churn",
-                            "tier_counters"),
+                            "tier_counters", "gemm_shapes"),
                    help="chain8b: decode weight chain (default); llama70b: full 70B-"
                         "shaped decode step under a 120 GB HBM weight budget; "
                         "throughput8b: 8B-shaped decode at up to 256 requests under a "
@@ -81,7 +81,10 @@ def parse():
                         "(modulus sweep, batch sensitivity, contrast placements, "
                         "allocator under Poisson arrivals, concurrent streaming "
                         "probe); tier_counters: one tiered call of --part for a "
-                        "counter run")
+                        "counter run; gemm_shapes: the 8B layer matrices all-HBM at "
+                        "--batches")
+    p.add_argument("--batches", default="16,32,64,128,256",
+                   help="gemm_shapes: batch sizes (comma-separated, 1..256)")
     p.add_argument("--host-pin-gib", type=float, default=56.0,
                    help="throughput8b: pinned host memory the capacity-limited literal "
                         "variant may give its KV overflow (a process pins at most ~64 GiB "
@@ -1099,6 +1102,71 @@ def _seeded_weight(torch, N, K, seed):
     return w.to(torch.bfloat16).view(torch.int16)
 
 
+def gemm_shapes(args, bd, ctx, torch, bw_hbm, bw_host, alpha, M):
+    """All-HBM time of the Llama-3-8B layer matrices (fused qkv, o, fused
+    gate_up, down) at the batches of --batches, each call on the next of
+    enough placed copies to cover 512 MiB, so no call finds its weights in
+    the 256 MB memory-side cache.  Roofline fraction: algorithmic bytes
+    (weights, x, y) over the call time against 8 TB/s, or flops against the
+    2.5 PFLOP/s dense bf16 peak, whichever is higher.  Beside each: the
+    vendor BLAS (torch's linear on plain contiguous copies, bf16 out) on the
+    same shape, as a reference point for the kernel."""
+    shapes = [("qkv", 6144, 4096), ("o", 4096, 4096), ("gate_up", 28672, 4096),
+              ("down", 4096, 14336)]
+    batches = [int(b) for b in args.batches.split(",")]
+    if not batches or min(batches) < 1 or max(batches) > 256:
+        raise SystemExit("--batches: sizes in 1..256")
+    rows = []
+    for si, (name, N, K) in enumerate(shapes):
+        nbytes = N * K * 2
+        n = -(-nbytes // bd.PAGE_BYTES)
+        w = _seeded_weight(torch, N, K, 501 + si)
+        n_copies = -(-(512 << 20) // nbytes)
+        copies = [bd.boost_place_weights_map(ctx, w, nbytes, np.zeros(n, np.uint8))
+                  for _ in range(n_copies)]
+        plain = [w.view(torch.bfloat16).clone() for _ in range(n_copies)]
+        del w
+        torch.cuda.empty_cache()
+        g = torch.Generator(device="cuda")
+        g.manual_seed(11)
+        xs = torch.randn((max(batches), K), generator=g, device="cuda").to(
+            torch.bfloat16).view(torch.int16)
+        y = torch.empty((max(batches), N), dtype=torch.float32, device="cuda")
+        for B in batches:
+            log(f"step: gemm_shapes {name} B={B}")
+            x = xs[:B].contiguous()
+            us = _gemv_us(bd, ctx, torch, copies, N, K, x, B, y, max(3, args.steps))
+            alg = nbytes + B * K * 2 + B * N * 4
+            gbps, tflops = alg / us / 1e3, 2 * N * K * B / us / 1e6
+            xb = x.view(torch.bfloat16)
+
+            def blas():
+                for wp in plain:
+                    torch.nn.functional.linear(xb, wp)
+            blas()
+            torch.cuda.synchronize()
+            us_blas = float(np.median(time_steps(torch, blas, max(3, args.steps)))) * 1e3 / len(plain)
+            rows.append({"matrix": name, "N": N, "K": K, "B": B, "us": round(us, 2),
+                         "gbps": round(gbps, 1), "tflops": round(tflops, 1),
+                         "frac": round(max(gbps / 8000.0, tflops / 2500.0), 4),
+                         "vendor_blas_us": round(us_blas, 2)})
+        for h in copies:
+            bd.boost_tensor_free(h)
+        del plain
+        del xs, y
+        torch.cuda.empty_cache()
+    fr = [r["frac"] for r in rows]
+    return {"metric": "skinny GEMM roofline fraction of the 8B layer matrices (all-HBM)",
+            "value": round(float(np.exp(np.mean(np.log(fr)))), 4), "unit": "frac (geomean)",
+            "n_gpus": 1, "higher_is_better": True, "dtype": "bf16", "data": "synthetic",
+            "config": {"workload": "Llama-3-8B layer matrices [6144|4096|28672|4096 x "
+                                   "4096|4096|4096|14336], all pages in HBM",
+                       "batches": batches},
+            "calibration": {"hbm_gbps": round(bw_hbm, 1), "host_gbps": round(bw_host, 2),
+                            "alpha": round(alpha, 6)},
+            "rows": rows}
+
+
 def host_share_sweep(args, bd, ctx, torch, bw_hbm, bw_host, alpha, M_alpha):
     """Speedup of a tiered GEMV over all-HBM as the host share grows (the
     host-share sweep of §3): one 2 GiB bf16 matrix [131072 x 8192] (1024
@@ -1784,6 +1852,8 @@ def main():
     exp = {"host_share_sweep": lambda: host_share_sweep(args, bd, ctx, torch, bw_hbm,
                                                         bw_host, alpha, M),
            "cap_probe": lambda: cap_probe(args, bd, ctx, torch, bw_hbm, bw_host, alpha, M),
+           "gemm_shapes": lambda: gemm_shapes(args, bd, ctx, torch, bw_hbm, bw_host,
+                                              alpha, M),
            "batch_sweep": lambda: batch_sweep(args, bd, ctx, torch, bw_hbm, bw_host,
                                               alpha, M),
            "placements": lambda: placements_bench(args, bd, ctx, torch, bw_hbm, bw_host,
