@@ -320,21 +320,31 @@ int boost_decode_gemv(boost_ctx *ctx, const boost_tensor *W, int N, int K,
 /* The same product with the split-K reduction left to the consumer (§3.1
  * matmul; the fold saves the reduction launch and its round trip through
  * HBM between the projection and the element-wise step after it).  Writes
- * the S partial sums to `slices`, fp32 [S][B][N] contiguous (caller-owned
- * device memory of at least max_slices * B * N floats, 16-byte aligned), and
- * S to *n_slices (host int): y[b, n] equals, bit for bit, the sum of
- * slices[s][b][n] over s = 0..S-1 added in that order to 0.0f, the value
- * boost_decode_gemv returns (fp32); S == 1 means slices[0] is y itself.  S
- * is chosen as boost_decode_gemv chooses it, halved until the slices fit
+ * the split-K partial sums to `slices` (caller-owned device memory of
+ * boost_gemv_slices_floats(N, K, B, max_slices) floats, 16-byte aligned) and
+ * their count S to *n_slices (host int).  Layout: fp32 [S][B][N], then, for
+ * every row of W that crosses a 2 MiB page (rows r with r K and r K + K - 1
+ * on different pages), its two parts: part h (0: the columns on the earlier
+ * page, 1: on the later) of slice s for batch row b at
+ * [S B N + ((p 2 + h) S + s) B + b], p the page holding the row's last
+ * column.  y[b, n] equals, bit for bit, what boost_decode_gemv returns
+ * (fp32): for a row on one page, slices[s][b][n] added over s = 0..S-1 in
+ * that order to 0.0f; for a cut row, the parts h = 0 so added, plus the parts
+ * h = 1 so added.  S == 1 means slices[0] is y itself (cut rows included).
+ * S is chosen as boost_decode_gemv chooses it, halved until it is at most
  * max_slices; it depends only on the shapes, the placement and the context,
- * so it is known on the host when the call returns.  Only for tensors whose
- * rows never cross a 2 MiB page (K divides 2^20; EINVAL otherwise), whose
- * partials have no second part.  1 <= max_slices <= BOOST_MAX_GEMV_SLICES.
- * Other arguments and errors as boost_decode_gemv. */
+ * so it is known on the host when the call returns.
+ * 1 <= max_slices <= BOOST_MAX_GEMV_SLICES.  Other arguments and errors as
+ * boost_decode_gemv. */
 #define BOOST_MAX_GEMV_SLICES 8
 int boost_decode_gemv_slices(boost_ctx *ctx, const boost_tensor *W, int N, int K,
                              const void *x, int B, float *slices, int max_slices,
                              int *n_slices, void *stream);
+
+/* Floats a slice buffer of boost_decode_gemv_slices needs for an [N, K]
+ * matrix at batch B and up to max_slices slices (host-only arithmetic).
+ * Errors: EINVAL (null output, a size below 1). */
+int boost_gemv_slices_floats(int N, int K, int B, int max_slices, uint64_t *floats);
 
 /* ------------------------------------------- a2/a3: KV pool and allocator */
 
@@ -510,10 +520,11 @@ int boost_add_rmsnorm(boost_ctx *ctx, float *x, const float *r, const void *w, i
                       int d, float eps, void *out, void *stream);
 
 /* boost_add_rmsnorm with r handed over as the S split-K slices of
- * boost_decode_gemv_slices (fp32 [S][B][d], 16-byte aligned): r is their
- * slice-order sum, so x and out get the same bits as boost_decode_gemv
- * followed by boost_add_rmsnorm.  1 <= S <= BOOST_MAX_GEMV_SLICES. */
-int boost_add_rmsnorm_slices(boost_ctx *ctx, float *x, const float *r, int S,
+ * boost_decode_gemv_slices for a [d, K] matrix (the layout documented there,
+ * 16-byte aligned): r is their sum in the order given there, so x and out get
+ * the same bits as boost_decode_gemv followed by boost_add_rmsnorm.
+ * 1 <= S <= BOOST_MAX_GEMV_SLICES, K >= 1 (the producing matrix's). */
+int boost_add_rmsnorm_slices(boost_ctx *ctx, float *x, const float *r, int S, int K,
                              const void *w, int B, int d, float eps, void *out,
                              void *stream);
 
@@ -544,12 +555,13 @@ int boost_rope_kv_append(boost_ctx *ctx, const boost_kv_pool *pool, int layer,
                          void *q, void *stream);
 
 /* boost_rope_kv_append with qkv handed over as the S split-K slices of
- * boost_decode_gemv_slices (fp32 [S][B][(Hq + 2H) D]): every element is their
- * slice-order sum, so q and the pool get the same bits as boost_decode_gemv
- * followed by boost_rope_kv_append.  1 <= S <= BOOST_MAX_GEMV_SLICES. */
+ * boost_decode_gemv_slices for a [(Hq + 2H) D, K] matrix (the layout
+ * documented there): every element is their sum in the order given there, so
+ * q and the pool get the same bits as boost_decode_gemv followed by
+ * boost_rope_kv_append.  1 <= S <= BOOST_MAX_GEMV_SLICES, K >= 1. */
 int boost_rope_kv_append_slices(boost_ctx *ctx, const boost_kv_pool *pool, int layer,
-                                const float *qkv, int S, const int32_t *positions, int B,
-                                int Hq, double theta, const int32_t *block_tables,
+                                const float *qkv, int S, int K, const int32_t *positions,
+                                int B, int Hq, double theta, const int32_t *block_tables,
                                 int max_blocks, void *q, void *stream);
 
 /* out[b, j] = bf16(silu(gu[b, j]) * gu[b, F + j]) for the fused gate_up

@@ -88,15 +88,15 @@ _SIGS = {
     "boost_embed_gather": (_i32, [_vp, _vp, _i32, _i32, _vp, _i32, _vp, _vp]),
     "boost_rmsnorm": (_i32, [_vp, _vp, _vp, _i32, _i32, C.c_float, _vp, _vp]),
     "boost_add_rmsnorm": (_i32, [_vp, _vp, _vp, _vp, _i32, _i32, C.c_float, _vp, _vp]),
-    "boost_add_rmsnorm_slices": (_i32, [_vp, _vp, _vp, _i32, _vp, _i32, _i32, C.c_float, _vp,
-                                        _vp]),
+    "boost_add_rmsnorm_slices": (_i32, [_vp, _vp, _vp, _i32, _i32, _vp, _i32, _i32, C.c_float,
+                                        _vp, _vp]),
     "boost_rope_qkv": (_i32, [_vp, _vp, _vp, _i32, _i32, _i32, _i32, _dbl, _vp, _vp,
                               _vp, _vp]),
     "boost_kv_append": (_i32, [_vp, _vp, _i32, _vp, _i32, _vp, _vp, _vp, _i32, _vp]),
     "boost_rope_kv_append": (_i32, [_vp, _vp, _i32, _vp, _vp, _i32, _i32, _dbl, _vp, _i32,
                                     _vp, _vp]),
-    "boost_rope_kv_append_slices": (_i32, [_vp, _vp, _i32, _vp, _i32, _vp, _i32, _i32, _dbl,
-                                           _vp, _i32, _vp, _vp]),
+    "boost_rope_kv_append_slices": (_i32, [_vp, _vp, _i32, _vp, _i32, _i32, _vp, _i32, _i32,
+                                           _dbl, _vp, _i32, _vp, _vp]),
     "boost_silu_mul": (_i32, [_vp, _vp, _i32, _i32, _vp, _vp]),
     "boost_residual_add": (_i32, [_vp, _vp, _vp, C.c_int64, _vp]),
     "boost_argmax": (_i32, [_vp, _vp, _i32, _i32, _vp, _vp]),
@@ -118,6 +118,7 @@ _SIGS = {
     "boost_decode_gemv": (_i32, [_vp, _vp, _i32, _i32, _vp, _i32, _vp, _i32, _vp]),
     "boost_decode_gemv_slices": (_i32, [_vp, _vp, _i32, _i32, _vp, _i32, _vp, _i32,
                                         C.POINTER(_i32), _vp]),
+    "boost_gemv_slices_floats": (_i32, [_i32, _i32, _i32, _i32, C.POINTER(_u64)]),
 }
 
 _lib = None
@@ -373,9 +374,16 @@ def boost_decode_gemv(ctx: int, W: int, N: int, K: int, x, B: int, y,
 MAX_GEMV_SLICES = 8
 
 
+def boost_gemv_slices_floats(N: int, K: int, B: int, max_slices: int) -> int:
+    n = _u64(0)
+    _check(load().boost_gemv_slices_floats(N, K, B, max_slices, C.byref(n)))
+    return n.value
+
+
 def boost_decode_gemv_slices(ctx: int, W: int, N: int, K: int, x, B: int, slices,
                              max_slices: int, stream=None) -> int:
-    """Writes the split-K partial slices fp32 [S][B][N] and returns S."""
+    """Writes the split-K partial slices (fp32 [S][B][N], then the parts of
+    rows that cross a page) and returns S."""
     n = C.c_int32(0)
     _check(load().boost_decode_gemv_slices(ctx, W, N, K, _ptr(x), B, _ptr(slices), max_slices,
                                            C.byref(n), _stream(stream)))
@@ -476,9 +484,9 @@ def boost_add_rmsnorm(ctx: int, x, r, w, B: int, d: int, eps: float, out, stream
                                     _stream(stream)))
 
 
-def boost_add_rmsnorm_slices(ctx: int, x, r, S: int, w, B: int, d: int, eps: float, out,
-                             stream=None):
-    _check(load().boost_add_rmsnorm_slices(ctx, _ptr(x), _ptr(r), S, _ptr(w), B, d, eps,
+def boost_add_rmsnorm_slices(ctx: int, x, r, S: int, K: int, w, B: int, d: int, eps: float,
+                             out, stream=None):
+    _check(load().boost_add_rmsnorm_slices(ctx, _ptr(x), _ptr(r), S, K, _ptr(w), B, d, eps,
                                            _ptr(out), _stream(stream)))
 
 
@@ -501,12 +509,12 @@ def boost_rope_kv_append(ctx: int, pool: int, layer: int, qkv, positions, B: int
                                        _stream(stream)))
 
 
-def boost_rope_kv_append_slices(ctx: int, pool: int, layer: int, qkv, S: int, positions,
-                                B: int, Hq: int, theta: float, block_tables, max_blocks: int,
-                                q, stream=None):
-    _check(load().boost_rope_kv_append_slices(ctx, pool, layer, _ptr(qkv), S, _ptr(positions),
-                                              B, Hq, theta, _ptr(block_tables), max_blocks,
-                                              _ptr(q), _stream(stream)))
+def boost_rope_kv_append_slices(ctx: int, pool: int, layer: int, qkv, S: int, K: int,
+                                positions, B: int, Hq: int, theta: float, block_tables,
+                                max_blocks: int, q, stream=None):
+    _check(load().boost_rope_kv_append_slices(ctx, pool, layer, _ptr(qkv), S, K,
+                                              _ptr(positions), B, Hq, theta, _ptr(block_tables),
+                                              max_blocks, _ptr(q), _stream(stream)))
 
 
 def boost_silu_mul(ctx: int, gu, B: int, F: int, out, stream=None):

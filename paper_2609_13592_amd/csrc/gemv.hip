@@ -1072,13 +1072,11 @@ int64_t plan_grid(GemvParams& P, int n_pages, int rows_wg, const boost_ctx* ctx,
   return grid > 0x7fffffff ? -1 : grid;
 }
 
-// Largest S (halving from `want`) whose partials fit: the context's
-// workspace ([S][B][N] plus the cut rows' parts), or the caller's slice
-// buffer ([S][B][N]; a tensor without cut rows).
+// Largest S (halving from `want`) whose partials ([S][B][N] plus the cut
+// rows' parts) fit the context's workspace or the caller's slice buffer.
 int fit_slices(const GemvParams& P, int n_pages, int want, const boost_ctx* ctx) {
   int S = want;
-  const uint64_t per = P.slices ? static_cast<uint64_t>(P.B) * P.N
-                                : static_cast<uint64_t>(P.B) * (P.N + 2ull * (n_pages + 1));
+  const uint64_t per = static_cast<uint64_t>(P.B) * (P.N + 2ull * (n_pages + 1));
   const uint64_t cap = P.slices ? static_cast<uint64_t>(P.slice_floats) : ctx->gemm_ws_floats;
   while (S > 1 && S * per > cap) S /= 2;
   return S;
@@ -1385,21 +1383,28 @@ int boost_decode_gemv(boost_ctx* ctx, const boost_tensor* W, int N, int K, const
   return decode_gemv(ctx, W, N, K, x, B, y, y_dtype, nullptr, 0, nullptr, stream);
 }
 
+int boost_gemv_slices_floats(int N, int K, int B, int max_slices, uint64_t* floats) {
+  if (!floats) return fail(BOOST_EINVAL, "null argument");
+  if (N < 1 || K < 1 || B < 1 || max_slices < 1)
+    return fail(BOOST_EINVAL, "N=%d K=%d B=%d max_slices=%d", N, K, B, max_slices);
+  const uint64_t pages = (static_cast<uint64_t>(N) * K + kPageElems - 1) / kPageElems;
+  *floats = static_cast<uint64_t>(max_slices) * B * (N + 2 * (pages + 1));
+  return BOOST_OK;
+}
+
 int boost_decode_gemv_slices(boost_ctx* ctx, const boost_tensor* W, int N, int K,
                              const void* x, int B, float* slices, int max_slices,
                              int* n_slices, void* stream) {
   if (!slices || !n_slices) return fail(BOOST_EINVAL, "null argument");
   if (max_slices < 1 || max_slices > BOOST_MAX_GEMV_SLICES)
     return fail(BOOST_EINVAL, "max_slices %d outside [1, %d]", max_slices, BOOST_MAX_GEMV_SLICES);
-  if (K < 1 || kPageElems % K != 0)
-    return fail(BOOST_EINVAL, "K=%d: rows cross page boundaries (K must divide %lld)", K,
-                static_cast<long long>(kPageElems));
   if (reinterpret_cast<uintptr_t>(slices) & 15)
     return fail(BOOST_EINVAL, "slices must be 16-byte aligned");
+  uint64_t cap = 0;
+  if (int rc = boost_gemv_slices_floats(N, K, B, max_slices, &cap)) return rc;
   *n_slices = 0;
-  const int64_t cap = static_cast<int64_t>(max_slices) * B * N;
-  return decode_gemv(ctx, W, N, K, x, B, slices, BOOST_DTYPE_F32, slices, cap, n_slices,
-                     stream);
+  return decode_gemv(ctx, W, N, K, x, B, slices, BOOST_DTYPE_F32, slices,
+                     static_cast<int64_t>(cap), n_slices, stream);
 }
 
 }  // extern "C"

@@ -21,23 +21,60 @@ __device__ __forceinline__ uint16_t to_bf16(float f) {
   return static_cast<uint16_t>(u >> 16);
 }
 
-// Element i of a split-K GEMV output handed over as its S partial slices
-// (slice stride `stride` floats): the slices summed in slice order from zero,
-// the additions the GEMV's own reduction kernel makes, so a consumer that
-// takes the slices sees the same bits as one that takes the reduced output.
-// S == 1 is the unsplit output itself.
-// All S loads go out together (a loop over a run-time S would wait for
-// each in turn), then the sums in slice order.
-__device__ __forceinline__ float slice_sum(const float* p, int S, int64_t stride, int64_t i) {
-  if (S == 1) return p[i];
-  float part[BOOST_MAX_GEMV_SLICES];
+// A split-K GEMV output handed over as its S partial slices: [S][B][N]
+// fp32, then, for the rows that cross a 2 MiB page of the [N, K] matrix, the
+// two parts of each such row ([page of the row's end][part][S][B]).  S == 1
+// is the unsplit output itself.
+struct Slices {
+  const float* p;
+  int S, B;
+  int64_t N, K;
+};
+
+constexpr int64_t kPageElems = static_cast<int64_t>(bst::kPage / 2);
+
+// Whether row r of the [N, K] bf16 matrix crosses a page boundary (K = 0:
+// never, the caller having found that K divides a page).
+__device__ __forceinline__ bool cut_row(int64_t r, int64_t K) {
+  return (r * K) / kPageElems != (r * K + K - 1) / kPageElems;
+}
+
+// Element (b, r) of the output: the slices summed in slice order from zero,
+// and a cut row's earlier part then its later part, the additions the
+// GEMV's own reduction kernel makes, so a consumer that takes the slices
+// sees the same bits as one that takes the reduced output.  All loads go out
+// before the sums (a loop over a run-time S would wait for each in turn).
+__device__ __forceinline__ float slice_value(const Slices& sl, int b, int64_t r) {
+  const int64_t i = static_cast<int64_t>(b) * sl.N + r;
+  if (sl.S == 1) return sl.p[i];
+  const int64_t stride = static_cast<int64_t>(sl.B) * sl.N;
+  if (!cut_row(r, sl.K)) {
+    float part[BOOST_MAX_GEMV_SLICES];
 #pragma unroll
-  for (int s = 0; s < BOOST_MAX_GEMV_SLICES; ++s) part[s] = s < S ? p[s * stride + i] : 0.f;
-  float v = 0.f;
+    for (int s = 0; s < BOOST_MAX_GEMV_SLICES; ++s)
+      part[s] = s < sl.S ? sl.p[s * stride + i] : 0.f;
+    float v = 0.f;
+#pragma unroll
+    for (int s = 0; s < BOOST_MAX_GEMV_SLICES; ++s)
+      if (s < sl.S) v += part[s];
+    return v;
+  }
+  const int64_t p1 = (r * sl.K + sl.K - 1) / kPageElems;
+  const float* cut = sl.p + sl.S * stride;
+  float part0[BOOST_MAX_GEMV_SLICES], part1[BOOST_MAX_GEMV_SLICES];
+#pragma unroll
+  for (int s = 0; s < BOOST_MAX_GEMV_SLICES; ++s) {
+    part0[s] = s < sl.S ? cut[((p1 * 2 + 0) * sl.S + s) * sl.B + b] : 0.f;
+    part1[s] = s < sl.S ? cut[((p1 * 2 + 1) * sl.S + s) * sl.B + b] : 0.f;
+  }
+  float v = 0.f, v1 = 0.f;
 #pragma unroll
   for (int s = 0; s < BOOST_MAX_GEMV_SLICES; ++s)
-    if (s < S) v += part[s];
-  return v;
+    if (s < sl.S) {
+      v += part0[s];
+      v1 += part1[s];
+    }
+  return v + v1;
 }
 
 // One lane per 8 elements of one row; the row of token t is read through the
@@ -66,12 +103,10 @@ __global__ __launch_bounds__(256) void embed_gather_kernel(const char* const* __
 // One workgroup per row: sum of squares in a fixed order, then
 // y = bf16(x * (1 / sqrt(mean + eps)) * w).  With ADD the row first takes
 // the residual r (x += r in fp32, stored back), the same additions the
-// separate residual add makes, so the fused call gives the same bits; r may
-// come as S split-K slices of stride rs floats (see slice_sum).
+// separate residual add makes, so the fused call gives the same bits; the
+// residual may come as split-K slices (see slice_value; rs.p is r).
 template <bool ADD>
-__global__ __launch_bounds__(256) void rmsnorm_kernel(float* __restrict__ x,
-                                                      const float* __restrict__ r, int S,
-                                                      int64_t rs,
+__global__ __launch_bounds__(256) void rmsnorm_kernel(float* __restrict__ x, Slices rs,
                                                       const uint16_t* __restrict__ w, int d,
                                                       float eps, uint16_t* __restrict__ y) {
   __shared__ float part[4];
@@ -80,7 +115,7 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(float* __restrict__ x,
   for (int i = threadIdx.x; i < d; i += 256) {
     float v = row[i];
     if constexpr (ADD) {
-      v += slice_sum(r, S, rs, static_cast<int64_t>(blockIdx.x) * d + i);
+      v += slice_value(rs, blockIdx.x, i);
       row[i] = v;  // read back below by this same lane
     }
     s = fmaf(v, v, s);
@@ -97,55 +132,69 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(float* __restrict__ x,
 }
 
 // The same for rows of d <= 8192 floats with d % 4 == 0 and 16-byte aligned
-// rows: each lane loads its (at most 8) float4s of the row at once and keeps
-// them in registers for the second pass (the plain loop above is a chain of
+// rows: each lane loads its (at most NV = 4 or 8) float4s of the row at once
+// and keeps them in registers for the second pass (the plain loop above is a chain of
 // dependent round trips: 20 us for a batch of 8 rows of 8192).
 constexpr int kNormVec = 8;
-template <bool ADD>
-__global__ __launch_bounds__(256) void rmsnorm_vec_kernel(float* __restrict__ x,
-                                                          const float* __restrict__ r, int S,
-                                                          int64_t rs,
+// Pages of the producing [d, K] matrix (at most d, since K <= 2^20 elements
+// and d <= 8192 here): a workgroup of the vector norm sums each cut row once
+// into LDS, indexed by the page of the row's last column.
+constexpr int kMaxCutPages = 4 * 256 * kNormVec;
+template <bool ADD, int NV>
+__global__ __launch_bounds__(256) void rmsnorm_vec_kernel(float* __restrict__ x, Slices rs,
                                                           const uint16_t* __restrict__ w,
                                                           int d, float eps,
                                                           uint16_t* __restrict__ y) {
   __shared__ float part[4];
   const int n4 = d / 4;
   float4* row = reinterpret_cast<float4*>(x + static_cast<int64_t>(blockIdx.x) * d);
-  float4 v[kNormVec];
+  float4 v[NV];
 #pragma unroll
-  for (int u = 0; u < kNormVec; ++u) {
+  for (int u = 0; u < NV; ++u) {
     const int i = threadIdx.x + u * 256;
     v[u] = i < n4 ? row[i] : make_float4(0.f, 0.f, 0.f, 0.f);
   }
   if constexpr (ADD) {
-    // the residual, or the slice-order sum of its S slices (see slice_sum),
-    // taken in groups of four slices whose loads of the whole row go out
-    // before the group's additions (uniform guards, no waits between)
-    float4 a[kNormVec];
-    const float* r0 = r + static_cast<int64_t>(blockIdx.x) * d;
+    // the residual, or the slice-order sum of its S slices (see
+    // slice_value), taken in groups of four slices whose loads of the whole
+    // row go out before the group's additions (uniform guards, no waits
+    // between).  A row of the producing matrix that crosses a page takes
+    // its value from its two parts instead: one lane per page boundary sums
+    // them into LDS while the first group's loads are in flight.
+    __shared__ float cutv[kMaxCutPages];
+    const int S = rs.S;
+    const int64_t stride = static_cast<int64_t>(rs.B) * d;
+    float4 a[NV];
+    const float* r0 = rs.p + static_cast<int64_t>(blockIdx.x) * d;
     if (S == 1) {
 #pragma unroll
-      for (int u = 0; u < kNormVec; ++u) {
+      for (int u = 0; u < NV; ++u) {
         const int i = threadIdx.x + u * 256;
         a[u] = i < n4 ? reinterpret_cast<const float4*>(r0)[i] : make_float4(0.f, 0.f, 0.f, 0.f);
       }
     } else {
       const int nu = (n4 + 255) / 256;
+      const int64_t pages = (static_cast<int64_t>(d) * rs.K + kPageElems - 1) / kPageElems;
 #pragma unroll
-      for (int u = 0; u < kNormVec; ++u) a[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+      for (int u = 0; u < NV; ++u) a[u] = make_float4(0.f, 0.f, 0.f, 0.f);
       for (int s0 = 0; s0 < S; s0 += 4) {
-        float4 t[kNormVec][4];
+        float4 t[NV][4];
 #pragma unroll
-        for (int u = 0; u < kNormVec; ++u)
+        for (int u = 0; u < NV; ++u)
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
             const int i = threadIdx.x + u * 256;
             t[u][j] = u < nu && s0 + j < S && i < n4
-                          ? reinterpret_cast<const float4*>(r0 + (s0 + j) * rs)[i]
+                          ? reinterpret_cast<const float4*>(r0 + (s0 + j) * stride)[i]
                           : make_float4(0.f, 0.f, 0.f, 0.f);
           }
+        if (s0 == 0)
+          for (int q = threadIdx.x + 1; q < pages; q += 256) {
+            const int64_t e = static_cast<int64_t>(q) * kPageElems;
+            if (e % rs.K != 0) cutv[q] = slice_value(rs, blockIdx.x, e / rs.K);
+          }
 #pragma unroll
-        for (int u = 0; u < kNormVec; ++u)
+        for (int u = 0; u < NV; ++u)
 #pragma unroll
           for (int j = 0; j < 4; ++j)
             if (s0 + j < S) {
@@ -155,9 +204,22 @@ __global__ __launch_bounds__(256) void rmsnorm_vec_kernel(float* __restrict__ x,
               a[u].w += t[u][j].w;
             }
       }
+      __syncthreads();  // cutv
+      auto cut_value = [&](int64_t e) { return cutv[(e * rs.K + rs.K - 1) / kPageElems]; };
+#pragma unroll
+      for (int u = 0; u < NV; ++u) {
+        const int i = threadIdx.x + u * 256;
+        if (u < nu && i < n4) {
+          const int64_t e = 4 * static_cast<int64_t>(i);
+          if (cut_row(e, rs.K)) a[u].x = cut_value(e);
+          if (cut_row(e + 1, rs.K)) a[u].y = cut_value(e + 1);
+          if (cut_row(e + 2, rs.K)) a[u].z = cut_value(e + 2);
+          if (cut_row(e + 3, rs.K)) a[u].w = cut_value(e + 3);
+        }
+      }
     }
 #pragma unroll
-    for (int u = 0; u < kNormVec; ++u) {
+    for (int u = 0; u < NV; ++u) {
       const int i = threadIdx.x + u * 256;
       if (i < n4) {
         v[u].x += a[u].x;
@@ -170,7 +232,7 @@ __global__ __launch_bounds__(256) void rmsnorm_vec_kernel(float* __restrict__ x,
   }
   float s = 0.f;
 #pragma unroll
-  for (int u = 0; u < kNormVec; ++u) {
+  for (int u = 0; u < NV; ++u) {
     s = fmaf(v[u].x, v[u].x, s);
     s = fmaf(v[u].y, v[u].y, s);
     s = fmaf(v[u].z, v[u].z, s);
@@ -185,7 +247,7 @@ __global__ __launch_bounds__(256) void rmsnorm_vec_kernel(float* __restrict__ x,
   const uint2* w4 = reinterpret_cast<const uint2*>(w);
   uint2* out = reinterpret_cast<uint2*>(y + static_cast<int64_t>(blockIdx.x) * d);
 #pragma unroll
-  for (int u = 0; u < kNormVec; ++u) {
+  for (int u = 0; u < NV; ++u) {
     const int i = threadIdx.x + u * 256;
     if (i >= n4) break;
     const uint2 ww = w4[i];
@@ -208,30 +270,29 @@ struct PoolSlot {
   int max_blocks, T, nb;
 };
 
-// One workgroup per (request, head of the fused qkv output), one lane per
-// rotation pair.  Query and key heads are rotated (half-split pairs, angle in
+// One wavefront per (request, head of the fused qkv output), four to a
+// workgroup, one lane per rotation pair.  Query and key heads are rotated (half-split pairs, angle in
 // double precision); value heads are converted.  With POOL the key and value
 // heads go to the token's slot of the pool (the same bits the KV append
 // copies there), skipped like the append skips a position or block outside
-// the table or the pool.  qkv may come as S split-K slices of stride qs
-// floats (see slice_sum).
+// the table or the pool.  qkv may come as split-K slices (see slice_value).
+constexpr int kRopeWaves = 4;
 template <bool POOL>
-__global__ __launch_bounds__(64) void rope_qkv_kernel(const float* __restrict__ qkv, int S,
-                                                      int64_t qs,
-                                                      const int32_t* __restrict__ pos,
-                                                      int Hq, int H, int D, double log2_theta,
-                                                      uint16_t* __restrict__ q,
-                                                      uint16_t* __restrict__ k,
-                                                      uint16_t* __restrict__ v, PoolSlot ps) {
+__global__ __launch_bounds__(64 * kRopeWaves) void rope_qkv_kernel(
+    Slices qkv, const int32_t* __restrict__ pos, int Hq, int H, int D, double log2_theta,
+    uint16_t* __restrict__ q, uint16_t* __restrict__ k, uint16_t* __restrict__ v, PoolSlot ps) {
   const int heads = Hq + 2 * H;
-  const int b = blockIdx.x / heads, h = blockIdx.x % heads;
+  const int item = blockIdx.x * kRopeWaves + static_cast<int>(threadIdx.x >> 6);
+  if (item >= qkv.B * heads) return;  // uniform over the wavefront; no barrier follows
+  const int b = item / heads, h = item % heads;
+  const int lane = threadIdx.x & 63;
   const int half = D / 2;
-  const float* src = qkv + (static_cast<int64_t>(b) * heads + h) * D;
+  const int64_t col0 = static_cast<int64_t>(h) * D;  // this head's first column
   uint16_t* dst;
   if (h < Hq) {
     dst = q + (static_cast<int64_t>(b) * Hq + h) * D;
   } else if constexpr (POOL) {
-    const int p = pos[b];  // uniform over the workgroup
+    const int p = pos[b];  // uniform over the wavefront
     if (p < 0 || p >= ps.max_blocks * ps.T) return;
     const int32_t blk = ps.tables[static_cast<int64_t>(b) * ps.max_blocks + p / ps.T];
     if (blk < 0 || blk >= ps.nb) return;
@@ -246,8 +307,8 @@ __global__ __launch_bounds__(64) void rope_qkv_kernel(const float* __restrict__ 
   } else {
     dst = v + (static_cast<int64_t>(b) * H + (h - Hq - H)) * D;
   }
-  for (int i = threadIdx.x; i < half; i += blockDim.x) {
-    const float a = slice_sum(src, S, qs, i), c = slice_sum(src, S, qs, i + half);
+  for (int i = lane; i < half; i += 64) {
+    const float a = slice_value(qkv, b, col0 + i), c = slice_value(qkv, b, col0 + i + half);
     if (h >= Hq + H) {
       dst[i] = to_bf16(a);
       dst[i + half] = to_bf16(c);
@@ -388,8 +449,8 @@ int boost_embed_gather(boost_ctx* ctx, const boost_tensor* E, int V, int d,
 namespace {
 // x (+= r when r is given), then the norm; the row layout decides the
 // kernel, never r, so the fused and the separate calls take the same one
-int launch_rmsnorm(boost_ctx* ctx, float* x, const float* r, int S, const void* w, int B,
-                   int d, float eps, void* out, void* stream) {
+int launch_rmsnorm(boost_ctx* ctx, float* x, const float* r, int S, int K, const void* w,
+                   int B, int d, float eps, void* out, void* stream) {
   if (!ctx || !x || !w || !out) return fail(BOOST_EINVAL, "null argument");
   if (ctx->device < 0) return fail(BOOST_ENODEV, "plan-only context");
   if (B < 1 || d < 1 || !(eps >= 0.f)) return fail(BOOST_EINVAL, "B=%d d=%d eps=%g", B, d, eps);
@@ -401,19 +462,25 @@ int launch_rmsnorm(boost_ctx* ctx, float* x, const float* r, int S, const void* 
   auto s = static_cast<hipStream_t>(stream);
   auto wp = static_cast<const uint16_t*>(w);
   auto op = static_cast<uint16_t*>(out);
-  const int64_t rs = static_cast<int64_t>(B) * d;
-  if (vec && r)
-    hipLaunchKernelGGL(rmsnorm_vec_kernel<true>, dim3(B), dim3(256), 0, s, x, r, S, rs, wp, d,
-                       eps, op);
+  // K = 0: no row of the producing matrix crosses a page
+  const Slices rs{r, S, B, d, kPageElems % K ? K : 0};
+  const bool nv4 = d <= 4 * 256 * 4;  // four float4s per lane cover the row
+  if (vec && r && nv4)
+    hipLaunchKernelGGL((rmsnorm_vec_kernel<true, 4>), dim3(B), dim3(256), 0, s, x, rs, wp, d, eps,
+                       op);
+  else if (vec && r)
+    hipLaunchKernelGGL((rmsnorm_vec_kernel<true, kNormVec>), dim3(B), dim3(256), 0, s, x, rs, wp,
+                       d, eps, op);
+  else if (vec && nv4)
+    hipLaunchKernelGGL((rmsnorm_vec_kernel<false, 4>), dim3(B), dim3(256), 0, s, x, rs, wp, d, eps,
+                       op);
   else if (vec)
-    hipLaunchKernelGGL(rmsnorm_vec_kernel<false>, dim3(B), dim3(256), 0, s, x, r, S, rs, wp, d,
-                       eps, op);
+    hipLaunchKernelGGL((rmsnorm_vec_kernel<false, kNormVec>), dim3(B), dim3(256), 0, s, x, rs, wp,
+                       d, eps, op);
   else if (r)
-    hipLaunchKernelGGL(rmsnorm_kernel<true>, dim3(B), dim3(256), 0, s, x, r, S, rs, wp, d, eps,
-                       op);
+    hipLaunchKernelGGL(rmsnorm_kernel<true>, dim3(B), dim3(256), 0, s, x, rs, wp, d, eps, op);
   else
-    hipLaunchKernelGGL(rmsnorm_kernel<false>, dim3(B), dim3(256), 0, s, x, r, S, rs, wp, d, eps,
-                       op);
+    hipLaunchKernelGGL(rmsnorm_kernel<false>, dim3(B), dim3(256), 0, s, x, rs, wp, d, eps, op);
   BOOST_HIP(hipGetLastError());
   return BOOST_OK;
 }
@@ -424,23 +491,23 @@ extern "C" {
 int boost_rmsnorm(boost_ctx* ctx, const float* x, const void* w, int B, int d, float eps,
                   void* out, void* stream) {
   // the kernel without the residual never writes x
-  return launch_rmsnorm(ctx, const_cast<float*>(x), nullptr, 1, w, B, d, eps, out, stream);
+  return launch_rmsnorm(ctx, const_cast<float*>(x), nullptr, 1, 1, w, B, d, eps, out, stream);
 }
 
 int boost_add_rmsnorm(boost_ctx* ctx, float* x, const float* r, const void* w, int B, int d,
                       float eps, void* out, void* stream) {
   if (!r) return fail(BOOST_EINVAL, "null argument");
   if (reinterpret_cast<uintptr_t>(r) & 15) return fail(BOOST_EINVAL, "r must be 16-byte aligned");
-  return launch_rmsnorm(ctx, x, r, 1, w, B, d, eps, out, stream);
+  return launch_rmsnorm(ctx, x, r, 1, 1, w, B, d, eps, out, stream);
 }
 
-int boost_add_rmsnorm_slices(boost_ctx* ctx, float* x, const float* r, int S, const void* w,
-                             int B, int d, float eps, void* out, void* stream) {
+int boost_add_rmsnorm_slices(boost_ctx* ctx, float* x, const float* r, int S, int K,
+                             const void* w, int B, int d, float eps, void* out, void* stream) {
   if (!r) return fail(BOOST_EINVAL, "null argument");
   if (reinterpret_cast<uintptr_t>(r) & 15) return fail(BOOST_EINVAL, "r must be 16-byte aligned");
-  if (S < 1 || S > BOOST_MAX_GEMV_SLICES)
-    return fail(BOOST_EINVAL, "S=%d outside [1, %d]", S, BOOST_MAX_GEMV_SLICES);
-  return launch_rmsnorm(ctx, x, r, S, w, B, d, eps, out, stream);
+  if (S < 1 || S > BOOST_MAX_GEMV_SLICES || K < 1 || K > kPageElems)
+    return fail(BOOST_EINVAL, "S=%d (1..%d) K=%d (1..2^20)", S, BOOST_MAX_GEMV_SLICES, K);
+  return launch_rmsnorm(ctx, x, r, S, K, w, B, d, eps, out, stream);
 }
 
 int boost_rope_qkv(boost_ctx* ctx, const float* qkv, const int32_t* positions, int B, int Hq,
@@ -449,9 +516,11 @@ int boost_rope_qkv(boost_ctx* ctx, const float* qkv, const int32_t* positions, i
   if (ctx->device < 0) return fail(BOOST_ENODEV, "plan-only context");
   if (B < 1 || Hq < 1 || H < 1 || D < 2 || D % 2 || !(theta > 1.0))
     return fail(BOOST_EINVAL, "B=%d Hq=%d H=%d D=%d theta=%g", B, Hq, H, D, theta);
-  hipLaunchKernelGGL(rope_qkv_kernel<false>, dim3(B * (Hq + 2 * H)), dim3(64), 0,
-                     static_cast<hipStream_t>(stream), qkv, 1, int64_t{0}, positions, Hq, H, D,
-                     std::log2(theta),
+  const Slices sl{qkv, 1, B, static_cast<int64_t>(Hq + 2 * H) * D, 1};
+  hipLaunchKernelGGL(rope_qkv_kernel<false>,
+                     dim3((B * (Hq + 2 * H) + kRopeWaves - 1) / kRopeWaves),
+                     dim3(64 * kRopeWaves), 0,
+                     static_cast<hipStream_t>(stream), sl, positions, Hq, H, D, std::log2(theta),
                      static_cast<uint16_t*>(q), static_cast<uint16_t*>(k),
                      static_cast<uint16_t*>(v), PoolSlot{});
   BOOST_HIP(hipGetLastError());
@@ -461,13 +530,13 @@ int boost_rope_qkv(boost_ctx* ctx, const float* qkv, const int32_t* positions, i
 int boost_rope_kv_append(boost_ctx* ctx, const boost_kv_pool* p, int layer, const float* qkv,
                          const int32_t* positions, int B, int Hq, double theta,
                          const int32_t* block_tables, int max_blocks, void* q, void* stream) {
-  return boost_rope_kv_append_slices(ctx, p, layer, qkv, 1, positions, B, Hq, theta,
+  return boost_rope_kv_append_slices(ctx, p, layer, qkv, 1, 1, positions, B, Hq, theta,
                                      block_tables, max_blocks, q, stream);
 }
 
 int boost_rope_kv_append_slices(boost_ctx* ctx, const boost_kv_pool* p, int layer,
-                                const float* qkv, int S, const int32_t* positions, int B,
-                                int Hq, double theta, const int32_t* block_tables,
+                                const float* qkv, int S, int K, const int32_t* positions,
+                                int B, int Hq, double theta, const int32_t* block_tables,
                                 int max_blocks, void* q, void* stream) {
   if (!ctx || !p || !qkv || !positions || !block_tables || !q)
     return fail(BOOST_EINVAL, "null argument");
@@ -478,16 +547,18 @@ int boost_rope_kv_append_slices(boost_ctx* ctx, const boost_kv_pool* p, int laye
   if (B < 1 || max_blocks < 1 || Hq < 1 || !(theta > 1.0) || kPage % (2ull * D) != 0)
     return fail(BOOST_EINVAL, "B=%d max_blocks=%d Hq=%d theta=%g D=%d", B, max_blocks, Hq,
                 theta, D);
-  if (S < 1 || S > BOOST_MAX_GEMV_SLICES)
-    return fail(BOOST_EINVAL, "S=%d outside [1, %d]", S, BOOST_MAX_GEMV_SLICES);
+  if (S < 1 || S > BOOST_MAX_GEMV_SLICES || K < 1 || K > kPageElems)
+    return fail(BOOST_EINVAL, "S=%d (1..%d) K=%d (1..2^20)", S, BOOST_MAX_GEMV_SLICES, K);
   const uint64_t P = p->geom.pages;
   const PoolSlot ps{p->d_page_table + 2ull * layer * P, p->d_page_table + (2ull * layer + 1) * P,
                     block_tables, max_blocks, static_cast<int>(p->cfg.block_tokens),
                     static_cast<int>(p->geom.nb)};
-  const int64_t qs = static_cast<int64_t>(B) * (Hq + 2 * H) * D;
-  hipLaunchKernelGGL(rope_qkv_kernel<true>, dim3(B * (Hq + 2 * H)), dim3(64), 0,
-                     static_cast<hipStream_t>(stream), qkv, S, qs, positions, Hq, H, D,
-                     std::log2(theta),
+  // K = 0: no row of the producing matrix crosses a page
+  const Slices sl{qkv, S, B, static_cast<int64_t>(Hq + 2 * H) * D, kPageElems % K ? K : 0};
+  hipLaunchKernelGGL(rope_qkv_kernel<true>,
+                     dim3((B * (Hq + 2 * H) + kRopeWaves - 1) / kRopeWaves),
+                     dim3(64 * kRopeWaves), 0,
+                     static_cast<hipStream_t>(stream), sl, positions, Hq, H, D, std::log2(theta),
                      static_cast<uint16_t*>(q), nullptr, nullptr, ps);
   BOOST_HIP(hipGetLastError());
   return BOOST_OK;

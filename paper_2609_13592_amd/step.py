@@ -11,11 +11,11 @@ This module only sequences C-ABI calls and owns the activation buffers
 where every "residual_add -> rmsnorm" pair is one add_rmsnorm launch (the
 down projection's residual is added by the next layer's first norm, or by
 the final norm) and "rope_qkv -> kv_append" is one rope_kv_append launch.
-Where the qkv and o projections split K over workgroups, their partial
-slices go straight to the RoPE + KV append and to the residual norm, which
-sum them in the order the GEMV's own reduction kernel does (the same bits,
-one launch fewer per projection); a matrix whose rows cross page boundaries
-(K not dividing 2^20) keeps the reduction kernel.
+Where the qkv, o and down projections split K over workgroups, their
+partial slices go straight to the RoPE + KV append and to the residual
+norms (down's to the next layer's first norm, or the final one), which sum
+them in the order the GEMV's own reduction kernel does: the same bits, one
+launch fewer per projection.
 
 Weights are [out, in] bf16 matrices placed page by page (each tensor on its
 own, so modulo placement restarts per tensor); norm weights are small bf16
@@ -54,8 +54,9 @@ class DecodeModel:
                  matrices: dict, norms: dict, fold_slices: bool = True):
         """matrices: name -> placed tensor handle for 'embed', 'lm_head' and
         '<kind>.<layer>'; norms: name -> device bf16 tensor for 'norm1.<l>',
-        'norm2.<l>', 'norm_f'.  fold_slices: hand the split-K slices of qkv
-        and o to their consumers (False: every projection reduces its own)."""
+        'norm2.<l>', 'norm_f'.  fold_slices: hand the split-K slices of qkv,
+        o and down to their consumers (False: every projection reduces its
+        own)."""
         import torch
         self.ctx, self.dims, self.B, self.mb, self.pool = ctx, dims, batch, max_blocks, pool
         self.mat, self.norms = matrices, norms
@@ -66,11 +67,17 @@ class DecodeModel:
         self.x = torch.zeros((B, D.d), dtype=f32, device=dev)
         self.h = torch.zeros((B, D.d), dtype=b16, device=dev)
         qkv_n = (D.hq + 2 * D.hkv) * D.hd
-        folds = lambda K: fold_slices and bd.PAGE_BYTES // 2 % K == 0
-        self.fold_qkv, self.fold_o = folds(D.d), folds(D.hq * D.hd)
-        S = bd.MAX_GEMV_SLICES
-        self.qkv = torch.zeros((S if self.fold_qkv else 1, B, qkv_n), dtype=f32, device=dev)
-        self.o_sl = torch.zeros((S, B, D.d), dtype=f32, device=dev) if self.fold_o else None
+        self.fold = fold_slices
+
+        def slices(N, K):
+            n = bd.boost_gemv_slices_floats(N, K, B, bd.MAX_GEMV_SLICES)
+            return torch.zeros((n,), dtype=f32, device=dev)
+        if fold_slices:
+            self.qkv = slices(qkv_n, D.d)
+            self.o_sl = slices(D.d, D.hq * D.hd)
+            self.down_sl = slices(D.d, D.ffn)
+        else:
+            self.qkv = torch.zeros((B, qkv_n), dtype=f32, device=dev)
         self.q = torch.zeros((B, D.hq, D.hd), dtype=b16, device=dev)
         self.o = torch.zeros((B, D.hq, D.hd), dtype=b16, device=dev)
         self.tmp = torch.zeros((B, D.d), dtype=f32, device=dev)
@@ -91,21 +98,26 @@ class DecodeModel:
         F32, BF16 = bd.DTYPE_F32, bd.DTYPE_BF16
         bd.boost_embed_gather(c, self.mat["embed"], D.vocab, D.d, tokens, B, self.x, s)
         qkv_n = (D.hq + 2 * D.hkv) * D.hd
-        # a residual add waits in tmp until the next norm takes it (one launch)
+        # a residual add waits (in tmp, or as down's slices) until the next
+        # norm takes it (one launch)
         pending = False
+        S_down = 1
         for l in range(D.layers):
             if hooks is not None:
                 hooks.before_layer(l)
-            if pending:
+            if pending and self.fold:
+                bd.boost_add_rmsnorm_slices(c, self.x, self.down_sl, S_down, D.ffn,
+                                            self.norms[f"norm1.{l}"], B, D.d, EPS, self.h, s)
+            elif pending:
                 bd.boost_add_rmsnorm(c, self.x, self.tmp, self.norms[f"norm1.{l}"], B, D.d,
                                      EPS, self.h, s)
             else:
                 bd.boost_rmsnorm(c, self.x, self.norms[f"norm1.{l}"], B, D.d, EPS, self.h, s)
-            if self.fold_qkv:
+            if self.fold:
                 S = bd.boost_decode_gemv_slices(c, self.mat[f"qkv.{l}"], qkv_n, D.d, self.h, B,
                                                 self.qkv, bd.MAX_GEMV_SLICES, s)
-                bd.boost_rope_kv_append_slices(c, self.pool, l, self.qkv, S, positions, B, D.hq,
-                                               THETA, tables, self.mb, self.q, s)
+                bd.boost_rope_kv_append_slices(c, self.pool, l, self.qkv, S, D.d, positions, B,
+                                               D.hq, THETA, tables, self.mb, self.q, s)
             else:
                 bd.boost_decode_gemv(c, self.mat[f"qkv.{l}"], qkv_n, D.d, self.h, B, self.qkv,
                                      F32, s)
@@ -113,11 +125,11 @@ class DecodeModel:
                                         tables, self.mb, self.q, s)
             bd.boost_paged_attn_decode(c, self.pool, l, self.q, B, D.hq, tables, self.mb,
                                        lens, 0.0, self.o, BF16, s)
-            if self.fold_o:
+            if self.fold:
                 S = bd.boost_decode_gemv_slices(c, self.mat[f"o.{l}"], D.d, D.hq * D.hd, self.o,
                                                 B, self.o_sl, bd.MAX_GEMV_SLICES, s)
-                bd.boost_add_rmsnorm_slices(c, self.x, self.o_sl, S, self.norms[f"norm2.{l}"], B,
-                                            D.d, EPS, self.h, s)
+                bd.boost_add_rmsnorm_slices(c, self.x, self.o_sl, S, D.hq * D.hd,
+                                            self.norms[f"norm2.{l}"], B, D.d, EPS, self.h, s)
             else:
                 bd.boost_decode_gemv(c, self.mat[f"o.{l}"], D.d, D.hq * D.hd, self.o, B,
                                      self.tmp, F32, s)
@@ -126,14 +138,22 @@ class DecodeModel:
             bd.boost_decode_gemv(c, self.mat[f"gate_up.{l}"], 2 * D.ffn, D.d, self.h, B,
                                  self.gu, F32, s)
             bd.boost_silu_mul(c, self.gu, B, D.ffn, self.act, s)
-            bd.boost_decode_gemv(c, self.mat[f"down.{l}"], D.d, D.ffn, self.act, B,
-                                 self.tmp, F32, s)
+            if self.fold:
+                S_down = bd.boost_decode_gemv_slices(c, self.mat[f"down.{l}"], D.d, D.ffn,
+                                                     self.act, B, self.down_sl,
+                                                     bd.MAX_GEMV_SLICES, s)
+            else:
+                bd.boost_decode_gemv(c, self.mat[f"down.{l}"], D.d, D.ffn, self.act, B,
+                                     self.tmp, F32, s)
             if hooks is not None:
                 hooks.after_layer(l)
             pending = True
         if hooks is not None:
             hooks.before_head()
-        if pending:
+        if pending and self.fold:
+            bd.boost_add_rmsnorm_slices(c, self.x, self.down_sl, S_down, D.ffn,
+                                        self.norms["norm_f"], B, D.d, EPS, self.h, s)
+        elif pending:
             bd.boost_add_rmsnorm(c, self.x, self.tmp, self.norms["norm_f"], B, D.d, EPS,
                                  self.h, s)
         else:

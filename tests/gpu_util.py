@@ -63,3 +63,32 @@ def fill_pool(bd, ctx, pool, layer, lengths, ks, vs, rid_base=0, max_blocks=None
         bd.boost_kv_write(ctx, pool, layer, s, k, v, int(s.numel()), stream())
         sync()
     return tables
+
+
+def slices_sum(flat, S, B, N, K):
+    """The output [B, N] that a split-K slice buffer stands for, by the layout
+    and order the library's header states: S slices [S][B][N] added in slice
+    order to 0.0f (fp32 adds), and for a row of the [N, K] matrix that
+    crosses a 2 MiB page, the sum of its earlier page's parts plus the sum of
+    its later page's parts, kept after the slices by the page of the row's
+    last column.  One slice is the output itself."""
+    flat = np.asarray(flat, np.float32)
+    if S == 1:
+        return flat[:B * N].reshape(B, N).copy()
+    sl = flat[:S * B * N].reshape(S, B, N)
+    acc = np.zeros((B, N), np.float32)
+    for s in range(S):
+        acc = acc + sl[s]
+    tail = flat[S * B * N:]
+    page = 1 << 20
+    for r in range(N):
+        first, last = r * K // page, (r * K + K - 1) // page
+        if first == last:
+            continue
+        v0, v1 = np.zeros(B, np.float32), np.zeros(B, np.float32)
+        for s in range(S):
+            o0, o1 = ((last * 2) * S + s) * B, ((last * 2 + 1) * S + s) * B
+            v0 = v0 + tail[o0:o0 + B]
+            v1 = v1 + tail[o1:o1 + B]
+        acc[:, r] = v0 + v1
+    return acc

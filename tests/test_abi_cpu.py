@@ -77,6 +77,18 @@ def test_host_numa_setting():
         bd.boost_shutdown(ctx)
 
 
+def test_gemv_slices_floats():
+    """Slice buffer size: max_slices * B * (N + 2 (pages + 1)) floats, pages of
+    2^20 bf16 elements of the [N, K] matrix (the 8B o and down matrices)."""
+    assert bd.boost_gemv_slices_floats(4096, 4096, 64, 8) == 8 * 64 * (4096 + 2 * 17)
+    assert bd.boost_gemv_slices_floats(4096, 14336, 64, 4) == 4 * 64 * (4096 + 2 * 57)
+    assert bd.boost_gemv_slices_floats(3, 8, 1, 1) == 1 * (3 + 2 * 2)
+    for bad in ((0, 8, 1, 1), (8, 0, 1, 1), (8, 8, 0, 1), (8, 8, 1, 0)):
+        with pytest.raises(bd.BoostError) as e:
+            bd.boost_gemv_slices_floats(*bad)
+        assert e.value.code == bd.EINVAL
+
+
 def test_cap_sweep_needs_a_device():
     ctx = bd.boost_init(-1)
     try:

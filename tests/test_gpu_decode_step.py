@@ -139,21 +139,22 @@ def test_small_model_step_parity_and_invariance(gpu_ctx):
 
 
 def test_split_projection_fold_matches_reduction(gpu_ctx):
-    """A batch of 24 on d = 2048 splits K of the qkv and o projections over
-    workgroups (four slices each); handing the slices to the RoPE + KV append
-    and to the residual norm gives the same ids and logits, bit for bit, as
-    reducing each projection first, and both meet the oracle."""
-    dims = Dims(layers=2, d=2048, hq=16, hkv=4, hd=128, ffn=2048, vocab=1000)
+    """A batch of 24 on d = 2048 splits K of the qkv, o and down projections
+    over workgroups (down's rows, K = 3072, cross page boundaries); handing
+    the slices to the RoPE + KV append and to the residual norms gives the
+    same ids and logits, bit for bit, as reducing each projection first, and
+    both meet the oracle."""
+    dims = Dims(layers=2, d=2048, hq=16, hkv=4, hd=128, ffn=3072, vocab=1000)
     w = model_weights(dims, 8)
     lengths = synth.context_lengths(21, 24, 1, 200)
     tokens = synth.context_lengths(22, 24, 0, dims.vocab - 1)
     model, pool, mats, tables, kc, vc = build(gpu_ctx, dims, w, lengths, True, bd.KV_LPP)
     try:
-        assert model.fold_qkv and model.fold_o
+        assert model.fold
         folded = run(model, tokens, lengths, tables)
         plain = DecodeModel(gpu_ctx, dims, len(lengths), model.mb, pool, mats, model.norms,
                             fold_slices=False)
-        assert not plain.fold_qkv and not plain.fold_o
+        assert not plain.fold
         reduced = run(plain, tokens, lengths, tables)
     finally:
         free(pool, mats)

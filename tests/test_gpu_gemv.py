@@ -6,7 +6,7 @@ import synth
 from oracle import gemv as og
 from oracle import placement as opl
 from paper_2609_13592_amd import binding as bd
-from tests.gpu_util import dev_f32, dev_u16, host_u16, stream, sync, to_dev_u16
+from tests.gpu_util import dev_f32, dev_u16, host_u16, slices_sum, stream, sync, to_dev_u16
 
 pytestmark = pytest.mark.gpu
 TOL = 2e-2          # stated bar for bf16 inputs (max rel err)
@@ -361,25 +361,17 @@ def test_full_size_70b_tensor_sampled_batch8(gpu_ctx, kind):
         torch.cuda.empty_cache()
 
 
-def slice_order_sum(sl, S):
-    """The split-K slices added in slice order to 0.0f in fp32 (IEEE adds in
-    numpy); one slice is the output itself."""
-    if S == 1:
-        return sl[0].copy()
-    acc = np.zeros_like(sl[0])
-    for s in range(S):
-        acc = acc + sl[s]
-    return acc
-
-
 @pytest.mark.parametrize("N,K,B,split", [(6144, 4096, 64, True), (4096, 4096, 64, True),
                                          (128, 16384, 64, True), (600, 4096, 128, None),
-                                         (3072, 2048, 24, True), (2048, 2048, 24, True), (300, 2048, 3, False),
-                                         (1000, 8, 100, None)])
+                                         (3072, 2048, 24, True), (2048, 2048, 24, True),
+                                         (300, 2048, 3, False), (1000, 8, 100, None),
+                                         (4096, 14336, 64, True), (2048, 3072, 24, True),
+                                         (300, 14336, 7, None), (130, 14336, 256, None)])
 def test_slices_sum_to_y(gpu_ctx, N, K, B, split):
-    """The slices entry point writes split-K partials whose slice-order sum is
+    """The slices entry point writes split-K partials (and the parts of rows
+    cut by page boundaries) whose sum, in the order the header states, is
     boost_decode_gemv's y bit for bit, under the HBM, alternating and MPP
-    maps; a cap of one slice gives an unsplit y within the oracle's bar.
+    maps; caps of one and two slices give a y within the oracle's bar.
     `split` says whether the shape must split (None: either)."""
     w, x = synth.gemv_inputs(91 + N + K + B, N, K, B)
     n = opl.n_pages(w.nbytes)
@@ -387,28 +379,29 @@ def test_slices_sum_to_y(gpu_ctx, N, K, B, split):
             "mpp3": opl.mpp_tier_map(w.nbytes, 3)}
     xd = to_dev_u16(x)
     r64 = og.gemv_f64(w, x)
+    size = bd.boost_gemv_slices_floats(N, K, B, bd.MAX_GEMV_SLICES)
     ys = []
     for name, tiers in maps.items():
         t = place(gpu_ctx, w, tiers=tiers)
         try:
             y = run_gemv(gpu_ctx, t, N, K, xd, B)
-            sl = dev_f32(bd.MAX_GEMV_SLICES, B, N)
+            sl = dev_f32(size)
+            sl.fill_(float("nan"))  # the unwritten entries must not reach y
             S = bd.boost_decode_gemv_slices(gpu_ctx, t, N, K, xd, B, sl, bd.MAX_GEMV_SLICES,
                                             stream())
             sync()
             assert 1 <= S <= bd.MAX_GEMV_SLICES
             if split is not None:
                 assert (S > 1) == split, (name, S)
-            got = slice_order_sum(sl.cpu().numpy(), S)
+            got = slices_sum(sl.cpu().numpy(), S, B, N, K)
             assert np.array_equal(got.view(np.uint32), y.view(np.uint32)), name
             ys.append(y)
-            # capped at one and at two slices
             for cap in (1, 2):
                 sl.fill_(float("nan"))
                 S2 = bd.boost_decode_gemv_slices(gpu_ctx, t, N, K, xd, B, sl, cap, stream())
                 sync()
                 assert 1 <= S2 <= cap
-                y2 = slice_order_sum(sl.cpu().numpy(), S2)
+                y2 = slices_sum(sl.cpu().numpy(), S2, B, N, K)
                 assert og.rel_err(y2, r64) <= TOL, (name, cap)
                 assert_f32_bound(y2, w, x)
         finally:
@@ -419,27 +412,20 @@ def test_slices_sum_to_y(gpu_ctx, N, K, B, split):
 
 
 def test_slices_bad_arguments(gpu_ctx):
-    """Rows crossing page boundaries (K not dividing 2^20) and slice caps
-    outside [1, 8] are refused before anything runs."""
-    w, x = synth.gemv_inputs(2, 300, 14336, 64)
-    t = place(gpu_ctx, w, M=3)
-    xd = to_dev_u16(x)
-    sl = dev_f32(bd.MAX_GEMV_SLICES, 64, 300)
-    try:
-        for K, cap in ((14336, 8), (14336, 1)):
-            with pytest.raises(bd.BoostError) as e:
-                bd.boost_decode_gemv_slices(gpu_ctx, t, 300, K, xd, 64, sl, cap, stream())
-            assert e.value.code == bd.EINVAL
-    finally:
-        bd.boost_tensor_free(t)
+    """Slice caps outside [1, 8] and misaligned buffers are refused before
+    anything runs."""
     w, x = synth.gemv_inputs(3, 256, 4096, 64)
     t = place(gpu_ctx, w, M=3)
     xd = to_dev_u16(x)
+    sl = dev_f32(bd.boost_gemv_slices_floats(256, 4096, 64, bd.MAX_GEMV_SLICES) + 4)
     try:
         for cap in (0, bd.MAX_GEMV_SLICES + 1):
             with pytest.raises(bd.BoostError) as e:
                 bd.boost_decode_gemv_slices(gpu_ctx, t, 256, 4096, xd, 64, sl, cap, stream())
             assert e.value.code == bd.EINVAL
+        with pytest.raises(bd.BoostError) as e:
+            bd.boost_decode_gemv_slices(gpu_ctx, t, 256, 4096, xd, 64, sl[1:], 8, stream())
+        assert e.value.code == bd.EINVAL
     finally:
         bd.boost_tensor_free(t)
 

@@ -8,7 +8,7 @@ import synth
 from oracle import decode_step as ods
 from oracle.gemv import bf16_to_f32, f32_to_bf16
 from paper_2609_13592_amd import binding as bd
-from tests.gpu_util import host_u16, stream, sync, to_dev_u16
+from tests.gpu_util import host_u16, slices_sum, stream, sync, to_dev_u16
 
 pytestmark = pytest.mark.gpu
 B, D_MODEL, HQ, HKV, HD, FFN, VOCAB = 8, 8192, 64, 8, 128, 28672, 128256
@@ -171,56 +171,59 @@ def test_add_rmsnorm_equals_add_then_norm(gpu_ctx, d):
     assert e.value.code == bd.EINVAL
 
 
-@pytest.mark.parametrize("d,S", [(4096, 1), (4096, 4), (8192, 8), (1026, 3)])
-def test_add_rmsnorm_slices_equals_sum_then_fused(gpu_ctx, d, S):
-    """With the residual handed over as S split-K slices, x and the norm get
-    the same bits as the fused call on the slices' slice-order fp32 sum
-    (vector path and plain loop); bad slice counts are refused."""
+def random_slices(rng, S, B, N, K):
+    """A slice buffer in the GEMV's layout: S random slices [S][B][N] and, for
+    the rows of an [N, K] matrix that cross a page, random parts after them."""
+    pages = -(-N * K // (1 << 20))
+    tail = (pages + 1) * 2 * S * B if S > 1 else 0
+    return (rng.standard_normal(S * B * N + tail) * 2).astype(np.float32)
+
+
+@pytest.mark.parametrize("d,S,K", [(4096, 1, 4096), (4096, 4, 4096), (8192, 8, 8192),
+                                   (1026, 3, 4096), (4096, 4, 14336), (4096, 8, 14336),
+                                   (1026, 2, 3000)])
+def test_add_rmsnorm_slices_equals_sum_then_fused(gpu_ctx, d, S, K):
+    """With the residual handed over as S split-K slices of a [d, K] matrix
+    (K = 14336 and 3000: rows cut by pages, whose parts follow the slices), x
+    and the norm get the same bits as the fused call on the sum the header
+    defines (vector path and plain loop); bad slice counts are refused."""
     import torch
-    rng = np.random.default_rng(200 + d + S)
+    rng = np.random.default_rng(200 + d + S + K)
     Bn = 6
     x = (rng.standard_normal((Bn, d)) * 2).astype(np.float32)
-    sl = (rng.standard_normal((S, Bn, d)) * 2).astype(np.float32)
-    r = sl[0].copy()
-    if S > 1:
-        r = np.zeros((Bn, d), np.float32)
-        for s in range(S):
-            r = r + sl[s]
+    flat = random_slices(rng, S, Bn, d, K)
+    r = slices_sum(flat, S, Bn, d, K)
     w = synth.round_bf16((1 + 0.1 * rng.standard_normal(d)).astype(np.float32))
     wd = to_dev_u16(w)
     x1, x2 = dev(x), dev(x)
     o1 = torch.empty((Bn, d), dtype=torch.int16, device="cuda")
     o2 = torch.empty((Bn, d), dtype=torch.int16, device="cuda")
     bd.boost_add_rmsnorm(gpu_ctx, x1, dev(r), wd, Bn, d, 1e-5, o1, stream())
-    bd.boost_add_rmsnorm_slices(gpu_ctx, x2, dev(sl), S, wd, Bn, d, 1e-5, o2, stream())
+    bd.boost_add_rmsnorm_slices(gpu_ctx, x2, dev(flat), S, K, wd, Bn, d, 1e-5, o2, stream())
     sync()
     assert np.array_equal(x2.cpu().numpy().view(np.uint32), (x + r).view(np.uint32))
     assert np.array_equal(x1.cpu().numpy().view(np.uint32), x2.cpu().numpy().view(np.uint32))
     assert np.array_equal(host_u16(o1), host_u16(o2))
     assert_bf16_close(host_u16(o2), ods.to_bf16(ods.rmsnorm((x + r).astype(np.float64), w)))
-    for bad in (0, bd.MAX_GEMV_SLICES + 1):
+    for bad_s, bad_k in ((0, K), (bd.MAX_GEMV_SLICES + 1, K), (S, 0)):
         with pytest.raises(bd.BoostError) as e:
-            bd.boost_add_rmsnorm_slices(gpu_ctx, x2, dev(sl), bad, wd, Bn, d, 1e-5, o2,
-                                        stream())
+            bd.boost_add_rmsnorm_slices(gpu_ctx, x2, dev(flat), bad_s, bad_k, wd, Bn, d, 1e-5,
+                                        o2, stream())
         assert e.value.code == bd.EINVAL
 
 
-@pytest.mark.parametrize("S", [1, 2, 8])
-def test_rope_kv_append_slices_equals_sum(gpu_ctx, S):
-    """RoPE + KV append of S qkv slices writes the same q and pool slots as the
-    call on their slice-order fp32 sum (attention over the two pools agrees
-    bitwise)."""
+@pytest.mark.parametrize("S,K", [(1, 8192), (2, 8192), (8, 8192), (4, 14336)])
+def test_rope_kv_append_slices_equals_sum(gpu_ctx, S, K):
+    """RoPE + KV append of S qkv slices (K = 14336: rows cut by pages) writes
+    the same q and pool slots as the call on their sum (attention over the two
+    pools agrees bitwise)."""
     import torch
-    rng = np.random.default_rng(30 + S)
+    rng = np.random.default_rng(30 + S + K)
     heads = HQ + 2 * HKV
     mb = 8
     pos = np.array([0, 3, 15, 16, 40, 77, 100, 127], dtype=np.int32)
-    sl = rng.standard_normal((S, B, heads * HD)).astype(np.float32)
-    qkv = sl[0].copy()
-    if S > 1:
-        qkv = np.zeros((B, heads * HD), np.float32)
-        for s in range(S):
-            qkv = qkv + sl[s]
+    flat = random_slices(rng, S, B, heads * HD, K)
+    qkv = slices_sum(flat, S, B, heads * HD, K)
     pools, outs, qs = [], [], []
     try:
         for sliced in (False, True):
@@ -231,7 +234,7 @@ def test_rope_kv_append_slices_equals_sum(gpu_ctx, S):
             td, pd = dev(tables), dev(pos)
             q = torch.empty((B, HQ, HD), dtype=torch.int16, device="cuda")
             if sliced:
-                bd.boost_rope_kv_append_slices(gpu_ctx, pool, 0, dev(sl), S, pd, B, HQ,
+                bd.boost_rope_kv_append_slices(gpu_ctx, pool, 0, dev(flat), S, K, pd, B, HQ,
                                                500000.0, td, mb, q, stream())
             else:
                 bd.boost_rope_kv_append(gpu_ctx, pool, 0, dev(qkv), pd, B, HQ, 500000.0, td, mb,
@@ -246,8 +249,8 @@ def test_rope_kv_append_slices_equals_sum(gpu_ctx, S):
         assert np.array_equal(qs[0], qs[1])
         assert np.array_equal(outs[0].view(np.uint32), outs[1].view(np.uint32))
         with pytest.raises(bd.BoostError) as e:
-            bd.boost_rope_kv_append_slices(gpu_ctx, pools[1], 0, dev(sl), 0, dev(pos), B, HQ,
-                                           500000.0, dev(np.zeros((B, mb), np.int32)), mb,
+            bd.boost_rope_kv_append_slices(gpu_ctx, pools[1], 0, dev(flat), 0, K, dev(pos), B,
+                                           HQ, 500000.0, dev(np.zeros((B, mb), np.int32)), mb,
                                            dev(qs[1]), stream())
         assert e.value.code == bd.EINVAL
     finally:
