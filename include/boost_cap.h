@@ -253,6 +253,13 @@ int boost_place_weights_map(boost_ctx *ctx, const void *src, uint64_t bytes,
 int boost_tensor_tiers(const boost_tensor *t, uint8_t *tier_out,
                        uint64_t tier_cap, uint64_t *n_pages);
 
+/* The closed form of t's tier map that the GEMV kernels use to find a page
+ * (§3.1: placement by page index modulo M over superpages of SP pages):
+ * page p is on host iff (p / SP) % M == M - 1, *M = 0 when no page is on
+ * host; *M = -1 when the map has no such form (arbitrary maps, staged views),
+ * and the kernels read the page tables instead.  Errors: EINVAL (null). */
+int boost_tensor_layout(const boost_tensor *t, int32_t *M, int32_t *SP);
+
 /* Copy `bytes` bytes starting at logical offset `offset` of a placed tensor
  * back to host memory `dst` through its page table (checks, synchronises). */
 int boost_tensor_read(const boost_tensor *t, uint64_t offset, void *dst,

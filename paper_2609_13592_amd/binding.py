@@ -82,6 +82,7 @@ _SIGS = {
     "boost_place_weights": (_i32, [_vp, _vp, _u64, _u32, _u64, C.POINTER(_vp)]),
     "boost_place_weights_map": (_i32, [_vp, _vp, _u64, _vp, _u64, C.POINTER(_vp)]),
     "boost_tensor_tiers": (_i32, [_vp, _vp, _u64, C.POINTER(_u64)]),
+    "boost_tensor_layout": (_i32, [_vp, C.POINTER(_i32), C.POINTER(_i32)]),
     "boost_tensor_read": (_i32, [_vp, _u64, _vp, _u64]),
     "boost_tensor_free": (_i32, [_vp]),
     "boost_gemv_set_schedule": (_i32, [_vp, _i32, _i32]),
@@ -329,6 +330,13 @@ def boost_place_weights_map(ctx: int, src, nbytes: int, tiers) -> int:
     _check(load().boost_place_weights_map(ctx, _ptr(src), nbytes, _ptr(t), t.size,
                                           C.byref(h)))
     return h.value
+
+
+def boost_tensor_layout(t: int):
+    """(M, SP) of the tensor's closed-form map, M = -1 when it has none."""
+    m, sp = C.c_int32(0), C.c_int32(0)
+    _check(load().boost_tensor_layout(t, C.byref(m), C.byref(sp)))
+    return m.value, sp.value
 
 
 def boost_tensor_tiers(t: int) -> np.ndarray:

@@ -38,6 +38,14 @@ struct GemvParams {
   const uint8_t* tiers;  // tier of every page
   const int32_t* hbm_pages;
   const int32_t* host_pages;
+  // the same in closed form where the tensor's map is modulo placement:
+  // page p is on host iff (p / lay_SP) % lay_M == lay_M - 1 (lay_M = 0: no
+  // host page), each tier's pages sit in page order in one slab; lay_M < 0:
+  // read the tables
+  const char* hbm_base;
+  const char* host_base;
+  int lay_M;
+  int lay_SP;
   int n_pages;
   int n_hbm_pages;
   int n_host_pages;
@@ -60,6 +68,34 @@ struct GemvParams {
   float* slices;
   int64_t slice_floats;
 };
+
+// Page lookups: the closed form of modulo placement where the tensor has it
+// (no dependent load before a unit's first weight load), else the tables.
+__device__ __forceinline__ const char* page_addr(const GemvParams& P, int p) {
+  if (P.lay_M < 0) return P.page_table[p];
+  if (P.lay_M == 0) return P.hbm_base + static_cast<int64_t>(p) * bst::kPage;
+  const int g = p / P.lay_SP, before = g / P.lay_M;  // host superpages before g's group
+  if (g % P.lay_M == P.lay_M - 1)
+    return P.host_base + (static_cast<int64_t>(before) * P.lay_SP + p % P.lay_SP) * bst::kPage;
+  return P.hbm_base + (static_cast<int64_t>(p) - static_cast<int64_t>(before) * P.lay_SP) *
+                          bst::kPage;
+}
+__device__ __forceinline__ uint8_t page_tier(const GemvParams& P, int p) {
+  if (P.lay_M < 0) return P.tiers[p];
+  return P.lay_M > 0 && (p / P.lay_SP) % P.lay_M == P.lay_M - 1 ? BOOST_TIER_HOST
+                                                                 : BOOST_TIER_HBM;
+}
+// the i-th HBM page and the k-th host page in page order
+__device__ __forceinline__ int hbm_page(const GemvParams& P, int i) {
+  if (P.lay_M < 0) return P.hbm_pages[i];
+  if (P.lay_M == 0) return i;
+  const int per = (P.lay_M - 1) * P.lay_SP;  // HBM pages of a group of M superpages
+  return (i / per) * P.lay_M * P.lay_SP + i % per;
+}
+__device__ __forceinline__ int host_page(const GemvParams& P, int k) {
+  if (P.lay_M < 0) return P.host_pages[k];
+  return (k / P.lay_SP) * P.lay_M * P.lay_SP + (P.lay_M - 1) * P.lay_SP + k % P.lay_SP;
+}
 
 __device__ __forceinline__ float lo_bf16(uint32_t v) { return __uint_as_float(v << 16); }
 __device__ __forceinline__ float hi_bf16(uint32_t v) {
@@ -224,13 +260,13 @@ __device__ void gemv_unit(const GemvParams& P, int page, int j, float* lds) {
   const bool cut_last = rbase + kRowsWg > r_hi && (r_hi + 1) * K > pe1;
   bool prev_same = false, next_same = false;
   if (cut_first || cut_last) {
-    const uint8_t tier = P.tiers[page];
-    prev_same = cut_first && P.tiers[page - 1] == tier;
-    next_same = cut_last && page + 1 < P.n_pages && P.tiers[page + 1] == tier;
+    const uint8_t tier = page_tier(P, page);
+    prev_same = cut_first && page_tier(P, page - 1) == tier;
+    next_same = cut_last && page + 1 < P.n_pages && page_tier(P, page + 1) == tier;
   }
 
   const __amdgpu_buffer_rsrc_t wr =
-      make_rsrc(P.page_table[page], static_cast<uint32_t>((pe1 - pe0) * 2));
+      make_rsrc(page_addr(P, page), static_cast<uint32_t>((pe1 - pe0) * 2));
   const __amdgpu_buffer_rsrc_t xr =
       make_rsrc(P.x, static_cast<uint32_t>(B * K * 2));
   // 0 = whole row here, 1 = tail of a row begun on the previous page,
@@ -266,7 +302,7 @@ __device__ void gemv_unit(const GemvParams& P, int page, int j, float* lds) {
   if (join) {  // uniform over the slot (same rows, same page): the next page's part
     const int64_t pe2 = min(pe1 + kPageElems, total);
     const __amdgpu_buffer_rsrc_t wr2 =
-        make_rsrc(P.page_table[page + 1], static_cast<uint32_t>((pe2 - pe1) * 2));
+        make_rsrc(page_addr(P, page + 1), static_cast<uint32_t>((pe2 - pe1) * 2));
     accumulate<B, RW, UN>(wr2, xr, ro2, K, k_beg, k_end, lane, acc2);
   }
 
@@ -329,23 +365,23 @@ __device__ void gemv_unit(const GemvParams& P, int page, int j, float* lds) {
   }
 }
 
-// Unit `idx` of a list of n pages (list == nullptr: pages 0..n-1) with U units
-// each.  Normally page idx / U, unit idx % U.  With tail_first the first n
+// Unit `idx` of a list of n pages (the HBM pages in page order, or with
+// all_pages every page) with U units each.  Normally page idx / U, unit idx % U.  With tail_first the first n
 // indices are the last non-empty unit of every page and the rest the other
 // units in page order: the last unit of a page holds the row cut by the page
 // boundary, which it sums over both pages when they are in one tier, so it
 // reads twice as many steps as the others; dispatched first it overlaps
 // them instead of running alone at the end of the launch.
 template <int kRowsWg>
-__device__ __forceinline__ void unit_of(const GemvParams& P, const int32_t* list, int n, int U,
+__device__ __forceinline__ void unit_of(const GemvParams& P, bool all_pages, int n, int U,
                                         int idx, int& page, int& j) {
   if (!P.tail_first) {
-    page = list ? list[idx / U] : idx / U;
+    page = all_pages ? idx / U : hbm_page(P, idx / U);
     j = idx % U;
     return;
   }
   const int i = idx < n ? idx : (idx - n) / (U - 1);
-  page = list ? list[i] : i;
+  page = all_pages ? i : hbm_page(P, i);
   const int64_t total = static_cast<int64_t>(P.N) * P.K;
   const int64_t pe0 = static_cast<int64_t>(page) * kPageElems;
   const int64_t pe1 = min(pe0 + kPageElems, total);
@@ -366,14 +402,14 @@ __global__ __launch_bounds__(kThreads) void gemv_kernel(GemvParams P) {
   const int U = P.units_per_page;
   int page, j;
   if (P.address_order) {
-    unit_of<kRowsWg>(P, nullptr, P.n_pages, U, bid, page, j);
+    unit_of<kRowsWg>(P, true, P.n_pages, U, bid, page, j);
     gemv_unit<B, RW, UN, KS>(P, page, j, lds);
   } else if (bid < P.host_workers) {
     const int n_host_units = P.n_host_pages * U;
     for (int v = bid; v < n_host_units; v += P.host_workers)
-      gemv_unit<B, RW, UN, KS>(P, P.host_pages[v / U], v % U, lds);
+      gemv_unit<B, RW, UN, KS>(P, host_page(P, v / U), v % U, lds);
   } else {
-    unit_of<kRowsWg>(P, P.hbm_pages, P.n_hbm_pages, U, bid - P.host_workers, page, j);
+    unit_of<kRowsWg>(P, false, P.n_hbm_pages, U, bid - P.host_workers, page, j);
     gemv_unit<B, RW, UN, KS>(P, page, j, lds);
   }
 }
@@ -386,7 +422,7 @@ __global__ __launch_bounds__(256) void split_fixup(GemvParams P, int n_pages, in
   if (bnd >= n_pages) return;
   const int64_t e = static_cast<int64_t>(bnd) * kPageElems;
   if (e % P.K == 0) return;  // this boundary falls between rows
-  if (P.join && P.tiers[bnd - 1] == P.tiers[bnd]) return;  // summed by one workgroup
+  if (P.join && page_tier(P, bnd - 1) == page_tier(P, bnd)) return;  // summed by one workgroup
   const float* s0 = P.partial + static_cast<int64_t>(bnd) * 2 * bst::kMaxGemvBatch;
   store_y(P, b, e / P.K, s0[b] + s0[bst::kMaxGemvBatch + b]);
 }
@@ -456,7 +492,7 @@ __device__ void mfma_unit(const GemvParams& P, int page, int unit, float* lds) {
   const int lrow = lane & 15, lgrp = lane >> 4;
 
   const __amdgpu_buffer_rsrc_t wr =
-      make_rsrc(P.page_table[page], static_cast<uint32_t>((pe1 - pe0) * 2));
+      make_rsrc(page_addr(P, page), static_cast<uint32_t>((pe1 - pe0) * 2));
   const __amdgpu_buffer_rsrc_t xr =
       make_rsrc(P.x, static_cast<uint32_t>(static_cast<int64_t>(P.B) * K * 2));
   uint32_t xo[BT];
@@ -644,10 +680,10 @@ __global__ __launch_bounds__(kThreads) void mfma_kernel(GemvParams P) {
   } else if (bid < P.host_workers) {
     const int n_host_units = P.n_host_pages * U;
     for (int v = bid; v < n_host_units; v += P.host_workers)
-      mfma_unit<BT, RT, UN, WL>(P, P.host_pages[v / U], v % U, lds);
+      mfma_unit<BT, RT, UN, WL>(P, host_page(P, v / U), v % U, lds);
   } else {
     const int u = bid - P.host_workers;
-    mfma_unit<BT, RT, UN, WL>(P, P.hbm_pages[u / U], u % U, lds);
+    mfma_unit<BT, RT, UN, WL>(P, hbm_page(P, u / U), u % U, lds);
   }
 }
 
@@ -752,7 +788,7 @@ __device__ __forceinline__ void gemm_dma_unit(const GemvParams& P, int page_in, 
   const int lrow = lane & 15, lgrp = lane >> 4;
 
   const __amdgpu_buffer_rsrc_t wr =
-      make_rsrc_uniform(P.page_table[page], static_cast<uint32_t>((pe1 - pe0) * 2));
+      make_rsrc_uniform(page_addr(P, page), static_cast<uint32_t>((pe1 - pe0) * 2));
   const __amdgpu_buffer_rsrc_t xr =
       make_rsrc_uniform(P.x, static_cast<uint32_t>(static_cast<int64_t>(P.B) * K * 2));
 
@@ -917,10 +953,10 @@ __global__ __launch_bounds__(64 * NW) void gemm_dma_kernel(GemvParams P) {
     const int Uh = U * 4 * RT;  // 16-row sub-units per host page
     const int n_host_sub = P.n_host_pages * Uh;
     for (int v = bid; v < n_host_sub; v += P.host_workers)
-      gemm_dma_unit<BT, RT, true, NW>(P, P.host_pages[v / Uh], v % Uh, ring);
+      gemm_dma_unit<BT, RT, true, NW>(P, host_page(P, v / Uh), v % Uh, ring);
   } else {
     const int u = bid - P.host_workers;
-    gemm_dma_unit<BT, RT, false, NW>(P, P.hbm_pages[u / U], u % U, ring);
+    gemm_dma_unit<BT, RT, false, NW>(P, hbm_page(P, u / U), u % U, ring);
   }
 }
 
@@ -1306,6 +1342,10 @@ int decode_gemv(boost_ctx* ctx, const boost_tensor* W, int N, int K, const void*
   P.page_table = W->d_page_table;
   P.hbm_pages = W->d_hbm_pages;
   P.host_pages = W->d_host_pages;
+  P.hbm_base = W->hbm.base;
+  P.host_base = W->host.base;
+  P.lay_M = W->lay_M;
+  P.lay_SP = W->lay_SP;
   P.n_hbm_pages = static_cast<int>(W->hbm_pages.size());
   P.n_host_pages = static_cast<int>(W->host_pages.size());
   P.address_order = ctx->gemv_schedule == BOOST_SCHED_ADDRESS;

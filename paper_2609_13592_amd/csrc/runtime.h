@@ -54,6 +54,11 @@ struct boost_tensor {
   std::vector<char*> copy_ptr;          // address for host-side copies
   std::vector<int32_t> hbm_pages, host_pages;
   bst::Slab hbm, host;
+  // the map in closed form when it is modulo placement: page p on host iff
+  // (p / lay_SP) % lay_M == lay_M - 1 (lay_M = 0: every page in HBM), each
+  // tier's pages in page order in its slab; lay_M < 0: no closed form (the
+  // kernels read the tables)
+  int32_t lay_M = -1, lay_SP = 1;
   // device-side copies
   char** d_page_table = nullptr;        // [n_pages]
   uint8_t* d_tiers = nullptr;           // [n_pages] tier codes

@@ -182,6 +182,30 @@ static int upload(void** dst, const void* src, size_t bytes) {
   return BOOST_OK;
 }
 
+// The closed form of a tier map that is modulo placement (§3.1): host iff
+// (p / SP) % M == M - 1, with SP the first run of host pages and M - 1 the
+// superpages before it; M = 0 when no page is on host; M = -1 when the map
+// has no such form.
+static void modulo_form(const std::vector<uint8_t>& tiers, int32_t& M, int32_t& SP) {
+  M = -1;
+  SP = 1;
+  const uint64_t n = tiers.size();
+  uint64_t first = 0;
+  while (first < n && tiers[first] != BOOST_TIER_HOST) ++first;
+  if (first == n) {
+    M = 0;
+    return;
+  }
+  uint64_t run = 0;
+  while (first + run < n && tiers[first + run] == BOOST_TIER_HOST) ++run;
+  if (first % run != 0 || first / run + 1 > INT32_MAX || run > INT32_MAX) return;
+  const uint64_t m = first / run + 1;
+  for (uint64_t i = 0; i < n; ++i)
+    if ((tiers[i] == BOOST_TIER_HOST) != ((i / run) % m == m - 1)) return;
+  M = static_cast<int32_t>(m);
+  SP = static_cast<int32_t>(run);
+}
+
 static int place(boost_ctx* ctx, const void* src, uint64_t bytes,
                  const uint8_t* tiers, uint64_t n_pages, boost_tensor** out) {
   if (!ctx || !src || !out || !tiers) return fail(BOOST_EINVAL, "null argument");
@@ -214,6 +238,7 @@ static int place(boost_ctx* ctx, const void* src, uint64_t bytes,
     free_tensor(t);
     return rc;
   }
+  modulo_form(t->tiers, t->lay_M, t->lay_SP);
   t->page_ptr.resize(n_pages);
   t->copy_ptr.resize(n_pages);
   for (size_t i = 0; i < t->hbm_pages.size(); ++i)
@@ -376,6 +401,13 @@ int boost_tensor_tiers(const boost_tensor* t, uint8_t* tier_out, uint64_t tier_c
   *n_pages = t->n_pages;
   if (tier_out)
     std::memcpy(tier_out, t->tiers.data(), std::min<uint64_t>(tier_cap, t->n_pages));
+  return BOOST_OK;
+}
+
+int boost_tensor_layout(const boost_tensor* t, int32_t* M, int32_t* SP) {
+  if (!t || !M || !SP) return fail(BOOST_EINVAL, "null argument");
+  *M = t->lay_M;
+  *SP = t->lay_SP;
   return BOOST_OK;
 }
 

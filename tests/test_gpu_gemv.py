@@ -31,6 +31,12 @@ def run_gemv(ctx, t, N, K, x_dev, B, y_dtype=bd.DTYPE_F32):
     return y.cpu().numpy() if y_dtype == bd.DTYPE_F32 else host_u16(y)
 
 
+def irregular_map(n):
+    """Host pages at 0, 3, 5, 8, 10, ... (two per five, unevenly spaced): a map
+    with no modulo closed form, so the kernels read the page tables."""
+    return ((np.arange(n) * 7) % 5 < 2).astype(np.uint8)
+
+
 def place(ctx, w, tiers=None, M=None):
     nbytes = w.nbytes
     if tiers is not None:
@@ -127,7 +133,7 @@ def test_placement_invariance_and_parity(gpu_ctx, N, K, B):
     n = opl.n_pages(w.nbytes)
     maps = {"hbm": np.zeros(n, np.uint8), "host": np.ones(n, np.uint8),
             "alt": (np.arange(n) % 2).astype(np.uint8),
-            "mpp3": opl.mpp_tier_map(w.nbytes, 3)}
+            "mpp3": opl.mpp_tier_map(w.nbytes, 3), "irregular": irregular_map(n)}
     xd = to_dev_u16(x)
     r64 = og.gemv_f64(w, x)
     r32 = og.gemv_f32(w, x)
@@ -169,7 +175,7 @@ def test_mfma_placement_invariance_and_parity(gpu_ctx, N, K, B):
     n = opl.n_pages(w.nbytes)
     maps = {"hbm": np.zeros(n, np.uint8), "host": np.ones(n, np.uint8),
             "alt": (np.arange(n) % 2).astype(np.uint8),
-            "mpp3": opl.mpp_tier_map(w.nbytes, 3)}
+            "mpp3": opl.mpp_tier_map(w.nbytes, 3), "irregular": irregular_map(n)}
     xd = to_dev_u16(x)
     r64 = og.gemv_f64(w, x)
     outs = []
@@ -307,6 +313,7 @@ def test_prefetch_staged_view(gpu_ctx):
     v = bd.boost_staged_view(gpu_ctx, t, staging, staging.numel())
     try:
         assert not bd.boost_tensor_tiers(v).any()
+        assert bd.boost_tensor_layout(v)[0] == -1  # staged pages: no closed form
         xd = to_dev_u16(x)
         bd.boost_prefetch(gpu_ctx, v, stream())
         yv = run_gemv(gpu_ctx, v, N, K, xd, 1)
@@ -453,3 +460,33 @@ def test_host_pages_bound_to_a_numa_node(gpu_ctx):
         bd.boost_set_host_numa(gpu_ctx, bd.NUMA_DEVICE)
     assert og.rel_err(ys[0], og.gemv_f64(w, x)) <= TOL
     assert np.array_equal(ys[0].view(np.uint32), ys[1].view(np.uint32))
+
+
+def test_closed_form_layouts(gpu_ctx):
+    """Modulo maps get the closed form the kernels compute pages from (all
+    HBM, all host, alternating, MPP with and without superpages); an
+    irregular map and a staged view keep the tables; the GEMV gives the same
+    bits either way."""
+    w, x = synth.gemv_inputs(8, 2048, 4096, 3)   # 8 pages
+    n = opl.n_pages(w.nbytes)
+    xd = to_dev_u16(x)
+    cases = [(np.zeros(n, np.uint8), (0, 1)), (np.ones(n, np.uint8), (1, n)),
+             ((np.arange(n) % 2).astype(np.uint8), (2, 1)),
+             (((np.arange(n) // 2) % 3 == 2).astype(np.uint8), (3, 2)),
+             (irregular_map(n), (-1, 1))]
+    ys = []
+    for tiers, want in cases:
+        t = place(gpu_ctx, w, tiers=tiers)
+        try:
+            assert bd.boost_tensor_layout(t) == want, (tiers, want)
+            ys.append(run_gemv(gpu_ctx, t, 2048, 4096, xd, 3))
+        finally:
+            bd.boost_tensor_free(t)
+    t = place(gpu_ctx, w, M=4)
+    try:
+        M, SP = bd.boost_tensor_layout(t)
+        assert M == 4 or bd.boost_tensor_tiers(t).sum() == 0
+    finally:
+        bd.boost_tensor_free(t)
+    for y in ys[1:]:
+        assert np.array_equal(y.view(np.uint32), ys[0].view(np.uint32))
