@@ -132,26 +132,28 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(float* __restrict__ x, Sli
 }
 
 // The same for rows of d <= 8192 floats with d % 4 == 0 and 16-byte aligned
-// rows: each lane loads its (at most NV = 4 or 8) float4s of the row at once
-// and keeps them in registers for the second pass (the plain loop above is a chain of
-// dependent round trips: 20 us for a batch of 8 rows of 8192).
-constexpr int kNormVec = 8;
+// rows: each of the workgroup's 1024 lanes loads its (at most NV = 2) float4s
+// of the row at once and keeps them in registers for the second pass (the
+// plain loop above is a chain of dependent round trips: 20 us for a batch of
+// 8 rows of 8192); sixteen wavefronts per row keep its slice loads in flight.
+constexpr int kNormThreads = 1024;
+constexpr int kNormVec = 2;
 // Pages of the producing [d, K] matrix (at most d, since K <= 2^20 elements
 // and d <= 8192 here): a workgroup of the vector norm sums each cut row once
 // into LDS, indexed by the page of the row's last column.
-constexpr int kMaxCutPages = 4 * 256 * kNormVec;
+constexpr int kMaxCutPages = 4 * kNormThreads * kNormVec;
 template <bool ADD, int NV>
-__global__ __launch_bounds__(256) void rmsnorm_vec_kernel(float* __restrict__ x, Slices rs,
-                                                          const uint16_t* __restrict__ w,
-                                                          int d, float eps,
-                                                          uint16_t* __restrict__ y) {
-  __shared__ float part[4];
+__global__ __launch_bounds__(kNormThreads) void rmsnorm_vec_kernel(
+    float* __restrict__ x, Slices rs, const uint16_t* __restrict__ w, int d, float eps,
+    uint16_t* __restrict__ y) {
+  constexpr int NT = kNormThreads;
+  __shared__ float part[NT / 64];
   const int n4 = d / 4;
   float4* row = reinterpret_cast<float4*>(x + static_cast<int64_t>(blockIdx.x) * d);
   float4 v[NV];
 #pragma unroll
   for (int u = 0; u < NV; ++u) {
-    const int i = threadIdx.x + u * 256;
+    const int i = threadIdx.x + u * NT;
     v[u] = i < n4 ? row[i] : make_float4(0.f, 0.f, 0.f, 0.f);
   }
   if constexpr (ADD) {
@@ -169,11 +171,11 @@ __global__ __launch_bounds__(256) void rmsnorm_vec_kernel(float* __restrict__ x,
     if (S == 1) {
 #pragma unroll
       for (int u = 0; u < NV; ++u) {
-        const int i = threadIdx.x + u * 256;
+        const int i = threadIdx.x + u * NT;
         a[u] = i < n4 ? reinterpret_cast<const float4*>(r0)[i] : make_float4(0.f, 0.f, 0.f, 0.f);
       }
     } else {
-      const int nu = (n4 + 255) / 256;
+      const int nu = (n4 + NT - 1) / NT;
       const int64_t pages = (static_cast<int64_t>(d) * rs.K + kPageElems - 1) / kPageElems;
 #pragma unroll
       for (int u = 0; u < NV; ++u) a[u] = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -183,13 +185,13 @@ __global__ __launch_bounds__(256) void rmsnorm_vec_kernel(float* __restrict__ x,
         for (int u = 0; u < NV; ++u)
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
-            const int i = threadIdx.x + u * 256;
+            const int i = threadIdx.x + u * NT;
             t[u][j] = u < nu && s0 + j < S && i < n4
                           ? reinterpret_cast<const float4*>(r0 + (s0 + j) * stride)[i]
                           : make_float4(0.f, 0.f, 0.f, 0.f);
           }
         if (s0 == 0)
-          for (int q = threadIdx.x + 1; q < pages; q += 256) {
+          for (int q = threadIdx.x + 1; q < pages; q += NT) {
             const int64_t e = static_cast<int64_t>(q) * kPageElems;
             if (e % rs.K != 0) cutv[q] = slice_value(rs, blockIdx.x, e / rs.K);
           }
@@ -208,7 +210,7 @@ __global__ __launch_bounds__(256) void rmsnorm_vec_kernel(float* __restrict__ x,
       auto cut_value = [&](int64_t e) { return cutv[(e * rs.K + rs.K - 1) / kPageElems]; };
 #pragma unroll
       for (int u = 0; u < NV; ++u) {
-        const int i = threadIdx.x + u * 256;
+        const int i = threadIdx.x + u * NT;
         if (u < nu && i < n4) {
           const int64_t e = 4 * static_cast<int64_t>(i);
           if (cut_row(e, rs.K)) a[u].x = cut_value(e);
@@ -220,7 +222,7 @@ __global__ __launch_bounds__(256) void rmsnorm_vec_kernel(float* __restrict__ x,
     }
 #pragma unroll
     for (int u = 0; u < NV; ++u) {
-      const int i = threadIdx.x + u * 256;
+      const int i = threadIdx.x + u * NT;
       if (i < n4) {
         v[u].x += a[u].x;
         v[u].y += a[u].y;
@@ -242,13 +244,15 @@ __global__ __launch_bounds__(256) void rmsnorm_vec_kernel(float* __restrict__ x,
   for (int m = 32; m >= 1; m >>= 1) s += __shfl_xor(s, m, 64);
   if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = s;
   __syncthreads();
-  const float tot = ((part[0] + part[1]) + part[2]) + part[3];
+  float tot = part[0];  // the wavefronts' sums in wavefront order
+#pragma unroll
+  for (int i = 1; i < NT / 64; ++i) tot += part[i];
   const float scale = 1.0f / sqrtf(tot / static_cast<float>(d) + eps);
   const uint2* w4 = reinterpret_cast<const uint2*>(w);
   uint2* out = reinterpret_cast<uint2*>(y + static_cast<int64_t>(blockIdx.x) * d);
 #pragma unroll
   for (int u = 0; u < NV; ++u) {
-    const int i = threadIdx.x + u * 256;
+    const int i = threadIdx.x + u * NT;
     if (i >= n4) break;
     const uint2 ww = w4[i];
     const float w0 = __uint_as_float(ww.x << 16), w1 = __uint_as_float(ww.x & 0xffff0000u);
@@ -454,7 +458,7 @@ int launch_rmsnorm(boost_ctx* ctx, float* x, const float* r, int S, int K, const
   if (!ctx || !x || !w || !out) return fail(BOOST_EINVAL, "null argument");
   if (ctx->device < 0) return fail(BOOST_ENODEV, "plan-only context");
   if (B < 1 || d < 1 || !(eps >= 0.f)) return fail(BOOST_EINVAL, "B=%d d=%d eps=%g", B, d, eps);
-  const bool vec = d % 4 == 0 && d <= 4 * 256 * kNormVec &&
+  const bool vec = d % 4 == 0 && d <= 4 * kNormThreads * kNormVec &&
                    (reinterpret_cast<uintptr_t>(x) & 15) == 0 &&
                    (reinterpret_cast<uintptr_t>(r) & 15) == 0 &&
                    (reinterpret_cast<uintptr_t>(w) & 7) == 0 &&
@@ -464,19 +468,16 @@ int launch_rmsnorm(boost_ctx* ctx, float* x, const float* r, int S, int K, const
   auto op = static_cast<uint16_t*>(out);
   // K = 0: no row of the producing matrix crosses a page
   const Slices rs{r, S, B, d, kPageElems % K ? K : 0};
-  const bool nv4 = d <= 4 * 256 * 4;  // four float4s per lane cover the row
-  if (vec && r && nv4)
-    hipLaunchKernelGGL((rmsnorm_vec_kernel<true, 4>), dim3(B), dim3(256), 0, s, x, rs, wp, d, eps,
-                       op);
+  const bool nv1 = d <= 4 * kNormThreads;  // one float4 per lane covers the row
+  const dim3 g(B), t(kNormThreads);
+  if (vec && r && nv1)
+    hipLaunchKernelGGL((rmsnorm_vec_kernel<true, 1>), g, t, 0, s, x, rs, wp, d, eps, op);
   else if (vec && r)
-    hipLaunchKernelGGL((rmsnorm_vec_kernel<true, kNormVec>), dim3(B), dim3(256), 0, s, x, rs, wp,
-                       d, eps, op);
-  else if (vec && nv4)
-    hipLaunchKernelGGL((rmsnorm_vec_kernel<false, 4>), dim3(B), dim3(256), 0, s, x, rs, wp, d, eps,
-                       op);
+    hipLaunchKernelGGL((rmsnorm_vec_kernel<true, kNormVec>), g, t, 0, s, x, rs, wp, d, eps, op);
+  else if (vec && nv1)
+    hipLaunchKernelGGL((rmsnorm_vec_kernel<false, 1>), g, t, 0, s, x, rs, wp, d, eps, op);
   else if (vec)
-    hipLaunchKernelGGL((rmsnorm_vec_kernel<false, kNormVec>), dim3(B), dim3(256), 0, s, x, rs, wp,
-                       d, eps, op);
+    hipLaunchKernelGGL((rmsnorm_vec_kernel<false, kNormVec>), g, t, 0, s, x, rs, wp, d, eps, op);
   else if (r)
     hipLaunchKernelGGL(rmsnorm_kernel<true>, dim3(B), dim3(256), 0, s, x, rs, wp, d, eps, op);
   else
