@@ -63,8 +63,8 @@ struct GemvParams {
   int S;     // K slices per row group (matrix-core path; 1 = no split)
   float* ws;  // S > 1: [S][B][N] partials, then [(n_pages + 1) * 2][S][B] of cut rows
   float* partial;  // [(n_pages + 1) boundaries][2 sides][kMaxGemvBatch]
-  // host side only: a caller's buffer for the K slices ([S][B][N] partial
-  // sums, summed by the consumer instead of split_reduce) and its size
+  // host side only: a caller's buffer for the K slices (the layout of ws,
+  // summed by the consumer instead of split_reduce) and its size in floats
   float* slices;
   int64_t slice_floats;
 };
@@ -1319,7 +1319,7 @@ int dispatch(GemvParams& P, const boost_tensor* W, int K, int B, const boost_ctx
              hipStream_t s);
 
 // The decode GEMV behind both entry points: y, or with `slices` the split-K
-// partial sums [S][B][N] in fp32 (S reported through n_slices).
+// partial sums in fp32 in the layout of ws (S reported through n_slices).
 int decode_gemv(boost_ctx* ctx, const boost_tensor* W, int N, int K, const void* x, int B,
                 void* y, int y_dtype, float* slices, int64_t slice_floats, int* n_slices,
                 void* stream) {
