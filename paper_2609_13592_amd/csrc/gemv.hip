@@ -961,12 +961,18 @@ __global__ __launch_bounds__(64 * NW) void gemm_dma_kernel(GemvParams P) {
 }
 
 // Wavefronts per workgroup of the direct-to-LDS GEMM: eight (two per SIMD,
-// sharing the one ring of the workgroup) from BOOST_GEMM_NW8_BT batch tiles.
-// At 16 batch tiles (B = 129..256) eight took the 8B matrices 3-12 % faster
-// (B = 256: gate_up 110 -> 102 us, down 92 -> 81 us); at 4 tiles they were
+// sharing the one ring of the workgroup) from BOOST_GEMM_NW8_BT batch tiles,
+// and for 128-row units from BOOST_GEMM_NW8_RT2_BT.  At 16 batch tiles
+// (B = 129..256) eight took the 8B matrices 3-12 % faster (B = 256: gate_up
+// 110 -> 102 us, down 92 -> 81 us); at 8 tiles (B = 113..128) they took the
+// 128-row units of gate_up and down 5-8 % faster (69 -> 65 us, 55 -> 50 us)
+// and did nothing for the 64-row units of qkv and o; at 4 tiles they were
 // -10..+5 %.
 #ifndef BOOST_GEMM_NW8_BT
 #define BOOST_GEMM_NW8_BT 16
+#endif
+#ifndef BOOST_GEMM_NW8_RT2_BT
+#define BOOST_GEMM_NW8_RT2_BT 8
 #endif
 
 // y of a split-K call: the S slice partials of every (batch row, row) in
@@ -1231,7 +1237,7 @@ int launch_gemm_shape(GemvParams& P, int n_pages, bool need_fixup, const boost_c
     grid = P.host_workers + static_cast<int64_t>(P.n_hbm_pages) * P.units_per_page;
   }
   if (grid > 0x7fffffff) return bst::fail(BOOST_EINVAL, "grid too large");
-  if constexpr (BT >= BOOST_GEMM_NW8_BT && BT % 4 == 0)
+  if constexpr ((BT >= BOOST_GEMM_NW8_BT || (BT >= BOOST_GEMM_NW8_RT2_BT && RT == 2)) && BT % 4 == 0)
     hipLaunchKernelGGL((gemm_dma_kernel<BT, RT, 8>), dim3(static_cast<unsigned>(grid)),
                        dim3(8 * 64), 0, s, P);
   else
