@@ -964,15 +964,15 @@ __global__ __launch_bounds__(64 * NW) void gemm_dma_kernel(GemvParams P) {
 // sharing the one ring of the workgroup) from BOOST_GEMM_NW8_BT batch tiles,
 // and for 128-row units from BOOST_GEMM_NW8_RT2_BT.  At 16 batch tiles
 // (B = 129..256) eight took the 8B matrices 3-12 % faster (B = 256: gate_up
-// 110 -> 102 us, down 92 -> 81 us); at 8 tiles (B = 113..128) they took the
-// 128-row units of gate_up and down 5-8 % faster (69 -> 65 us, 55 -> 50 us)
-// and did nothing for the 64-row units of qkv and o; at 4 tiles they were
-// -10..+5 %.
+// 110 -> 102 us, down 92 -> 81 us); at 4 and 8 tiles (B = 49..64, 113..128)
+// they took the 128-row units 5-8 % faster (down 39 -> 37 us at B = 64;
+// gate_up 69 -> 65 us, down 55 -> 50 us at B = 128) while the 64-row units
+// of qkv and o were -10..+5 % (kept at four).
 #ifndef BOOST_GEMM_NW8_BT
 #define BOOST_GEMM_NW8_BT 16
 #endif
 #ifndef BOOST_GEMM_NW8_RT2_BT
-#define BOOST_GEMM_NW8_RT2_BT 8
+#define BOOST_GEMM_NW8_RT2_BT 4
 #endif
 
 // y of a split-K call: the S slice partials of every (batch row, row) in
