@@ -519,33 +519,34 @@ __device__ void mfma_unit(const GemvParams& P, int page, int unit, float* lds) {
   const int64_t k_end = min(s_end, k_beg + kper);
 
   if constexpr (WL) {
-    static_assert(RT == 1, "LDS-staged weights take one row tile");
+    static_assert(RT <= 2, "LDS-staged weights take one or two row tiles");
+    constexpr int kLd = 8 * RT;  // load instructions per chunk (two rows each)
     uint4* tile = reinterpret_cast<uint4*>(lds + mfma_lds_floats<BT, RT>()) +
-                  wave * (kWlTileFloats / 4);
+                  wave * (RT * kWlTileFloats / 4);
     // load instruction i: rows 2i and 2i+1 (lanes 0-31 / 32-63), 16 bytes
     // each; a row begun on the previous page gets a wrapped (huge) offset,
     // so its columns before the page read as zero
-    uint32_t lo[8];
+    uint32_t lo[kLd];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
+    for (int i = 0; i < kLd; ++i) {
       const int64_t r = rbase + 2 * i + (lane >> 5);
       lo[i] = r > r_hi ? kOOB : static_cast<uint32_t>((r * K - pe0) * 2);
     }
     const int wr_chunk = lane & 31;
-    uint4 wv[8];
+    uint4 wv[kLd];
     auto load_chunk = [&](int64_t kb) {
       const int64_t kc = kb + 8 * wr_chunk;
       const uint32_t oob = kc < k_end ? 0u : kOOB;
       const uint32_t kc2 = static_cast<uint32_t>(kc * 2);
 #pragma unroll
-      for (int i = 0; i < 8; ++i) wv[i] = load16<BOOST_MFMA_W_AUX>(wr, (lo[i] + kc2) | oob);
+      for (int i = 0; i < kLd; ++i) wv[i] = load16<BOOST_MFMA_W_AUX>(wr, (lo[i] + kc2) | oob);
     };
     if (k_beg < k_end) load_chunk(k_beg);
     constexpr int kChunkSteps = kWlCols / kStep;
 #pragma unroll 1
     for (int64_t kb = k_beg; kb < k_end; kb += kWlCols) {
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
+      for (int i = 0; i < kLd; ++i) {
         const int rr = 2 * i + (lane >> 5);
         tile[rr * 32 + (wr_chunk ^ (rr & 15))] = wv[i];
       }
@@ -563,13 +564,15 @@ __device__ void mfma_unit(const GemvParams& P, int page, int unit, float* lds) {
       load_chunk(kb + kWlCols);
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int st = 0; st < kChunkSteps; ++st) {
-        const uint4 a = tile[lrow * 32 + ((4 * st + lgrp) ^ lrow)];
+      for (int st = 0; st < kChunkSteps; ++st)
 #pragma unroll
-        for (int t = 0; t < BT; ++t)
-          acc[0][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-              as_bf16x8(a), as_bf16x8(xv[st][t]), acc[0][t], 0, 0, 0);
-      }
+        for (int ra = 0; ra < RT; ++ra) {
+          const uint4 a = tile[(16 * ra + lrow) * 32 + ((4 * st + lgrp) ^ lrow)];
+#pragma unroll
+          for (int t = 0; t < BT; ++t)
+            acc[ra][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                as_bf16x8(a), as_bf16x8(xv[st][t]), acc[ra][t], 0, 0, 0);
+        }
     }
   } else {
     // byte offset of column 0 of this lane's row in every row tile (wrapped
@@ -672,7 +675,7 @@ __device__ void mfma_unit(const GemvParams& P, int page, int unit, float* lds) {
 
 template <int BT, int RT, int UN, bool WL>
 __global__ __launch_bounds__(kThreads) void mfma_kernel(GemvParams P) {
-  __shared__ float lds[mfma_lds_floats<BT, RT>() + (WL ? kWaves * kWlTileFloats : 0)];
+  __shared__ float lds[mfma_lds_floats<BT, RT>() + (WL ? kWaves * RT * kWlTileFloats : 0)];
   const int bid = blockIdx.x;
   const int U = P.units_per_page;
   if (P.address_order) {
@@ -1284,6 +1287,12 @@ int launch_mfma(GemvParams& P, int n_pages, bool need_fixup, const boost_ctx* ct
   if constexpr (BT >= BOOST_GEMM_MIN_BT) {
     return launch_gemm<BT>(P, n_pages, need_fixup, ctx, s);
   } else if constexpr (BT <= 2) {
+    // two row tiles share each x fragment above 8 batch rows on matrices of
+    // at least 2^25 elements (8B at B = 12..16: gate_up 54.5 -> 50.4 us,
+    // down 42.0 -> 36.6 us); smaller matrices need the workgroups of one
+    // (qkv, o: 19-27 % slower with two), and at B = 7..8 the two are even
+    if (P.B > 8 && static_cast<int64_t>(P.N) * P.K >= (int64_t{1} << 25))
+      return launch_mfma_shape<BT, 2, 1, true>(P, n_pages, need_fixup, ctx, s);
     return launch_mfma_shape<BT, 1, 1, true>(P, n_pages, need_fixup, ctx, s);
   } else if constexpr (BT <= 8) {
     // workgroups with 64-row units: pages x units per page (a page meets at

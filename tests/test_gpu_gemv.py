@@ -158,19 +158,23 @@ def test_placement_invariance_and_parity(gpu_ctx, N, K, B):
         assert np.array_equal(y.view(np.uint32), outs[0].view(np.uint32))
 
 
-@pytest.mark.parametrize("N,K,B", [(300, 14336, 7), (5000, 520, 16), (257, 4104, 20),
+@pytest.mark.parametrize("N,K,B", [(300, 14336, 7), (5000, 520, 16), (2400, 14336, 12),
+                                   (257, 4104, 20),
                                    (257, 4104, 33), (77, 28672, 64), (300, 14336, 64),
                                    (1000, 8, 100), (600, 4096, 128), (300, 14336, 128),
                                    (130, 14336, 256), (40, 56, 200)])
 def test_mfma_placement_invariance_and_parity(gpu_ctx, N, K, B):
     """Batches from 7 up run on the matrix cores: bitwise-equal y under every
     map and schedule, every result within the bar of the oracle (ragged
-    batch tiles, rows cut by page boundaries, pages of both tiers).  From
-    B = 17 the GEMM covers 2, 4, 8 and 16 batch tiles with 64-row units
-    (B = 20, 33, 64, 100, 128, 200) and 128-row units (K = 14336 at B = 64,
-    128 and 256, on eight wavefronts), each with its own wavefront grid, and the host pages of the
-    "host", "alt" and "mpp3" maps run as 16-row sub-units: the bitwise
-    comparison across maps checks that they sum in the same order."""
+    batch tiles, rows cut by page boundaries, pages of both tiers).  Up to
+    B = 16 one batch tile with weights staged through LDS, in one row tile
+    or (B = 12 on a matrix of 2^25 elements) two.  From B = 17 the GEMM
+    covers 2, 4, 8 and 16 batch tiles with 64-row units (B = 20, 33, 64,
+    100, 128, 200) and 128-row units (K = 14336 at B = 64, 128 and 256, on
+    eight wavefronts), each with its own wavefront grid, and the host pages
+    of the "host", "alt" and "mpp3" maps run as 16-row sub-units: the
+    bitwise comparison across maps checks that they sum in the same
+    order."""
     w, x = synth.gemv_inputs(17 + N + K + B, N, K, B)
     n = opl.n_pages(w.nbytes)
     maps = {"hbm": np.zeros(n, np.uint8), "host": np.ones(n, np.uint8),
