@@ -1581,20 +1581,25 @@ def placements_bench(args, bd, ctx, torch, bw_hbm, bw_host, alpha, M):
         for h, N, K in ops[name]:
             bd.boost_decode_gemv(ctx, h, N, K, xs[K], 1, ys[N], bd.DTYPE_F32, sp)
     res = {}
-    for sched in ("cap", "address"):
-        bd.boost_gemv_set_schedule(ctx, bd.SCHED_CAP if sched == "cap" else bd.SCHED_ADDRESS,
-                                   args.host_workers)
+    scheds = {"cap": bd.SCHED_CAP, "address": bd.SCHED_ADDRESS}
+    for sc in scheds.values():
+        bd.boost_gemv_set_schedule(ctx, sc, args.host_workers)
         for name in kinds:
             step(name)
-        torch.cuda.synchronize()
-        ms = {k: [] for k in kinds}
-        for _ in range(max(5, args.steps // 2)):
+    torch.cuda.synchronize()
+    # every (schedule, placement) pair once per round, the schedules' order
+    # alternating from round to round, so that a drift of the box over the
+    # run (clocks, temperature) falls on all of them alike
+    ms = {(name, sc): [] for name in kinds for sc in scheds}
+    for r in range(max(5, args.steps // 2)):
+        for sched in (("cap", "address") if r % 2 == 0 else ("address", "cap")):
+            bd.boost_gemv_set_schedule(ctx, scheds[sched], args.host_workers)
             for name in kinds:
-                ms[name].append(time_steps(torch, lambda: step(name), 1)[0])
-        for name in kinds:
-            t = float(np.median(ms[name]))
-            res.setdefault(name, {})[sched] = {"ms_per_step": round(t, 4),
-                                               "gbps": round(alg / (t * 1e-3) / 1e9, 1)}
+                ms[(name, sched)].append(time_steps(torch, lambda: step(name), 1)[0])
+    for (name, sched), v in ms.items():
+        t = float(np.median(v))
+        res.setdefault(name, {})[sched] = {"ms_per_step": round(t, 4),
+                                           "gbps": round(alg / (t * 1e-3) / 1e9, 1)}
     bd.boost_gemv_set_schedule(ctx, bd.SCHED_CAP, args.host_workers)
     # one grid wave of the batch-1 GEMV covers about 2048 workgroups x 32 KiB
     wave_pages = 32
