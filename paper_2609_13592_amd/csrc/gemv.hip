@@ -1037,12 +1037,14 @@ __global__ __launch_bounds__(256) void split_reduce(GemvParams P) {
 // the L1 cache (counters: as many L2 requests for x as for the weights) and
 // would be fetched from L2 once per row; two rows per wavefront reuse one x
 // slice from registers (8B down projection 22.2 -> 21.2 us, 70B 44.0 ->
-// 42.1 us; with a row over two wavefronts it did not pay).
+// 42.1 us; with a row over two wavefronts it did not pay), with eight load
+// steps in flight per row (four: 21.8 us, eight: 21.4, sixteen: 30.4 at
+// half the occupancy).
 #ifndef BOOST_GEMV_RW1_LONG
 #define BOOST_GEMV_RW1_LONG 2
 #endif
 #ifndef BOOST_GEMV_UN1_LONG
-#define BOOST_GEMV_UN1_LONG 4
+#define BOOST_GEMV_UN1_LONG 8
 #endif
 #ifndef BOOST_GEMV_RW1
 #define BOOST_GEMV_RW1 1
