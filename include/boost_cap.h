@@ -108,7 +108,10 @@ int boost_host_numa_info(const boost_ctx *ctx, int *device_node, int *n_nodes,
  * reads a device buffer of `hbm_bytes` and a pinned, device-mapped host buffer
  * of `host_bytes` (both allocated and freed inside the call, so this call
  * synchronises and must not be captured), `iters` timed passes each after one
- * warm-up pass; the best grid of a small sweep is kept for each tier.
+ * warm-up pass; the best of a small sweep is kept for each tier (HBM: static
+ * slices over 4..32 workgroups per compute unit, and persistent workers, one
+ * per compute unit, dealt 256 KiB chunks round robin; host: 16..1024
+ * workgroups).
  * Outputs (any may be NULL): GB/s (1e9 B/s) of each tier and alpha.
  * Errors: EINVAL (sizes < 64 MiB, iters < 1), ENODEV, ENOMEM, EHIP. */
 int boost_calibrate(boost_ctx *ctx, uint64_t hbm_bytes, uint64_t host_bytes,
@@ -142,7 +145,10 @@ typedef struct boost_cap_point {
   int32_t chunk_static; /* with hbm_chunk_kib > 0: 0 every chunk from the
                            queue; 1 the chunks dealt to the persistent workers
                            round robin, no queue; 2 each worker's first chunk
-                           is its own index, the rest from the queue */
+                           is its own index, the rest from the queue; 3 as 1,
+                           with every workgroup holding 96 KiB of LDS so that
+                           no two share a compute unit (host depth 8,
+                           non-temporal host loads, no DMA) */
 } boost_cap_point;
 
 /* Concurrent two-tier streaming probe (the bound §3 "CAP" measures with a

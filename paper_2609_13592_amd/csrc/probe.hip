@@ -74,8 +74,12 @@ __global__ __launch_bounds__(kThreads) void stream_read(const char* __restrict__
 // flight and cache policy HAUX, and the others split the HBM buffer as
 // stream_read does.  Thread 0 of every workgroup stores the constant-rate
 // clock at its start and after its last load returned, so the host can tell
-// when each tier's workgroups finished inside the one launch.
-template <int HD, int HAUX>
+// when each tier's workgroups finished inside the one launch.  With EXCL the
+// kernel holds more than half of a compute unit's LDS, so no two of its
+// workgroups share a compute unit: the host workgroups' long-latency loads
+// then never occupy the vector L1 of a CU that streams HBM.
+constexpr int kExclLdsWords = 24 * 1024;  // 96 KiB of the CU's 160 KiB
+template <int HD, int HAUX, bool EXCL>
 __global__ __launch_bounds__(kThreads) void cap_stream(const char* __restrict__ hbm,
                                                        uint64_t hbm_vec,
                                                        const char* __restrict__ host,
@@ -96,7 +100,7 @@ __global__ __launch_bounds__(kThreads) void cap_stream(const char* __restrict__ 
     acc = stream_slice<HD, HAUX>(host, host_vec, bid / host_stride, host_wgs);
   } else if (chunk_vec == 0) {
     acc = stream_slice(hbm, hbm_vec, bid - hosts_before, static_cast<int>(gridDim.x) - host_wgs);
-  } else if (chunk_static == 1) {
+  } else if (chunk_static == 1 || chunk_static == 3) {
     // persistent HBM workers, chunks dealt round robin (no queue)
     const uint64_t n_chunks = (hbm_vec + chunk_vec - 1) / chunk_vec;
     const uint64_t workers = static_cast<uint64_t>(gridDim.x) - host_wgs;
@@ -150,7 +154,14 @@ __global__ __launch_bounds__(kThreads) void cap_stream(const char* __restrict__ 
     // the XCD this workgroup ran on (hardware register XCC_ID, bits 3:0)
     clocks[3 * bid + 2] = __builtin_amdgcn_s_getreg((3 << 11) | 20) & 0xf;
   }
-  if (acc == 0x9e3779b9u) sink[bid] = acc;
+  if constexpr (EXCL) {
+    __shared__ uint32_t pad[kExclLdsWords];
+    if (acc == 0x9e3779b9u) pad[threadIdx.x] = acc;
+    __syncthreads();
+    if (acc == 0x9e3779b9u) sink[bid] = pad[threadIdx.x ^ 1];
+  } else if (acc == 0x9e3779b9u) {
+    sink[bid] = acc;
+  }
 }
 
 typedef void (*CapKernel)(const char*, uint64_t, const char*, uint64_t, int, int, uint32_t,
@@ -162,12 +173,14 @@ typedef void (*CapKernel)(const char*, uint64_t, const char*, uint64_t, int, int
 template <int HD>
 CapKernel cap_kernel_for_policy(int policy) {
   switch (policy) {
-    case 0: return cap_stream<HD, 2>;
-    case 1: return cap_stream<HD, 0>;
-    default: return cap_stream<HD, 17>;
+    case 0: return cap_stream<HD, 2, false>;
+    case 1: return cap_stream<HD, 0, false>;
+    default: return cap_stream<HD, 17, false>;
   }
 }
-CapKernel cap_kernel(int depth, int policy) {
+// exclusive compute units: depth 8, non-temporal host loads only
+CapKernel cap_kernel(int depth, int policy, bool excl) {
+  if (excl) return cap_stream<8, 2, true>;
   switch (depth) {
     case 1: return cap_kernel_for_policy<1>(policy);
     case 2: return cap_kernel_for_policy<2>(policy);
@@ -191,6 +204,36 @@ int measure(const void* src, uint64_t bytes, int grid, int iters, uint32_t* sink
   for (int it = 0; it < iters; ++it)
     hipLaunchKernelGGL(stream_read, dim3(grid), dim3(kThreads), 0, 0,
                        static_cast<const char*>(src), n_vec, sink);
+  BOOST_HIP(hipGetLastError());
+  BOOST_HIP(hipEventRecord(b, 0));
+  BOOST_HIP(hipEventSynchronize(b));
+  float ms = 0;
+  BOOST_HIP(hipEventElapsedTime(&ms, a, b));
+  (void)hipEventDestroy(a);
+  (void)hipEventDestroy(b);
+  *gbps = static_cast<double>(bytes) * iters / (ms * 1e-3) / 1e9;
+  return BOOST_OK;
+}
+
+// Read bandwidth of persistent workers, one per compute unit, dealt chunks
+// of 256 KiB round robin (`cap_stream` with no host workgroups): the fastest
+// HBM stream of the layouts the concurrent probe measures.  clocks holds
+// 3 * grid entries, sink grid entries.
+int measure_round_robin(const void* src, uint64_t bytes, int grid, int iters, uint64_t* clocks,
+                        uint32_t* sink, double* gbps) {
+  hipEvent_t a, b;
+  BOOST_HIP(hipEventCreate(&a));
+  BOOST_HIP(hipEventCreate(&b));
+  const uint32_t chunk_vec = 256u * 64u;  // 256 KiB in 16-byte vectors
+  auto launch = [&]() {
+    hipLaunchKernelGGL((cap_stream<8, 2, true>), dim3(grid), dim3(kThreads), 0, 0,
+                       static_cast<const char*>(src), bytes / 16, nullptr, uint64_t{0}, 0, 1,
+                       chunk_vec, 3, nullptr, clocks, sink);
+  };
+  launch();
+  BOOST_HIP(hipGetLastError());
+  BOOST_HIP(hipEventRecord(a, 0));
+  for (int it = 0; it < iters; ++it) launch();
   BOOST_HIP(hipGetLastError());
   BOOST_HIP(hipEventRecord(b, 0));
   BOOST_HIP(hipEventSynchronize(b));
@@ -247,8 +290,12 @@ int boost_cap_sweep(boost_ctx* ctx, uint64_t hbm_bytes, uint64_t host_bytes, int
     if (p.host_policy < 0 || p.host_policy > 2 || p.dma < 0 || p.dma > 1)
       return fail(BOOST_EINVAL, "point %d: policy %d dma %d", i, p.host_policy, p.dma);
     if (p.hbm_chunk_kib < 0 || p.hbm_chunk_kib > (1 << 20) || p.hbm_chunk_kib % 4 ||
-        p.chunk_static < 0 || p.chunk_static > 2)
-      return fail(BOOST_EINVAL, "point %d: HBM chunk %d KiB", i, p.hbm_chunk_kib);
+        p.chunk_static < 0 || p.chunk_static > 3 || (p.chunk_static && !p.hbm_chunk_kib))
+      return fail(BOOST_EINVAL, "point %d: HBM chunk %d KiB, mode %d", i, p.hbm_chunk_kib,
+                  p.chunk_static);
+    if (p.chunk_static == 3 && (p.host_depth != 8 || p.host_policy != 0 || p.dma))
+      return fail(BOOST_EINVAL, "point %d: exclusive compute units take host depth 8, "
+                  "non-temporal host loads and no DMA", i);
     if (p.dma && p.host_wgs)
       return fail(BOOST_EINVAL, "point %d: DMA points read the host bytes by copy, not "
                   "by workgroups", i);
@@ -297,7 +344,7 @@ int boost_cap_sweep(boost_ctx* ctx, uint64_t hbm_bytes, uint64_t host_bytes, int
   for (int i = 0; i < n_points && !rc; ++i) {
     const boost_cap_point& p = pts[i];
     const int grid = p.hbm_wgs + p.host_wgs;
-    const CapKernel kern = cap_kernel(p.host_depth, p.host_policy);
+    const CapKernel kern = cap_kernel(p.host_depth, p.host_policy, p.chunk_static == 3);
     const uint32_t chunk_vec = static_cast<uint32_t>(p.hbm_chunk_kib) * 64u;  // 16 B vectors
     // the queue starts empty for every launch (plain stream order, no graph),
     // cleared before the launch's first event
@@ -419,7 +466,9 @@ int boost_calibrate(boost_ctx* ctx, uint64_t hbm_bytes, uint64_t host_bytes, int
   if (!rc) rc = slab_alloc(ctx, (host_bytes + kPage - 1) / kPage, true, host);
   double best_d = 0, best_h = 0;
   uint32_t* sink = nullptr;
-  if (!rc && hipMalloc(&sink, 1 << 20) != hipSuccess)
+  uint64_t* clocks = nullptr;
+  if (!rc && (hipMalloc(&sink, 1 << 20) != hipSuccess ||
+              hipMalloc(&clocks, static_cast<size_t>(ctx->n_cu) * 24) != hipSuccess))
     rc = fail(BOOST_ENOMEM, "sink allocation failed");
   if (!rc && hipMemset(dev.base, 0x5a, hbm_bytes) != hipSuccess)
     rc = fail(BOOST_EHIP, "memset failed");
@@ -431,6 +480,12 @@ int boost_calibrate(boost_ctx* ctx, uint64_t hbm_bytes, uint64_t host_bytes, int
     rc = measure(dev.base, hbm_bytes, ctx->n_cu * mult, iters, sink, &g);
     best_d = std::max(best_d, g);
   }
+  // and one persistent worker per compute unit
+  if (!rc) {
+    double g = 0;
+    rc = measure_round_robin(dev.base, hbm_bytes, ctx->n_cu, iters, clocks, sink, &g);
+    best_d = std::max(best_d, g);
+  }
   // host link: from a handful of workgroups up to one per CU and beyond
   for (int grid : {16, 64, 256, 1024}) {
     if (rc) break;
@@ -439,6 +494,7 @@ int boost_calibrate(boost_ctx* ctx, uint64_t hbm_bytes, uint64_t host_bytes, int
     best_h = std::max(best_h, g);
   }
   (void)hipFree(sink);
+  (void)hipFree(clocks);
   slab_free(dev);
   slab_free(host);
   if (rc) return rc;

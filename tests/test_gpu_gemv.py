@@ -70,10 +70,14 @@ def test_cap_probe_points(gpu_ctx):
            dict(hbm_bytes=T, hbm_wgs=3000, hbm_chunk_kib=64),
            dict(hbm_bytes=T - 16, hbm_wgs=1000, hbm_chunk_kib=256, chunk_static=1),
            dict(hbm_bytes=T - 16, hbm_wgs=1000, host_bytes=4 << 20, host_wgs=8,
-                hbm_chunk_kib=256, chunk_static=2)]
+                hbm_chunk_kib=256, chunk_static=2),
+           dict(hbm_bytes=T - (4 << 20) - 16, hbm_wgs=240, host_bytes=4 << 20, host_wgs=16,
+                host_stride=8, hbm_chunk_kib=64, chunk_static=3)]
     r = bd.boost_cap_sweep(gpu_ctx, T, H, pts, 2)
-    assert r.shape == (9, 16)
+    assert r.shape == (10, 16)
     assert 500 < r[7, 2] < 9000 and 500 < r[8, 2] < 9000 and 1 < r[8, 3] < 200
+    # round robin on compute units of their own, host workgroups on one XCD
+    assert 500 < r[9, 2] < 9000 and 1 < r[9, 3] < 200
     # queue-fed HBM workers (a ragged last chunk; more workers than slots)
     assert 500 < r[5, 2] < 9000 and 1 < r[5, 3] < 200
     assert 500 < r[6, 2] < 9000
@@ -87,7 +91,9 @@ def test_cap_probe_points(gpu_ctx):
     assert r[4, 6] > 0 and 1 < r[4, 3] < 200
     for bad in (dict(hbm_bytes=T, hbm_wgs=16, host_depth=3),
                 dict(hbm_bytes=T, hbm_wgs=16, hbm_chunk_kib=6),
-                dict(hbm_bytes=T, hbm_wgs=16, hbm_chunk_kib=64, chunk_static=3),
+                dict(hbm_bytes=T, hbm_wgs=16, hbm_chunk_kib=64, chunk_static=4),
+                dict(hbm_bytes=T, hbm_wgs=16, chunk_static=1),
+                dict(hbm_bytes=T, hbm_wgs=16, hbm_chunk_kib=64, chunk_static=3, host_depth=2),
                 dict(hbm_bytes=T, hbm_wgs=16, host_bytes=H, host_wgs=1, dma=1),
                 dict(hbm_bytes=T + 16, hbm_wgs=16),
                 dict(hbm_bytes=T, hbm_wgs=4, host_bytes=H, host_wgs=2, host_stride=8),
