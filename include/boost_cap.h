@@ -110,8 +110,8 @@ int boost_host_numa_info(const boost_ctx *ctx, int *device_node, int *n_nodes,
  * synchronises and must not be captured), `iters` timed passes each after one
  * warm-up pass; the best of a small sweep is kept for each tier (HBM: static
  * slices over 4..32 workgroups per compute unit, and persistent workers, one
- * per compute unit, dealt 256 KiB chunks round robin; host: 16..1024
- * workgroups).
+ * per compute unit, dealt 256 KiB chunks round robin, swept before and after
+ * the host tier; host: 16..1024 workgroups).
  * Outputs (any may be NULL): GB/s (1e9 B/s) of each tier and alpha.
  * Errors: EINVAL (sizes < 64 MiB, iters < 1), ENODEV, ENOMEM, EHIP. */
 int boost_calibrate(boost_ctx *ctx, uint64_t hbm_bytes, uint64_t host_bytes,

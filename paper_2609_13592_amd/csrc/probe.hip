@@ -473,19 +473,22 @@ int boost_calibrate(boost_ctx* ctx, uint64_t hbm_bytes, uint64_t host_bytes, int
   if (!rc && hipMemset(dev.base, 0x5a, hbm_bytes) != hipSuccess)
     rc = fail(BOOST_EHIP, "memset failed");
   if (!rc) std::memset(host.host_base, 0x5a, host_bytes);
-  // HBM: grids of 4 to 32 workgroups per CU
-  for (int mult : {4, 8, 16, 32}) {
-    if (rc) break;
-    double g = 0;
-    rc = measure(dev.base, hbm_bytes, ctx->n_cu * mult, iters, sink, &g);
-    best_d = std::max(best_d, g);
-  }
-  // and one persistent worker per compute unit
-  if (!rc) {
+  // HBM: grids of 4 to 32 workgroups per CU, and one persistent worker per
+  // compute unit; run before and after the host sweep (the first GPU work of
+  // a process can stream slower), the best of both kept
+  auto hbm_sweep = [&]() {
+    for (int mult : {4, 8, 16, 32}) {
+      if (rc) return;
+      double g = 0;
+      rc = measure(dev.base, hbm_bytes, ctx->n_cu * mult, iters, sink, &g);
+      best_d = std::max(best_d, g);
+    }
+    if (rc) return;
     double g = 0;
     rc = measure_round_robin(dev.base, hbm_bytes, ctx->n_cu, iters, clocks, sink, &g);
     best_d = std::max(best_d, g);
-  }
+  };
+  hbm_sweep();
   // host link: from a handful of workgroups up to one per CU and beyond
   for (int grid : {16, 64, 256, 1024}) {
     if (rc) break;
@@ -493,6 +496,7 @@ int boost_calibrate(boost_ctx* ctx, uint64_t hbm_bytes, uint64_t host_bytes, int
     rc = measure(host.base, host_bytes, grid, iters, sink, &g);
     best_h = std::max(best_h, g);
   }
+  hbm_sweep();
   (void)hipFree(sink);
   (void)hipFree(clocks);
   slab_free(dev);
