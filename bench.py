@@ -1258,10 +1258,11 @@ def cap_probe(args, bd, ctx, torch, bw_hbm, bw_host, alpha, M_alpha):
                "alpha_share_queue_one_xcd_8wg": dict(hbm_bytes=T - hb, hbm_wgs=n_cu * 8 - 8,
                                                      host_bytes=hb, host_wgs=8, host_stride=8,
                                                      hbm_chunk_kib=256),
-               # one workgroup short of a CU each, so its grid differs from the next
+               # one and two workgroups short of a CU each, so that their grids
+               # differ from each other and from calibration's (one per CU)
                "hbm_only_one_per_cu": dict(hbm_bytes=T, hbm_wgs=n_cu - 1, hbm_chunk_kib=256,
                                            chunk_static=3),
-               "alpha_share_one_per_cu_spread_8wg": dict(hbm_bytes=T - hb, hbm_wgs=n_cu - 8,
+               "alpha_share_one_per_cu_spread_8wg": dict(hbm_bytes=T - hb, hbm_wgs=n_cu - 10,
                                                          host_bytes=hb, host_wgs=8,
                                                          hbm_chunk_kib=256, chunk_static=3)}
         res = bd.boost_cap_sweep(ctx, T, HOST, list(pts.values()), 3)
