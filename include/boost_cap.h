@@ -347,6 +347,10 @@ int boost_decode_gemv(boost_ctx *ctx, const boost_tensor *W, int N, int K,
  * S is chosen as boost_decode_gemv chooses it, halved until it is at most
  * max_slices; it depends only on the shapes, the placement and the context,
  * so it is known on the host when the call returns.
+ * It touches no workspace of the context: the partials live in `slices`, and
+ * with S == 1 the parts of rows cut between pages of different tiers are
+ * staged in a buffer of the tensor W, so calls on different streams may
+ * overlap unless they use the same W.
  * 1 <= max_slices <= BOOST_MAX_GEMV_SLICES.  Other arguments and errors as
  * boost_decode_gemv. */
 #define BOOST_MAX_GEMV_SLICES 8

@@ -428,6 +428,44 @@ def test_slices_sum_to_y(gpu_ctx, N, K, B, split):
         assert np.array_equal(y.view(np.uint32), ys[0].view(np.uint32))
 
 
+def test_slices_calls_on_two_streams(gpu_ctx):
+    """The slices entry point keeps its partials in the caller's buffer (the
+    context's split-K workspace is not touched), so calls on two streams may
+    overlap: two split shapes under MPP maps, each called five times on its
+    own stream with the other's calls interleaved, sum to the serial
+    boost_decode_gemv results bit for bit."""
+    import torch
+    B = 64
+    shapes = [(6144, 4096), (4096, 14336)]
+    size = max(bd.boost_gemv_slices_floats(N, K, B, bd.MAX_GEMV_SLICES) for N, K in shapes)
+    ts, xs, ys, bufs = [], [], [], []
+    try:
+        for i, (N, K) in enumerate(shapes):
+            w, x = synth.gemv_inputs(501 + i, N, K, B)
+            t = place(gpu_ctx, w, tiers=opl.mpp_tier_map(w.nbytes, 3))
+            ts.append(t)
+            xs.append(to_dev_u16(x))
+            ys.append(run_gemv(gpu_ctx, t, N, K, xs[-1], B))
+            bufs.append([dev_f32(size) for _ in range(5)])
+        torch.cuda.synchronize()
+        streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+        S = [[0] * 5, [0] * 5]
+        for r in range(5):
+            for i, (N, K) in enumerate(shapes):
+                S[i][r] = bd.boost_decode_gemv_slices(gpu_ctx, ts[i], N, K, xs[i], B, bufs[i][r],
+                                                      bd.MAX_GEMV_SLICES,
+                                                      streams[i].cuda_stream)
+        torch.cuda.synchronize()
+        for i, (N, K) in enumerate(shapes):
+            for r in range(5):
+                assert S[i][r] > 1, (N, K)
+                got = slices_sum(bufs[i][r].cpu().numpy(), S[i][r], B, N, K)
+                assert np.array_equal(got.view(np.uint32), ys[i].view(np.uint32)), (N, K, r)
+    finally:
+        for t in ts:
+            bd.boost_tensor_free(t)
+
+
 def test_slices_bad_arguments(gpu_ctx):
     """Slice caps outside [1, 8] and misaligned buffers are refused before
     anything runs."""
