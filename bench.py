@@ -1218,6 +1218,32 @@ def host_share_sweep(args, bd, ctx, torch, bw_hbm, bw_host, alpha, M_alpha):
             "hbm_only_us": round(t_hbm, 2), "best_M": best["M"], "sweep": out}
 
 
+def cap_measured_optimum(out):
+    """The measured-optimal host share of a CAP sweep `out` (its
+    `hbm_stream_modes` and `concurrent*` layouts, each with `hbm_only_us`,
+    `hbm_only_spread` and `points`).  Every point is also timed against the
+    fastest all-HBM launch of any layout (added to the points and to `out`):
+    host reads gain only if they beat the best way to stream HBM alone, by
+    more than the spread of their layout's all-HBM reference (at least
+    0.2 %).  Without a gain the optimum is "no host page" (share 0)."""
+    tags = [t for t in out if t.startswith("concurrent")]
+    fastest = min([v["us"] for v in out["hbm_stream_modes"].values()] +
+                  [out[t]["hbm_only_us"] for t in tags])
+    out["fastest_hbm_only_us"] = round(fastest, 2)
+    for t in tags:
+        for r in out[t]["points"]:
+            r["speedup_vs_fastest_hbm_only"] = round(fastest / r["us"], 4)
+    cands = [(tag, r) for tag in tags for r in out[tag]["points"]]
+    tag, best = max(cands, key=lambda c: c[1]["speedup_vs_fastest_hbm_only"])
+    noise = out[tag]["hbm_only_spread"]
+    gain = best["speedup_vs_fastest_hbm_only"] > 1.0 + max(noise, 0.002)
+    return {"host_share": best["host_share"] if gain else 0.0,
+            "host_workgroups": best["host_workgroups"] if gain else 0,
+            "speedup_vs_hbm_only": best["speedup_vs_fastest_hbm_only"] if gain else 1.0,
+            "best_host_point": dict(best, layout=tag), "reference_spread": noise,
+            "modulus": int(round(1 / best["host_share"])) if gain else None}
+
+
 def cap_probe(args, bd, ctx, torch, bw_hbm, bw_host, alpha, M_alpha):
     """The streaming-probe bound of concurrent access (§3 "CAP": the paper
     sweeps the host share of a streaming kernel whose workgroups read host
@@ -1422,26 +1448,7 @@ def cap_probe(args, bd, ctx, torch, bw_hbm, bw_host, alpha, M_alpha):
                     if r[3] > 0 else None}
                    for f, r, t_ref, h_ref in zip(shares, res, t_refs, h_refs)]}
 
-    tags = [t for t in out if t.startswith("concurrent")]
-    # every point against the fastest all-HBM launch of any layout: host
-    # reads gain only if they beat the best way to stream HBM alone
-    fastest = min([v["us"] for v in out["hbm_stream_modes"].values()] +
-                  [out[t]["hbm_only_us"] for t in tags])
-    out["fastest_hbm_only_us"] = round(fastest, 2)
-    for t in tags:
-        for r in out[t]["points"]:
-            r["speedup_vs_fastest_hbm_only"] = round(fastest / r["us"], 4)
-    cands = [(tag, r) for tag in tags for r in out[tag]["points"]]
-    tag, best = max(cands, key=lambda c: c[1]["speedup_vs_fastest_hbm_only"])
-    # a gain must clear the spread of the all-HBM reference of its layout
-    noise = out[tag]["hbm_only_spread"]
-    gain = best["speedup_vs_fastest_hbm_only"] > 1.0 + max(noise, 0.002)
-    out["measured_optimum"] = {
-        "host_share": best["host_share"] if gain else 0.0,
-        "host_workgroups": best["host_workgroups"] if gain else 0,
-        "speedup_vs_hbm_only": best["speedup_vs_fastest_hbm_only"] if gain else 1.0,
-        "best_host_point": dict(best, layout=tag), "reference_spread": noise,
-        "modulus": int(round(1 / best["host_share"])) if gain else None}
+    out["measured_optimum"] = cap_measured_optimum(out)
     return {"metric": "concurrent HBM + host streaming vs HBM alone (CAP bound)",
             "value": out["measured_optimum"]["speedup_vs_hbm_only"], "unit": "x",
             "n_gpus": 1, "higher_is_better": True, "dtype": "u8", "data": "synthetic",

@@ -142,3 +142,37 @@ def test_more_gpus_refused():
     r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 2 and "one GPU" in r.stderr
+
+
+def _cap_out(points_by_layout, modes):
+    out = {"hbm_stream_modes": {k: {"us": v} for k, v in modes.items()}}
+    for tag, (ref_us, spread, pts) in points_by_layout.items():
+        out[tag] = {"hbm_only_us": ref_us, "hbm_only_spread": spread,
+                    "points": [{"host_share": f, "host_workgroups": h, "us": us,
+                                "speedup_vs_hbm_only": round(ref_us / us, 4)}
+                               for f, h, us in pts]}
+    return out
+
+
+def test_cap_optimum_against_fastest_stream():
+    """A layout that beats its own slow all-HBM reference but not the fastest
+    all-HBM stream of another layout yields "no host page"; a point that beats
+    the fastest stream by more than its layout's spread is the optimum."""
+    modes = {"static": 316.0, "one_per_cu": 292.0}
+    out = _cap_out({"concurrent_queue": (348.0, 0.002, [(1 / 130, 16, 343.0)]),
+                    "concurrent_one_per_cu": (292.5, 0.003, [(1 / 1024, 8, 294.0)])}, modes)
+    opt = bench.cap_measured_optimum(out)
+    assert out["fastest_hbm_only_us"] == 292.0
+    assert opt["host_share"] == 0.0 and opt["modulus"] is None and opt["speedup_vs_hbm_only"] == 1.0
+    assert opt["best_host_point"]["layout"] == "concurrent_one_per_cu"
+    q = out["concurrent_queue"]["points"][0]
+    assert q["speedup_vs_hbm_only"] > 1.0 > q["speedup_vs_fastest_hbm_only"]
+    # a real gain over the fastest stream, above the 0.3 % spread
+    out = _cap_out({"concurrent_one_per_cu": (292.5, 0.003, [(1 / 130, 8, 289.0),
+                                                             (1 / 256, 8, 291.5)])}, modes)
+    opt = bench.cap_measured_optimum(out)
+    assert opt["host_share"] == 1 / 130 and opt["modulus"] == 130 and opt["host_workgroups"] == 8
+    assert opt["speedup_vs_hbm_only"] == round(292.0 / 289.0, 4)
+    # within the spread: no gain
+    out = _cap_out({"concurrent_one_per_cu": (292.5, 0.003, [(1 / 130, 8, 291.5)])}, modes)
+    assert bench.cap_measured_optimum(out)["host_share"] == 0.0
